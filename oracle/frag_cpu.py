@@ -1,0 +1,93 @@
+"""The fragment method on the CPU, in double precision.
+
+TEST INFRASTRUCTURE and the CPU "image-based" baseline: see the package
+docstring.  It follows Section 2.2 step by step and shares nothing with the GPU
+library:
+
+  - the image is one fragment holding the whole extended maps (Eqs. 1-2);
+  - a convolutional layer keeps the fragment count and convolves every
+    fragment's extended maps the way a patch is convolved, each size shrinking
+    by k - 1 (Eqs. 3-4);
+  - a k x k max-pooling layer turns every fragment into k^2 fragments, one per
+    offset (o_x, o_y) in {0..k-1}^2; the child's pixel (xbar, ybar) is the
+    maximum over o_x + k*xbar .. o_x + k*xbar + k - 1 (and the same in y) of
+    the parent (Eq. 5), and its size is div(s - o, k) per axis (Eqs. 6-7);
+    children of fragment f are numbered f*k^2 + o_y*k + o_x;
+  - fully connected layers act on every fragment as convolutions whose kernel
+    covers the whole patch-level map (Section 3: a fragment depends on one
+    fragment of the layer below, for fully connected layers too);
+  - the last layer's softmax is taken per pixel over the classes.
+
+Every fragment carries where its pixel (0, 0) lands in the output and the step
+between its neighbouring pixels: the input fragment starts at (0, 0) with step
+1; the child at offset o of a fragment with base b and step t gets base
+b + o*t and step t*k, since its window xbar starts at parent pixel o + k*xbar.
+A fragment pixel (y, x) at the end is the patch whose top-left corner is
+(base_y + step*y, base_x + step*x): a crop of a fragment's maps is one patch's
+maps (Section 3).
+"""
+import numpy as np
+
+
+def _conv(a, w, b, act):
+    """Valid cross-correlation of one fragment a [h, w, ci] with OIHW weights."""
+    co, ci, k, _ = w.shape
+    h, wd, _ = a.shape
+    ho, wo = max(h - k + 1, 0), max(wd - k + 1, 0)
+    out = np.empty((ho, wo, co), np.float64)
+    out[...] = b
+    if ho and wo:
+        for dy in range(k):
+            for dx in range(k):
+                out += a[dy:dy + ho, dx:dx + wo, :] @ w[:, :, dy, dx].T
+    if act == "tanh":
+        np.tanh(out, out=out)
+    return out
+
+
+def _pool_children(a, k):
+    """The k^2 children of fragment a [h, w, c] in offset order (o_y, o_x)."""
+    h, wd, c = a.shape
+    kids = []
+    for oy in range(k):
+        for ox in range(k):
+            hc, wc = max((h - oy) // k, 0), max((wd - ox) // k, 0)
+            m = np.full((hc, wc, c), -np.inf)
+            for i in range(k):
+                for j in range(k):
+                    y0, x0 = oy + i, ox + j
+                    m = np.maximum(m, a[y0:y0 + k * hc:k, x0:x0 + k * wc:k, :][:hc, :wc])
+            kids.append(((oy, ox), m))
+    return kids
+
+
+def frag_scan(layers, params, image, patch):
+    """Outputs of the net for every patch of every image, [B, H-w0+1, W-w0+1, n]."""
+    img = np.asarray(image, dtype=np.float64)
+    B, H, W, C = img.shape
+    ny, nx = H - patch + 1, W - patch + 1
+    n_out = layers[-1]["c_out"]
+    res = np.full((B, ny, nx, n_out), np.nan)
+    for b in range(B):
+        # (base_y, base_x, step, maps)
+        frags = [(0, 0, 1, img[b])]
+        for L, p in zip(layers, params):
+            if L["kind"] == "pool":
+                nxt = []
+                for (by, bx, t, a) in frags:
+                    for (oy, ox), m in _pool_children(a, L["k"]):
+                        nxt.append((by + oy * t, bx + ox * t, t * L["k"], m))
+                frags = nxt
+            else:
+                w = np.asarray(p[0], np.float64)
+                bias = np.asarray(p[1], np.float64)
+                frags = [(by, bx, t, _conv(a, w, bias, L["act"])) for (by, bx, t, a) in frags]
+        for (by, bx, t, a) in frags:
+            z = a
+            if layers[-1]["act"] == "softmax" and z.size:
+                z = z - z.max(axis=-1, keepdims=True)
+                z = np.exp(z)
+                z = z / z.sum(axis=-1, keepdims=True)
+            hf, wf = z.shape[:2]
+            res[b, by:by + t * hf:t, bx:bx + t * wf:t, :] = z
+    return res
