@@ -1,0 +1,202 @@
+"""Benchmark of the fragment-based image scan on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload ID] [--no-cpu]
+
+A step is one full scan (every layer, the head and the reassembly) of the
+workload's synthetic image batch, already resident in device memory.  Prints
+one JSON line:
+  value        output pixels per second (windows classified per second)
+  roofline     the launch that takes the most time, its algorithmic work per
+               launch over its mean duration (HIP events around each launch on
+               the scan's stream), against the MI355X peak for its bound
+  launches     the same for every launch of the scan
+  cpu_baseline the per-patch CPU oracle on a bounded sample of windows, on
+               this host's cores
+Default workload: net N4 (the paper's Table 1 net) on a 512 x 512 greyscale
+image, 418 x 418 windows.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK = {  # MI355X published dense peaks
+    "hbm_gbs": 8000.0,
+    "f32_tflops": 157.3,
+    "bf16_tflops": 2516.6,
+}
+
+
+def kernel_source_digest():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_1302_1700_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel_name, workload):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        entries = json.load(f)
+    for e in entries:
+        if e.get("kernel") == kernel_name and e.get("workload") == workload \
+                and e.get("source_digest") == kernel_source_digest():
+            return e.get("bytes_per_launch")
+    return None
+
+
+def cpu_baseline(w, params, img, seconds_target=15.0):
+    """Per-patch oracle on a deterministic sample of windows."""
+    import numpy as np
+    import oracle
+    rng = np.random.default_rng(1234)
+    ny, nx = w.out_h, w.out_w
+    # calibrate on a small sample, then size the timed sample
+    cal = np.stack([rng.integers(0, w.batch, 16), rng.integers(0, ny, 16), rng.integers(0, nx, 16)], 1)
+    t0 = time.perf_counter()
+    oracle.patch_forward(w.layers, params, img, w.patch, cal)
+    rate = 16 / max(time.perf_counter() - t0, 1e-6)
+    n = int(min(max(rate * seconds_target, 32), 20000))
+    pts = np.stack([rng.integers(0, w.batch, n), rng.integers(0, ny, n), rng.integers(0, nx, n)], 1)
+    t0 = time.perf_counter()
+    oracle.patch_forward(w.layers, params, img, w.patch, pts)
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
+    total = w.batch * ny * nx
+    return {
+        "value": n / dt,
+        "unit": "output px/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": "%d seeded random windows of the same image, per-patch float64 forward "
+                  "(C, OpenMP); full map extrapolates to %.0f s" % (n, total / (n / dt)),
+    }
+
+
+def cpu_fragment_baseline(w, params, img):
+    """The fragment method on the CPU (float64, numpy/BLAS), full image."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    dt = time.perf_counter() - t0
+    return {"value": w.batch * w.out_h * w.out_w / dt, "unit": "output px/s", "seconds": dt,
+            "cores": len(os.sched_getaffinity(0)), "kind": "cpu fragment method (float64)",
+            "sample": "full image"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--profile-reps", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline legs")
+    ap.add_argument("--cpu-fragment", action="store_true", help="also time the CPU fragment method")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_1302_1700_amd import fragscan
+    from paper_1302_1700_amd import workloads as wl
+
+    w = wl.WORKLOADS[args.workload]
+    params, img = wl.workload_inputs(args.workload)
+    torch.cuda.set_device(0)
+    net = fragscan.Net(w.layers, params, w.channels, 0, w.dtype)
+    x = torch.from_numpy(img).cuda()
+    out = torch.empty((w.batch, w.out_h, w.out_w, w.n_classes), dtype=torch.float32, device="cuda")
+    ws = net.workspace(w.batch, w.height, w.width, x.device)
+    plan = net.plan(w.batch, w.height, w.width)
+    launches = net.launches(w.batch, w.height, w.width)
+
+    for _ in range(args.warmup):
+        net.scan(x, out=out, workspace=ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(args.steps):
+        net.scan(x, out=out, workspace=ws)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    pixels = w.batch * w.out_h * w.out_w
+
+    # per-launch times, HIP events around every launch on the same stream
+    per = net.profile(x, reps=args.profile_reps, out=out)
+    peak_mm = PEAK["bf16_tflops"] if w.dtype == "bf16" else PEAK["f32_tflops"]
+    rows = []
+    for L, t in zip(launches, per):
+        r = {"name": L["name"], "layer": L["layer"], "ms": t, "flops": L["flops"], "bytes": L["bytes"],
+             "tflops": L["flops"] / (t * 1e-3) / 1e12 if t > 0 else 0.0,
+             "gbs": L["bytes"] / (t * 1e-3) / 1e9 if t > 0 else 0.0}
+        ai = L["flops"] / L["bytes"] if L["bytes"] else 0.0
+        ridge = peak_mm * 1e12 / (PEAK["hbm_gbs"] * 1e9)
+        r["bound"] = "mfma" if ai >= ridge else "hbm"
+        r["frac"] = r["tflops"] / peak_mm if r["bound"] == "mfma" else r["gbs"] / PEAK["hbm_gbs"]
+        rows.append(r)
+    dom = max(rows, key=lambda r: r["ms"])
+    conv_flops = sum(r["flops"] for r in rows)
+    conv_ms = sum(r["ms"] for r in rows if r["flops"] > 0)
+    traffic = measured_traffic(dom["name"], w.name)
+    if dom["bound"] == "mfma":
+        roof = {"bound": "mfma", "achieved": dom["tflops"], "peak": peak_mm, "unit": "TFLOP/s",
+                "frac": dom["tflops"] / peak_mm}
+    else:
+        roof = {"bound": "hbm", "achieved": dom["gbs"], "peak": PEAK["hbm_gbs"], "unit": "GB/s",
+                "frac": dom["gbs"] / PEAK["hbm_gbs"]}
+    roof["traffic"] = traffic
+    roof["kernel"] = dom["name"]
+    roof["layer"] = dom["layer"]
+    roof["work_per_launch"] = dom["flops"] if dom["bound"] == "mfma" else dom["bytes"]
+    roof["mean_launch_ms"] = dom["ms"]
+
+    res = {
+        "metric": "output pixels/sec per image scan (1 GPU) + conv TFLOP/s as % MFMA peak",
+        "value": pixels / (ms * 1e-3),
+        "unit": "output px/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "image": [w.batch, w.height, w.width, w.channels],
+                   "patch": w.patch, "outputs": [w.batch, w.out_h, w.out_w], "fragments": net.info["n_fragments"]},
+        "tflops": plan["flops"] / (ms * 1e-3) / 1e12,
+        "pct_mfma_peak": 100.0 * plan["flops"] / (ms * 1e-3) / 1e12 / peak_mm,
+        "conv_tflops_in_conv_kernels": conv_flops / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0,
+        "roofline": roof,
+        "launches": rows,
+    }
+    net.close()
+    if not args.no_cpu:
+        res["cpu_baseline"] = cpu_baseline(w, params, img)
+        if args.cpu_fragment:
+            res["cpu_fragment"] = cpu_fragment_baseline(w, params, img)
+    print(json.dumps(res))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,212 @@
+/*
+ * fragscan — fragment-based image scanning with deep max-pooling CNNs on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library applies a net made of convolutional, max-pooling and fully
+ * connected layers to every w_0 x w_0 window of an image in one pass, the way
+ * Giusti et al., "Fast Image Scanning with Deep Max-Pooling Convolutional
+ * Neural Networks" (IDSIA-01-13) describe in Section 2.2: every convolution is
+ * computed once on whole extended maps, every k x k max-pooling layer splits
+ * each fragment into k^2 fragments, one per pooling offset, and the fragments
+ * of the last layer are put back together into a dense map holding, for every
+ * window, the net's output (class posterior probabilities when the last layer
+ * is a softmax, Section 1).
+ *
+ * Conventions used throughout
+ *   - A window ("patch") is named by its top-left pixel (Y, X); the output
+ *     map has (H - w_0 + 1) x (W - w_0 + 1) entries per image (Section 2.2:
+ *     all windows completely contained in the image).
+ *   - Images are [B][H][W][C] float32, channels innermost; outputs are
+ *     [B][H - w_0 + 1][W - w_0 + 1][n_classes] float32.
+ *   - Convolutions are valid cross-correlations; weights are OIHW
+ *     [c_out][c_in][k][k] float32, biases [c_out] float32.
+ *   - Fragment ids follow the offset order of Section 2.2.2 (o_x fastest):
+ *     the child of fragment f at pooling offset (o_x, o_y) of a k x k pool is
+ *     f * k^2 + o_y * k + o_x, starting from fragment 0 (the whole image).
+ *
+ * Errors: every call returns an fs_status and never throws or aborts across
+ * this boundary; fs_last_error() gives a thread-local message for the last
+ * failing call on the calling thread.  Arguments are validated before any
+ * work is enqueued, so a failing fs_scan leaves the stream untouched.
+ *
+ * Memory: pointers named d_* are device pointers (HIP device memory the caller
+ * owns); pointers named h_* or described as host are host memory.  A net owns
+ * the device copy of its weights from fs_net_create to fs_net_destroy.
+ */
+#ifndef FRAGSCAN_H
+#define FRAGSCAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct fs_net fs_net; /* opaque; immutable after fs_net_create */
+
+typedef enum {
+    FS_OK = 0,
+    FS_ERR_INVALID_ARG = 1,  /* null / misaligned pointer, bad enum, bad count */
+    FS_ERR_SHAPE = 2,        /* net or image sizes the method does not allow */
+    FS_ERR_UNSUPPORTED = 3,  /* allowed by the method, not by this library */
+    FS_ERR_WORKSPACE = 4,    /* workspace smaller than fs_scan_plan asks for */
+    FS_ERR_OOM = 5,          /* device allocation failed (fs_net_create only) */
+    FS_ERR_HIP = 6           /* a HIP runtime call failed */
+} fs_status;
+
+/* Layer kinds (Section 2: input, convolutional, max-pooling and fully
+ * connected layers).  A fully connected layer is applied to every fragment
+ * as a convolution whose kernel covers the whole patch-level map it receives
+ * (k = w_L for the first one, then 1); a fragment at any layer depends on one
+ * fragment of the layer below (Section 3). */
+typedef enum { FS_CONV = 0, FS_MAXPOOL = 1, FS_FC = 2 } fs_kind;
+
+/* Activation after a layer.  FS_ACT_SOFTMAX is allowed on the last layer only
+ * and turns its outputs into class posterior probabilities (Section 1). */
+typedef enum { FS_ACT_NONE = 0, FS_ACT_TANH = 1, FS_ACT_SOFTMAX = 2 } fs_act;
+
+/* Storage and matrix-core operand type of activations and weights.  FS_BF16
+ * rounds the image, weights and every stored activation to bfloat16 (round to
+ * nearest even) and accumulates, adds biases, applies activations and the
+ * softmax in float32. */
+typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
+
+/* One layer.  For FS_MAXPOOL: k = pool size, c_in = c_out = channels, weight
+ * and bias NULL, act FS_ACT_NONE.  For FS_CONV / FS_FC: k = kernel size
+ * (FS_FC may pass 0 to take the size of the map it receives), weight = host
+ * OIHW [c_out][c_in][k][k] float32, bias = host [c_out] float32 or NULL for
+ * zeros.  Host arrays are copied by fs_net_create and not kept. */
+typedef struct {
+    int32_t kind;
+    int32_t k;
+    int32_t c_in;
+    int32_t c_out;
+    int32_t act;
+    const float *weight;
+    const float *bias;
+} fs_layer;
+
+typedef struct {
+    int32_t patch;        /* w_0 */
+    int32_t in_channels;  /* C */
+    int32_t n_classes;    /* c_out of the last layer */
+    int32_t n_layers;
+    int32_t n_pools;
+    int32_t stride;       /* product of pool sizes: output pixels one final
+                             fragment pixel step covers, per axis */
+    int32_t n_fragments;  /* F_L, the product of the squared pool sizes
+                             (Section 3) */
+    int32_t dtype;        /* fs_dtype */
+} fs_net_info;
+
+typedef struct {
+    int32_t batch;
+    int32_t out_h;           /* H - w_0 + 1 */
+    int32_t out_w;           /* W - w_0 + 1 */
+    int32_t n_launches;      /* kernel launches fs_scan enqueues */
+    size_t workspace_bytes;  /* device workspace fs_scan needs */
+    double flops;            /* algorithmic FLOPs of one scan: 2 * c_in * k^2 *
+                                c_out per output pixel of every fragment of
+                                every conv / fc layer */
+    double min_bytes;        /* sum over launches of the bytes each must move
+                                at least (read its input once, write its output
+                                once, read its weights once) */
+} fs_plan_info;
+
+/* Per-launch description, for measurement.  `name` is the kernel's symbol-
+ * like label as it appears in profiler traces (NUL-terminated). */
+typedef struct {
+    int32_t layer;        /* first net layer this launch computes */
+    int32_t n_layers;     /* net layers it covers (a fused head covers 1-2) */
+    int32_t kind;         /* 0 conv, 1 pool, 2 head */
+    int32_t fragments;    /* B * fragments written by this launch */
+    int64_t out_pixels;   /* true output pixels written, all fragments */
+    double flops;         /* algorithmic FLOPs (see fs_plan_info) */
+    double bytes;         /* minimum bytes (see fs_plan_info) */
+    int32_t grid;         /* workgroups launched */
+    int32_t block;        /* threads per workgroup */
+    char name[64];
+} fs_launch_info;
+
+/* Create a net.  The stack must be: conv / max-pool layers in any order, then
+ * one or more fully connected layers (Section 2); channels must chain; every
+ * pool must divide the patch-level map it receives (Section 2.1.2:
+ * mod(w_{l-1}, k) = 0); the patch-level map after the last layer must be
+ * 1 x 1.  `patch` is w_0 (0: derive it from the stack).  A patch that does
+ * not agree with the stack gives FS_ERR_SHAPE.  Weights are converted (and
+ * for FS_BF16 rounded) and uploaded to the current HIP device, which the net
+ * is then bound to.  On success *out receives the handle. */
+fs_status fs_net_create(const fs_layer *layers, int32_t n_layers, int32_t in_channels,
+                        int32_t patch, int32_t dtype, fs_net **out);
+
+/* The same validation and packing as fs_net_create, without touching any
+ * device: the handle answers fs_net_query, fs_scan_plan, fs_scan_launches,
+ * fs_fragment_table and fs_reassembly_index (host-side planning, e.g. on a
+ * machine without a GPU); fs_scan and fs_scan_profile reject it with
+ * FS_ERR_INVALID_ARG.  Release it with fs_net_destroy. */
+fs_status fs_net_create_plan_only(const fs_layer *layers, int32_t n_layers, int32_t in_channels,
+                                  int32_t patch, int32_t dtype, fs_net **out);
+
+/* Release a net and its device memory.  NULL is ignored.  The caller must
+ * make sure no scan using the net is still running. */
+void fs_net_destroy(fs_net *net);
+
+fs_status fs_net_query(const fs_net *net, fs_net_info *out);
+
+/* Sizes and work of a scan of B images of H x W (Section 2.2: an s x s image
+ * with s >= w_0 gives (s - w_0 + 1)^2 windows; rectangular images are the
+ * per-axis generalisation).  FS_ERR_SHAPE if H or W < w_0 or B < 1. */
+fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_plan_info *out);
+
+/* Per-launch description of the scan fs_scan would enqueue; writes
+ * min(capacity, n_launches) entries. */
+fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W,
+                           fs_launch_info *h_out, int32_t capacity);
+
+/* Scan B images.  d_image: device [B][H][W][C] float32; d_out: device
+ * [B][H-w_0+1][W-w_0+1][n_classes] float32; d_workspace: device scratch of at
+ * least fs_scan_plan's workspace_bytes (contents need not be initialised and
+ * are clobbered).  All three 256-byte aligned, non-overlapping.  `stream` is a
+ * hipStream_t (NULL = the default stream).  Asynchronous: returns once every
+ * kernel is enqueued; a device fault shows up at the caller's next stream
+ * synchronisation.  Calls on different streams with distinct workspaces and
+ * outputs may run concurrently on one net. */
+fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
+                  float *d_out, void *d_workspace, size_t workspace_bytes, void *stream);
+
+/* fs_scan, repeated `reps` times, with a HIP event recorded before and after
+ * every launch; synchronises the stream and writes, per launch, the mean of
+ * its event-to-event times over the repetitions in milliseconds into
+ * h_launch_ms[0 .. min(capacity, n_launches)).  For measurement only. */
+fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, int32_t H,
+                          int32_t W, float *d_out, void *d_workspace, size_t workspace_bytes,
+                          void *stream, int32_t reps, float *h_launch_ms, int32_t capacity);
+
+/* Fragment table of a scan of an H x W image: for every final fragment
+ * f = 0 .. F_L - 1 a record of 5 + 2 * n_pools int32:
+ *   f, h_f, w_f, Y0, X0, then (o_x, o_y) of each pool in layer order,
+ * where (h_f, w_f) is the fragment's size after the last layer (Eqs. 3-4 and
+ * 6-7, never below 0) and output pixel (Y0 + stride * y, X0 + stride * x)
+ * holds the fragment's pixel (y, x).  Host output; writes at most `capacity`
+ * int32 and stores the number the full table needs in *n_needed (n_needed
+ * may be NULL; h_out may be NULL to query the size). */
+fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_out,
+                            size_t capacity, size_t *n_needed);
+
+/* Reassembly index of an H x W image: for every output pixel, row-major over
+ * (Y, X), the triple (f, y, x): the final fragment and the position in it
+ * that holds the window with top-left corner (Y, X) (Section 3: the union of
+ * all fragments covers every window).  Host output, same size protocol as
+ * fs_fragment_table (3 * (H - w_0 + 1) * (W - w_0 + 1) int32). */
+fs_status fs_reassembly_index(const fs_net *net, int32_t H, int32_t W, int32_t *h_out,
+                              size_t capacity, size_t *n_needed);
+
+const char *fs_status_str(fs_status s);
+const char *fs_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FRAGSCAN_H */

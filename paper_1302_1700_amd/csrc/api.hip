@@ -1,0 +1,892 @@
+// C-ABI of the fragment scan: net validation, weight packing, the per-scan
+// fragment plan, and the launch sequence.  Declarations and the contract of
+// every entry point are in include/fragscan.h.
+//
+// Plan of a scan (Section 2.2), per layer, from F_0 = 1 fragment of size
+// H x W (Eqs. 1-2):
+//   conv / fc : F unchanged, each size s -> s - (k - 1)           (Eqs. 3-4)
+//   k-pool    : F -> k^2 F; the child at offset o of a fragment of size s gets
+//               div(s - o, k), never below 0                      (Eqs. 6-7)
+// Sizes are separable per axis, so each layer keeps one table of heights
+// (indexed by the y-offset chain) and one of widths (x-offset chain).
+#include "../../include/fragscan.h"
+#include "fs_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+using namespace fs;
+
+namespace {
+
+thread_local std::string g_err;
+
+fs_status fail(fs_status s, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return s;
+}
+
+fs_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(FS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+uint16_t host_f2bf(float f)
+{
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7f800000u) == 0x7f800000u) return (uint16_t)((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+struct NetLayer {
+    int kind, k, cin, cout, act;
+    int w_in, w_out;      // patch-level map sizes (Sections 2.1.1, 2.1.2)
+    // conv launch parameters fixed at creation
+    bool vec = false;     // channel-vector path
+    int nb = 1;           // output-channel blocks per workgroup
+    int nbt = 0;          // channel blocks, padded to a multiple of nb
+    int ksteps = 0;
+    size_t w_off = 0, b_off = 0;  // offsets into the net's device block
+};
+
+}  // namespace
+
+struct fs_net {
+    std::vector<NetLayer> L;
+    int patch = 0, C = 0, dtype = 0, ncls = 0;
+    std::vector<int> pool_k;
+    int S = 1, F = 1;
+    int device = 0;
+    bool head_fc = false;     // last layer fused into the head
+    size_t head_w_off = 0, head_b_off = 0;
+    int head_cin = 0;
+    void *d_mem = nullptr;
+    size_t mem_bytes = 0;
+};
+
+namespace {
+
+int kstep_of(int dtype) { return dtype == DT_BF16 ? 32 : 16; }
+int elem_of(int dtype) { return dtype == DT_BF16 ? 2 : 4; }
+
+// Pack OIHW weights for the conv kernel: for K step s, channel block nb and
+// lane (g = lane / 16, n = lane % 16) the LPE consecutive elements
+// e = 0..LPE-1 hold W[nb*16 + n][ci][dy][dx] for the K index
+//   vector path: tap = s / (cin / KSTEP), ci = (s % (cin / KSTEP)) * KSTEP + g*LPE + e
+//   gather path: kk = s*KSTEP + g*LPE + e, tap = kk / cin, ci = kk % cin
+// with tap = dy * k + dx; zero where the channel or K index is past the end.
+void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector<uint8_t> &out)
+{
+    const int KSTEP = kstep_of(dtype), LPE = KSTEP / 4, es = elem_of(dtype);
+    const size_t n = (size_t)l.ksteps * l.nbt * 64 * LPE;
+    out.assign(n * es, 0);
+    const int taps = l.k * l.k;
+    for (int s = 0; s < l.ksteps; ++s)
+        for (int nb = 0; nb < l.nbt; ++nb)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int e = 0; e < LPE; ++e) {
+                    const int g = lane / 16, nn = lane % 16;
+                    const int co = nb * 16 + nn;
+                    int tap, ci;
+                    if (l.vec) {
+                        const int ncc = l.cin / KSTEP;
+                        tap = s / ncc;
+                        ci = (s % ncc) * KSTEP + g * LPE + e;
+                    } else {
+                        const int kk = s * KSTEP + g * LPE + e;
+                        tap = kk / l.cin;
+                        ci = kk % l.cin;
+                    }
+                    float v = 0.f;
+                    if (co < l.cout && tap < taps) {
+                        const int dy = tap / l.k, dx = tap % l.k;
+                        v = w[(((size_t)co * l.cin + ci) * l.k + dy) * l.k + dx];
+                    }
+                    const size_t idx = (((size_t)s * l.nbt + nb) * 64 + lane) * LPE + e;
+                    if (dtype == DT_BF16) {
+                        const uint16_t h = host_f2bf(v);
+                        std::memcpy(&out[idx * 2], &h, 2);
+                    } else {
+                        std::memcpy(&out[idx * 4], &v, 4);
+                    }
+                }
+}
+
+int choose_nb(int nbt, bool vec)
+{
+    static const int cand_vec[] = {13, 8, 7, 4, 3, 2, 1};
+    static const int cand_gather[] = {4, 3, 2, 1};
+    const int *c = vec ? cand_vec : cand_gather;
+    const int nc = vec ? 7 : 4;
+    for (int i = 0; i < nc; ++i) {
+        const int nb = c[i];
+        const int pad = (nbt + nb - 1) / nb * nb;
+        if ((double)nbt / pad >= 0.8) return nb;
+    }
+    return 1;
+}
+
+// ---------------------------------------------------------------------------
+// Per-scan plan
+// ---------------------------------------------------------------------------
+
+struct Geo {  // fragment set entering a layer
+    int Q = 1;                    // fragments per axis; F = Q * Q per image
+    std::vector<int> ey, ex;      // true sizes per y / x index
+    int hmax = 0, wmax = 0, C = 0;
+    bool is_image = true;         // the input image (float32 even in bf16 nets)
+};
+
+struct Launch {
+    int type;                 // 0 conv, 1 pool, 2 head
+    int layer, n_layers;
+    int src, dst;             // -1 image, 0/1 workspace buffers, 2 output
+    bool in_f32;
+    ConvArgs conv;
+    PoolArgs pool;
+    HeadArgs head;
+    int mb = 0, nb = 0;
+    bool vec = false, has_fc = false;
+    int gx = 1, gy = 1;
+    int frags = 0;
+    long long out_pixels = 0;
+    double flops = 0, bytes = 0;
+    std::string name;
+};
+
+struct Plan {
+    int B, H, W, ny, nx;
+    std::vector<Launch> launches;
+    size_t buf_bytes = 0;      // each of the two ping-pong buffers
+    size_t ws_bytes = 0;
+    double flops = 0, bytes = 0;
+};
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+void fill_axis(AxisTable &t, const Geo &g)
+{
+    std::memset(&t, 0, sizeof t);
+    for (int i = 0; i < g.Q; ++i) {
+        t.y[i] = (uint16_t)g.ey[i];
+        t.x[i] = (uint16_t)g.ex[i];
+    }
+}
+
+long long true_pixels(const Geo &g)
+{
+    long long sy = 0, sx = 0;
+    for (int v : g.ey) sy += v;
+    for (int v : g.ex) sx += v;
+    return sy * sx;  // separable: sum over (fy, fx) of ey[fy] * ex[fx]
+}
+
+// Tile choice for a conv launch (see conv_kernel.hip for the scheme).
+fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, Launch &L)
+{
+    const int k = l.k;
+    const int hout_max = in.hmax - k + 1, wout_max = in.wmax - k + 1;
+    const int es = elem_of(net->dtype);
+    const int KSTEP = kstep_of(net->dtype);
+    const int cs = l.vec ? l.cin + 16 / es : l.cin;  // +16 bytes per pixel spreads LDS banks
+    const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
+    // distinct output widths present
+    std::vector<int> wouts;
+    for (int v : in.ex)
+        if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
+            wouts.push_back(v - k + 1);
+    const int mbs[3] = {2, 4, 1};
+    for (int mi = 0; mi < 3; ++mi) {
+        const int mb = mbs[mi];
+        if (!conv_tile_supported(mb, l.nb)) continue;
+        const int mt = 64 * mb;
+        int nbands = wout_max <= 64 ? 1 : (wout_max + 31) / 32;
+        for (; nbands <= wout_max; ++nbands) {
+            const int band_w = (wout_max + nbands - 1) / nbands;
+            int tmin = band_w;
+            for (int wo : wouts)
+                for (int b = 0; b < nbands; ++b) {
+                    const int twb = std::min(band_w, wo - b * band_w);
+                    if (twb > 0) tmin = std::min(tmin, twb);
+                }
+            int rmax = (mt - 1 + tmin - 1) / tmin + k;
+            rmax = std::min(rmax, in.hmax);
+            const size_t lds = offtab + (size_t)rmax * (band_w + k - 1) * cs * es;
+            if (lds > 96 * 1024) {
+                if (band_w <= 8) break;
+                continue;
+            }
+            L.mb = mb;
+            L.conv.band_w = band_w;
+            L.conv.nbands = nbands;
+            L.conv.mt = mt;
+            L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
+            L.conv.lds_cs = cs;
+            L.conv.lds_bytes = (int)lds;
+            return FS_OK;
+        }
+    }
+    return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile fits in LDS", L.layer);
+}
+
+fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
+{
+    if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
+    if (H < net->patch || W < net->patch)
+        return fail(FS_ERR_SHAPE, "image %dx%d smaller than the patch size %d", H, W, net->patch);
+    P = Plan();
+    P.B = B;
+    P.H = H;
+    P.W = W;
+    P.ny = H - net->patch + 1;
+    P.nx = W - net->patch + 1;
+    const int es = elem_of(net->dtype);
+
+    Geo g;
+    g.Q = 1;
+    g.ey = {H};
+    g.ex = {W};
+    g.hmax = H;
+    g.wmax = W;
+    g.C = net->C;
+    g.is_image = true;
+
+    const int nl = (int)net->L.size();
+    const int body = net->head_fc ? nl - 1 : nl;
+    int cur = -1;  // where the current activations live
+    size_t buf = 0;
+    for (int li = 0; li < body; ++li) {
+        const NetLayer &l = net->L[li];
+        Launch L{};
+        L.layer = li;
+        L.n_layers = 1;
+        L.src = cur;
+        L.dst = (cur == 0) ? 1 : 0;
+        L.in_f32 = g.is_image;
+        const int F = g.Q * g.Q;
+        const long long in_pix = true_pixels(g);
+        Geo o;
+        if (l.kind == 1) {  // pool
+            const int k = l.k;
+            o.Q = g.Q * k;
+            o.ey.assign(o.Q, 0);
+            o.ex.assign(o.Q, 0);
+            for (int i = 0; i < g.Q; ++i)
+                for (int off = 0; off < k; ++off) {
+                    o.ey[i * k + off] = std::max(g.ey[i] - off, 0) / k;
+                    o.ex[i * k + off] = std::max(g.ex[i] - off, 0) / k;
+                }
+            o.C = g.C;
+            o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
+            o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
+            if (g.Q * k > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
+            L.type = 1;
+            PoolArgs &a = L.pool;
+            a.F = F;
+            a.Q = g.Q;
+            a.in_h = g.hmax;
+            a.in_w = g.wmax;
+            a.out_h = std::max(o.hmax, 1);
+            a.out_w = std::max(o.wmax, 1);
+            a.C = g.C;
+            a.k = k;
+            a.n_children = B * F * k * k;
+            fill_axis(a.ext, g);
+            L.gx = B * F * k * k * a.out_h;
+            L.frags = B * F * k * k;
+            L.out_pixels = (long long)B * true_pixels(o);
+            L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * o.C * es;
+            L.name = pool_kernel_name(net->dtype, g.is_image);
+        } else {  // conv or fc as convolution
+            const int k = l.k;
+            o.Q = g.Q;
+            o.ey.resize(g.Q);
+            o.ex.resize(g.Q);
+            for (int i = 0; i < g.Q; ++i) {
+                o.ey[i] = std::max(g.ey[i] - (k - 1), 0);
+                o.ex[i] = std::max(g.ex[i] - (k - 1), 0);
+            }
+            o.C = l.cout;
+            o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
+            o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
+            L.type = 0;
+            L.vec = l.vec;
+            L.nb = l.nb;
+            ConvArgs &a = L.conv;
+            a.nfrag = B * F;
+            a.F = F;
+            a.Q = g.Q;
+            a.in_h = g.hmax;
+            a.in_w = g.wmax;
+            a.in_c = g.C;
+            a.out_h = std::max(o.hmax, 1);
+            a.out_w = std::max(o.wmax, 1);
+            a.k = k;
+            a.cin = l.cin;
+            a.cout = l.cout;
+            // the last layer, when not fused into the head, leaves its
+            // activation to the head (softmax needs all classes)
+            a.act = (li == nl - 1) ? ACT_NONE : l.act;
+            a.ksteps = l.ksteps;
+            a.nbt = l.nbt;
+            fill_axis(a.ext, g);
+            fs_status st = plan_conv_tiles(net, l, g, L);
+            if (st != FS_OK) return st;
+            L.gx = B * F * a.nbands * a.tiles_per_band;
+            L.gy = l.nbt / l.nb;
+            L.frags = B * F;
+            L.out_pixels = (long long)B * true_pixels(o);
+            L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
+            L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
+                      (double)l.cin * k * k * l.cout * es;
+            L.name = conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.vec);
+        }
+        o.is_image = false;
+        const size_t out_bytes = (size_t)B * o.Q * o.Q * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
+        buf = std::max(buf, out_bytes);
+        P.flops += L.flops;
+        P.bytes += L.bytes;
+        P.launches.push_back(L);
+        cur = L.dst;
+        g = o;
+    }
+
+    // head: the (fused) last layer, its activation, and the reassembly
+    {
+        Launch L{};
+        L.type = 2;
+        L.layer = net->head_fc ? nl - 1 : nl;
+        L.n_layers = net->head_fc ? 1 : 0;
+        L.src = cur;
+        L.dst = 2;
+        L.in_f32 = g.is_image;
+        L.has_fc = net->head_fc;
+        HeadArgs &a = L.head;
+        a.B = B;
+        a.F = g.Q * g.Q;
+        a.Q = g.Q;
+        a.in_h = std::max(g.hmax, 1);
+        a.in_w = std::max(g.wmax, 1);
+        a.C = g.C;
+        a.ny = P.ny;
+        a.nx = P.nx;
+        a.ncls = net->ncls;
+        a.act = net->L.back().act;
+        a.S = net->S;
+        // Y mod S -> per-axis fragment index: the mixed-radix digits of r
+        // (least significant = first pool) read back most significant first
+        for (int r = 0; r < net->S; ++r) {
+            int rr = r, idx = 0;
+            for (int k : net->pool_k) {
+                idx = idx * k + rr % k;
+                rr /= k;
+            }
+            a.digit_map[r] = (uint16_t)idx;
+        }
+        const long long npix = (long long)B * P.ny * P.nx;
+        L.gx = (int)((npix + 15) / 16);
+        L.frags = B * a.F;
+        L.out_pixels = npix;
+        L.flops = net->head_fc ? (double)npix * 2.0 * net->head_cin * net->ncls : 0.0;
+        L.bytes = (double)npix * g.C * (g.is_image ? 4 : es) + (double)npix * net->ncls * 4;
+        L.name = head_kernel_name(net->dtype, g.is_image, net->head_fc);
+        P.flops += L.flops;
+        P.bytes += L.bytes;
+        P.launches.push_back(L);
+    }
+    P.buf_bytes = align_up(buf, 256);
+    P.ws_bytes = 2 * P.buf_bytes;
+    return FS_OK;
+}
+
+fs_status check_device(const fs_net *net)
+{
+    if (net->device < 0) return fail(FS_ERR_INVALID_ARG, "net was created for planning only");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != net->device)
+        return fail(FS_ERR_INVALID_ARG, "current device %d is not the net's device %d", dev, net->device);
+    return FS_OK;
+}
+
+fs_status validate_scan(const fs_net *net, const float *d_image, int B, int H, int W, float *d_out,
+                        void *d_ws, size_t ws_bytes, Plan &P)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
+    if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
+        return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
+    fs_status st = make_plan(net, B, H, W, P);
+    if (st != FS_OK) return st;
+    if (ws_bytes < P.ws_bytes)
+        return fail(FS_ERR_WORKSPACE, "workspace of %zu bytes, the scan needs %zu", ws_bytes, P.ws_bytes);
+    if (P.ws_bytes && !d_ws) return fail(FS_ERR_INVALID_ARG, "workspace pointer is NULL");
+    if ((uintptr_t)d_ws & 255) return fail(FS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    return check_device(net);
+}
+
+hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_out, void *d_ws,
+                   hipStream_t s, int i)
+{
+    Launch &L = P.launches[i];
+    char *ws = static_cast<char *>(d_ws);
+    auto ptr = [&](int which) -> void * {
+        if (which == -1) return const_cast<float *>(d_image);
+        if (which == 2) return d_out;
+        return ws + (size_t)which * P.buf_bytes;
+    };
+    const char *mem = static_cast<const char *>(net->d_mem);
+    if (L.type == 0) {
+        const NetLayer &l = net->L[L.layer];
+        L.conv.in = ptr(L.src);
+        L.conv.out = ptr(L.dst);
+        L.conv.w = mem + l.w_off;
+        L.conv.bias = reinterpret_cast<const float *>(mem + l.b_off);
+        return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.vec, L.gx, L.gy, s);
+    }
+    if (L.type == 1) {
+        L.pool.in = ptr(L.src);
+        L.pool.out = ptr(L.dst);
+        return launch_pool(L.pool, net->dtype, L.in_f32, L.gx, s);
+    }
+    L.head.in = ptr(L.src);
+    L.head.out = d_out;
+    L.head.w = reinterpret_cast<const float *>(mem + net->head_w_off);
+    L.head.bias = reinterpret_cast<const float *>(mem + net->head_b_off);
+    return launch_head(L.head, net->dtype, L.in_f32, L.has_fc, L.gx, s);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C-ABI
+// ---------------------------------------------------------------------------
+
+extern "C" {
+
+const char *fs_status_str(fs_status s)
+{
+    switch (s) {
+    case FS_OK: return "ok";
+    case FS_ERR_INVALID_ARG: return "invalid argument";
+    case FS_ERR_SHAPE: return "shape not allowed";
+    case FS_ERR_UNSUPPORTED: return "unsupported";
+    case FS_ERR_WORKSPACE: return "workspace too small";
+    case FS_ERR_OOM: return "out of device memory";
+    case FS_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+const char *fs_last_error(void) { return g_err.c_str(); }
+
+static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in_channels, int32_t patch,
+                            int32_t dtype, bool upload, fs_net **out)
+{
+    if (!out) return fail(FS_ERR_INVALID_ARG, "out is NULL");
+    *out = nullptr;
+    if (!layers || n_layers < 1) return fail(FS_ERR_INVALID_ARG, "no layers");
+    if (in_channels < 1) return fail(FS_ERR_INVALID_ARG, "in_channels must be >= 1");
+    if (dtype != FS_F32 && dtype != FS_BF16) return fail(FS_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    if (patch < 0) return fail(FS_ERR_INVALID_ARG, "patch must be >= 0");
+
+    // --- validate the stack (Section 2) ---
+    std::vector<NetLayer> L(n_layers);
+    bool seen_fc = false;
+    int c = in_channels;
+    for (int i = 0; i < n_layers; ++i) {
+        const fs_layer &s = layers[i];
+        NetLayer &l = L[i];
+        l.kind = s.kind;
+        l.k = s.k;
+        l.cin = s.c_in;
+        l.cout = s.c_out;
+        l.act = s.act;
+        if (s.kind != FS_CONV && s.kind != FS_MAXPOOL && s.kind != FS_FC)
+            return fail(FS_ERR_INVALID_ARG, "layer %d: unknown kind %d", i, s.kind);
+        if (s.act != FS_ACT_NONE && s.act != FS_ACT_TANH && s.act != FS_ACT_SOFTMAX)
+            return fail(FS_ERR_INVALID_ARG, "layer %d: unknown activation %d", i, s.act);
+        if (s.act == FS_ACT_SOFTMAX && i != n_layers - 1)
+            return fail(FS_ERR_SHAPE, "layer %d: softmax is allowed on the last layer only", i);
+        if (s.c_in != c) return fail(FS_ERR_SHAPE, "layer %d: c_in %d, the layer below gives %d", i, s.c_in, c);
+        if (s.c_in < 1 || s.c_out < 1) return fail(FS_ERR_SHAPE, "layer %d: channel counts must be >= 1", i);
+        if (s.kind == FS_MAXPOOL) {
+            if (seen_fc) return fail(FS_ERR_SHAPE, "layer %d: pooling after a fully connected layer", i);
+            if (s.k < 1) return fail(FS_ERR_SHAPE, "layer %d: pool size must be >= 1", i);
+            if (s.c_out != s.c_in) return fail(FS_ERR_SHAPE, "layer %d: a pool keeps the channel count", i);
+            if (s.weight || s.bias) return fail(FS_ERR_INVALID_ARG, "layer %d: a pool has no weights", i);
+            if (s.act != FS_ACT_NONE) return fail(FS_ERR_UNSUPPORTED, "layer %d: activation on a pool", i);
+        } else {
+            if (s.kind == FS_CONV && seen_fc)
+                return fail(FS_ERR_SHAPE, "layer %d: convolution after a fully connected layer", i);
+            if (s.kind == FS_FC) seen_fc = true;
+            if (s.k < 0 || (s.k == 0 && s.kind != FS_FC)) return fail(FS_ERR_SHAPE, "layer %d: bad kernel size", i);
+            if (!s.weight) return fail(FS_ERR_INVALID_ARG, "layer %d: weight is NULL", i);
+        }
+        c = s.c_out;
+    }
+    // patch-level sizes: derive w_0 when the fully connected sizes are given
+    bool derivable = true;
+    for (auto &l : L)
+        if (l.kind == FS_FC && l.k == 0) derivable = false;
+    int w0 = patch;
+    if (derivable) {
+        int w = 1;
+        for (int i = n_layers - 1; i >= 0; --i) w = (L[i].kind == FS_MAXPOOL) ? w * L[i].k : w + L[i].k - 1;
+        if (patch == 0) w0 = w;
+        else if (patch != w) return fail(FS_ERR_SHAPE, "patch %d does not match the stack, which needs %d", patch, w);
+    } else if (patch == 0) {
+        return fail(FS_ERR_INVALID_ARG, "patch is 0 and a fully connected layer has k = 0");
+    }
+    {
+        int w = w0;
+        for (int i = 0; i < n_layers; ++i) {
+            NetLayer &l = L[i];
+            l.w_in = w;
+            if (l.kind == FS_MAXPOOL) {
+                if (w % l.k) return fail(FS_ERR_SHAPE, "layer %d: pool %d does not divide the map size %d", i, l.k, w);
+                w /= l.k;
+            } else {
+                if (l.kind == FS_FC && l.k == 0) l.k = w;
+                if (l.kind == FS_FC && l.k != w)
+                    return fail(FS_ERR_SHAPE, "layer %d: fully connected kernel %d on a %d map", i, l.k, w);
+                if (l.k > w) return fail(FS_ERR_SHAPE, "layer %d: kernel %d larger than the map %d", i, l.k, w);
+                w -= l.k - 1;
+            }
+            l.w_out = w;
+        }
+        if (w != 1) return fail(FS_ERR_SHAPE, "the last map is %dx%d, not 1x1", w, w);
+    }
+
+    fs_net *net = new (std::nothrow) fs_net();
+    if (!net) return fail(FS_ERR_OOM, "host allocation failed");
+    net->patch = w0;
+    net->C = in_channels;
+    net->dtype = dtype;
+    net->ncls = L.back().cout;
+    for (auto &l : L)
+        if (l.kind == FS_MAXPOOL) {
+            net->pool_k.push_back(l.k);
+            net->S *= l.k;
+            net->F *= l.k * l.k;
+        }
+    if (net->S > kMaxAxis) {
+        delete net;
+        return fail(FS_ERR_UNSUPPORTED, "pool sizes multiply to %d > %d per axis", net->S, kMaxAxis);
+    }
+    if (net->ncls > kMaxHeadClasses) {
+        delete net;
+        return fail(FS_ERR_UNSUPPORTED, "%d outputs; at most %d supported", net->ncls, kMaxHeadClasses);
+    }
+    const NetLayer &last = L.back();
+    net->head_fc = last.kind != FS_MAXPOOL && last.k == 1 && last.cin * last.cout <= kMaxHeadWeights;
+    net->head_cin = net->head_fc ? last.cin : 0;
+
+    // --- pack parameters into one device block ---
+    std::vector<uint8_t> blob;
+    auto push = [&](const void *p, size_t n) {
+        const size_t off = align_up(blob.size(), 256);
+        blob.resize(off + n);
+        std::memcpy(blob.data() + off, p, n);
+        return off;
+    };
+    const int KSTEP = kstep_of(dtype);
+    for (int i = 0; i < n_layers; ++i) {
+        NetLayer &l = L[i];
+        if (l.kind == FS_MAXPOOL) continue;
+        const fs_layer &s = layers[i];
+        std::vector<float> bias(l.cout, 0.f);
+        if (s.bias) std::memcpy(bias.data(), s.bias, sizeof(float) * l.cout);
+        if (i == n_layers - 1 && net->head_fc) {
+            std::vector<float> w((size_t)l.cout * l.cin);
+            std::memcpy(w.data(), s.weight, sizeof(float) * w.size());
+            net->head_w_off = push(w.data(), w.size() * 4);
+            net->head_b_off = push(bias.data(), bias.size() * 4);
+            continue;
+        }
+        // the layer that reads the float32 image of a bf16 net converts while
+        // staging, which the gather path does
+        l.vec = (l.cin % KSTEP) == 0 && !(dtype == FS_BF16 && i == 0);
+        const int nbt0 = (l.cout + 15) / 16;
+        l.nb = choose_nb(nbt0, l.vec);
+        l.nbt = (nbt0 + l.nb - 1) / l.nb * l.nb;
+        l.ksteps = l.vec ? l.k * l.k * (l.cin / KSTEP) : (l.k * l.k * l.cin + KSTEP - 1) / KSTEP;
+        std::vector<uint8_t> pw;
+        pack_conv_weights(l, s.weight, dtype, pw);
+        l.w_off = push(pw.data(), pw.size());
+        std::vector<float> bp((size_t)l.nbt * 16, 0.f);
+        std::copy(bias.begin(), bias.end(), bp.begin());
+        l.b_off = push(bp.data(), bp.size() * 4);
+    }
+    if (!net->head_fc) {  // the head still takes a (unused) bias pointer
+        std::vector<float> z(kMaxHeadClasses, 0.f);
+        net->head_w_off = push(z.data(), z.size() * 4);
+        net->head_b_off = push(z.data(), z.size() * 4);
+    }
+    net->L = L;
+    if (!upload) {  // planning-only handle: no device memory
+        net->device = -1;
+        *out = net;
+        return FS_OK;
+    }
+    hipError_t e = hipGetDevice(&net->device);
+    if (e != hipSuccess) {
+        delete net;
+        return hip_fail(e, "hipGetDevice");
+    }
+    net->mem_bytes = blob.size();
+    e = hipMalloc(&net->d_mem, blob.size());
+    if (e != hipSuccess) {
+        delete net;
+        return fail(FS_ERR_OOM, "hipMalloc(%zu): %s", blob.size(), hipGetErrorString(e));
+    }
+    e = hipMemcpy(net->d_mem, blob.data(), blob.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(net->d_mem);
+        delete net;
+        return hip_fail(e, "hipMemcpy (weights)");
+    }
+    *out = net;
+    return FS_OK;
+}
+
+fs_status fs_net_create(const fs_layer *layers, int32_t n_layers, int32_t in_channels, int32_t patch,
+                        int32_t dtype, fs_net **out)
+{
+    return net_create(layers, n_layers, in_channels, patch, dtype, true, out);
+}
+
+fs_status fs_net_create_plan_only(const fs_layer *layers, int32_t n_layers, int32_t in_channels,
+                                  int32_t patch, int32_t dtype, fs_net **out)
+{
+    return net_create(layers, n_layers, in_channels, patch, dtype, false, out);
+}
+
+void fs_net_destroy(fs_net *net)
+{
+    if (!net) return;
+    if (net->d_mem) (void)hipFree(net->d_mem);
+    delete net;
+}
+
+fs_status fs_net_query(const fs_net *net, fs_net_info *out)
+{
+    if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
+    out->patch = net->patch;
+    out->in_channels = net->C;
+    out->n_classes = net->ncls;
+    out->n_layers = (int)net->L.size();
+    out->n_pools = (int)net->pool_k.size();
+    out->stride = net->S;
+    out->n_fragments = net->F;
+    out->dtype = net->dtype;
+    return FS_OK;
+}
+
+fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_plan_info *out)
+{
+    if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
+    Plan P;
+    fs_status st = make_plan(net, B, H, W, P);
+    if (st != FS_OK) return st;
+    out->batch = B;
+    out->out_h = P.ny;
+    out->out_w = P.nx;
+    out->n_launches = (int)P.launches.size();
+    out->workspace_bytes = P.ws_bytes;
+    out->flops = P.flops;
+    out->min_bytes = P.bytes;
+    return FS_OK;
+}
+
+fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_launch_info *h_out,
+                           int32_t capacity)
+{
+    if (!net || (!h_out && capacity > 0) || capacity < 0) return fail(FS_ERR_INVALID_ARG, "bad argument");
+    Plan P;
+    fs_status st = make_plan(net, B, H, W, P);
+    if (st != FS_OK) return st;
+    const int n = std::min<int>(capacity, (int)P.launches.size());
+    for (int i = 0; i < n; ++i) {
+        const Launch &L = P.launches[i];
+        fs_launch_info &o = h_out[i];
+        std::memset(&o, 0, sizeof o);
+        o.layer = L.layer;
+        o.n_layers = L.n_layers;
+        o.kind = L.type;
+        o.fragments = L.frags;
+        o.out_pixels = L.out_pixels;
+        o.flops = L.flops;
+        o.bytes = L.bytes;
+        o.grid = L.gx * L.gy;
+        o.block = 256;
+        std::snprintf(o.name, sizeof o.name, "%s", L.name.c_str());
+    }
+    return FS_OK;
+}
+
+fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, float *d_out,
+                  void *d_workspace, size_t workspace_bytes, void *stream)
+{
+    Plan P;
+    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, P);
+    if (st != FS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < (int)P.launches.size(); ++i) {
+        hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+        if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
+                                         hipGetErrorString(e));
+    }
+    return FS_OK;
+}
+
+fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
+                          float *d_out, void *d_workspace, size_t workspace_bytes, void *stream, int32_t reps,
+                          float *h_launch_ms, int32_t capacity)
+{
+    if (reps < 1 || capacity < 0 || (!h_launch_ms && capacity > 0))
+        return fail(FS_ERR_INVALID_ARG, "bad reps / output");
+    Plan P;
+    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, P);
+    if (st != FS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int n = (int)P.launches.size();
+    std::vector<hipEvent_t> ev((size_t)(n + 1) * reps, nullptr);
+    hipError_t e = hipSuccess;
+    for (auto &x : ev) {
+        e = hipEventCreate(&x);
+        if (e != hipSuccess) break;
+    }
+    for (int r = 0; r < reps && e == hipSuccess; ++r) {
+        hipEvent_t *E = &ev[(size_t)r * (n + 1)];
+        e = hipEventRecord(E[0], s);
+        for (int i = 0; i < n && e == hipSuccess; ++i) {
+            e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+            if (e == hipSuccess) e = hipEventRecord(E[i + 1], s);
+        }
+    }
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    std::vector<double> acc(n, 0.0);
+    for (int r = 0; r < reps && e == hipSuccess; ++r) {
+        hipEvent_t *E = &ev[(size_t)r * (n + 1)];
+        for (int i = 0; i < n && e == hipSuccess; ++i) {
+            float ms = 0.f;
+            e = hipEventElapsedTime(&ms, E[i], E[i + 1]);
+            acc[i] += ms;
+        }
+    }
+    for (auto &x : ev)
+        if (x) (void)hipEventDestroy(x);
+    if (e != hipSuccess) return hip_fail(e, "profiled scan");
+    for (int i = 0; i < std::min(n, (int)capacity); ++i) h_launch_ms[i] = (float)(acc[i] / reps);
+    return FS_OK;
+}
+
+fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_out, size_t capacity,
+                            size_t *n_needed)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    Plan P;
+    fs_status st = make_plan(net, 1, H, W, P);
+    if (st != FS_OK) return st;
+    const int np = (int)net->pool_k.size();
+    const size_t rec = 5 + 2 * (size_t)np;
+    const size_t need = rec * net->F;
+    if (n_needed) *n_needed = need;
+    if (!h_out) return FS_OK;
+    // final per-axis sizes: replay the size recursion on one axis table each
+    std::vector<int> ey{H}, ex{W};
+    for (const NetLayer &l : net->L) {
+        if (l.kind == FS_MAXPOOL) {
+            std::vector<int> ny, nx;
+            for (size_t i = 0; i < ey.size(); ++i)
+                for (int o = 0; o < l.k; ++o) {
+                    ny.push_back(std::max(ey[i] - o, 0) / l.k);
+                    nx.push_back(std::max(ex[i] - o, 0) / l.k);
+                }
+            ey.swap(ny);
+            ex.swap(nx);
+        } else {
+            for (auto &v : ey) v = std::max(v - (l.k - 1), 0);
+            for (auto &v : ex) v = std::max(v - (l.k - 1), 0);
+        }
+    }
+    std::vector<int32_t> r(rec);
+    for (int f = 0; f < net->F; ++f) {
+        // digits of f, first pool most significant: d_m = o_y * k_m + o_x
+        std::vector<int> ox(np), oy(np);
+        int rest = f;
+        for (int m = np - 1; m >= 0; --m) {
+            const int k = net->pool_k[m];
+            const int d = rest % (k * k);
+            rest /= k * k;
+            ox[m] = d % k;
+            oy[m] = d / k;
+        }
+        int fy = 0, fx = 0, Y0 = 0, X0 = 0, S = 1;
+        for (int m = 0; m < np; ++m) {
+            const int k = net->pool_k[m];
+            fy = fy * k + oy[m];
+            fx = fx * k + ox[m];
+            Y0 += oy[m] * S;
+            X0 += ox[m] * S;
+            S *= k;
+        }
+        r[0] = f;
+        r[1] = ey[fy];
+        r[2] = ex[fx];
+        r[3] = Y0;
+        r[4] = X0;
+        for (int m = 0; m < np; ++m) {
+            r[5 + 2 * m] = ox[m];
+            r[6 + 2 * m] = oy[m];
+        }
+        const size_t base = (size_t)f * rec;
+        for (size_t j = 0; j < rec && base + j < capacity; ++j) h_out[base + j] = r[j];
+    }
+    return FS_OK;
+}
+
+fs_status fs_reassembly_index(const fs_net *net, int32_t H, int32_t W, int32_t *h_out, size_t capacity,
+                              size_t *n_needed)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    Plan P;
+    fs_status st = make_plan(net, 1, H, W, P);
+    if (st != FS_OK) return st;
+    const size_t need = (size_t)3 * P.ny * P.nx;
+    if (n_needed) *n_needed = need;
+    if (!h_out) return FS_OK;
+    const int np = (int)net->pool_k.size();
+    for (int Y = 0; Y < P.ny; ++Y)
+        for (int X = 0; X < P.nx; ++X) {
+            int f = 0, ry = Y, rx = X;
+            for (int m = 0; m < np; ++m) {
+                const int k = net->pool_k[m];
+                f = f * k * k + (ry % k) * k + (rx % k);
+                ry /= k;
+                rx /= k;
+            }
+            const size_t base = ((size_t)Y * P.nx + X) * 3;
+            const int32_t v[3] = {f, ry, rx};
+            for (int j = 0; j < 3 && base + j < capacity; ++j) h_out[base + j] = v[j];
+        }
+    return FS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,98 @@
+// Internal declarations shared by the host planner (api.hip) and the kernels.
+//
+// Data layout of every layer's activations ("fragment batch"):
+//   [B * F][Hmax][Wmax][C], channels innermost,
+// where F is the number of fragments per image at that layer, Hmax x Wmax the
+// largest fragment size, and the fragment of image b with per-axis indices
+// (fy, fx) sits at batch index b * F + fy * Q + fx (Q = product of the pool
+// sizes so far, F = Q * Q).  Fragment sizes are separable: a fragment's height
+// depends only on its y-offset chain and its width only on its x-offset chain,
+// so one table per axis (indexed by fy or fx) holds every fragment's true
+// size.  Pixels beyond a fragment's true size are padding: never read for a
+// valid output and never written.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fs {
+
+constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of pool sizes)
+constexpr int kMaxHeadClasses = 16;
+constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
+
+enum ActKind { ACT_NONE = 0, ACT_TANH = 1, ACT_SOFTMAX = 2 };
+enum DType { DT_F32 = 0, DT_BF16 = 1 };
+
+// Per-axis true sizes of the fragments a launch reads.
+struct AxisTable {
+    uint16_t y[kMaxAxis];
+    uint16_t x[kMaxAxis];
+};
+
+// Fragment-batched convolution (also the fully connected layers, as
+// convolutions with k = size of the map they receive).
+struct ConvArgs {
+    const void *in;       // [nfrag][in_h][in_w][in_c] (float or bf16; first layer: the image)
+    void *out;            // [nfrag][out_h][out_w][cout]
+    const void *w;        // swizzled weights (see api.hip: swizzle_conv_weights)
+    const float *bias;    // [nbt * 16], zero padded
+    int nfrag;            // B * F
+    int F, Q;             // fragments per image, per axis
+    int in_h, in_w, in_c; // padded input dims; in_c = channel pitch of the input
+    int out_h, out_w;     // padded output dims
+    int k, cin, cout, act;
+    int ksteps;           // K steps of the matrix-core loop
+    int nbt;              // total 16-wide output-channel blocks
+    int band_w;           // output columns per band
+    int nbands;           // bands per fragment
+    int tiles_per_band;   // tiles per band (enough for the tallest fragment)
+    int mt;               // output pixels per tile (64 * MB)
+    int lds_cs;           // channel stride of a pixel in LDS (elements)
+    int lds_bytes;        // dynamic LDS bytes of one workgroup
+    AxisTable ext;        // true sizes of the input fragments
+};
+
+struct PoolArgs {
+    const void *in;      // parents  [B*F][in_h][in_w][C]
+    void *out;           // children [B*F*k*k][out_h][out_w][C]
+    int F, Q;            // parents per image, per axis
+    int in_h, in_w;
+    int out_h, out_w;
+    int C, k;
+    int n_children;      // B * F * k * k
+    AxisTable ext;       // true sizes of the parents
+};
+
+// Last stage: (optionally) the last 1x1 layer, its activation, and the
+// reassembly of final fragments into the dense output map.
+struct HeadArgs {
+    const void *in;      // final fragments [B*F][in_h][in_w][C]
+    float *out;          // [B][ny][nx][ncls]
+    const float *w;      // [ncls][C] (has_fc) or unused
+    const float *bias;   // [ncls]
+    int B, F, Q;
+    int in_h, in_w, C;
+    int ny, nx, ncls, act;
+    int S;               // product of pool sizes
+    uint16_t digit_map[kMaxAxis];  // output coordinate mod S -> per-axis fragment index
+};
+
+// Launchers (return hipSuccess or the launch error).  `dtype` selects the
+// operand type; `in_f32` says the input is float32 even in a bf16 net (the
+// image).
+hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, bool vec,
+                       int grid_x, int grid_y, hipStream_t s);
+hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
+hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
+                       hipStream_t s);
+
+// Names the profiler shows for a launch (best effort, for reports).
+const char *conv_kernel_name(int dtype, bool in_f32, int mb, int nb, bool vec);
+const char *pool_kernel_name(int dtype, bool in_f32);
+const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
+
+// Supported (mb, nb) register tiles of the convolution kernel.
+bool conv_tile_supported(int mb, int nb);
+
+}  // namespace fs

@@ -1,0 +1,133 @@
+// Fragmenting max-pool (Section 2.2.2).
+//
+// A k x k max-pooling layer turns every input fragment into k^2 output
+// fragments, one per offset (o_x, o_y) in {0..k-1}^2.  Child pixel
+// (xbar, ybar) is the maximum of the parent's pixels with
+//   o_x + k*xbar <= x <= o_x + k*xbar + k - 1 and the same in y       (Eq. 5)
+// and the child's size is div(s - o, k) per axis (Eqs. 6-7), never below 0.
+//
+// One workgroup writes one row of one child: the row is a contiguous run of
+// w_c * C elements, so stores are fully coalesced; the k parent rows it reads
+// are contiguous runs too (neighbouring threads take neighbouring channel
+// vectors, then neighbouring pixels), and the k^2 siblings that read the same
+// parent rows are adjacent in the grid, so the overlap is served from cache.
+// Max is exact in any precision: bf16 values are compared as floats and
+// stored back unchanged.
+#include "fs_internal.h"
+
+namespace fs {
+namespace {
+
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// V = elements per thread per access (4 x f32 or 8 x bf16 = 16 bytes; 1 = scalar)
+template <bool BF, bool IN_F32, int V>
+__global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
+{
+    using TO = typename std::conditional<BF, uint16_t, float>::type;
+    using TI = typename std::conditional<IN_F32, float, TO>::type;
+
+    const int kk = a.k * a.k;
+    // blockIdx.x = ((b * F + f) * k*k + o) * out_h + ybar, grouped so that the
+    // k^2 children of a parent row band are neighbours:
+    const int ybar = blockIdx.x % a.out_h;
+    const int rest = blockIdx.x / a.out_h;
+    const int o = rest % kk;
+    const int p = rest / kk;            // parent batch index b * F + fy * Q + fx
+    const int oy = o / a.k, ox = o - (o / a.k) * a.k;
+    const int b = p / a.F;
+    const int rem = p - b * a.F;
+    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
+    const int hp = a.ext.y[fy], wp = a.ext.x[fx];
+    const int hc = hp >= oy ? (hp - oy) / a.k : 0;
+    const int wc = wp >= ox ? (wp - ox) / a.k : 0;
+    if (ybar >= hc || wc <= 0) return;
+
+    // child batch index in the (fy * k + oy, fx * k + ox) grid of Q * k per axis
+    const int Qc = a.Q * a.k;
+    const size_t child = (size_t)b * a.F * kk + (size_t)(fy * a.k + oy) * Qc + (fx * a.k + ox);
+
+    const TI *src = reinterpret_cast<const TI *>(a.in) +
+                    ((size_t)p * a.in_h + (oy + a.k * ybar)) * a.in_w * a.C;
+    TO *dst = reinterpret_cast<TO *>(a.out) + (child * a.out_h + ybar) * a.out_w * a.C;
+    const size_t prow = (size_t)a.in_w * a.C;
+
+    const int nv = a.C / V;
+    const int total = wc * nv;
+    for (int idx = threadIdx.x; idx < total; idx += 256) {
+        const int xbar = idx / nv;
+        const int cv = idx - xbar * nv;
+        const size_t base = (size_t)(ox + a.k * xbar) * a.C + cv * V;
+        float m[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) m[e] = -INFINITY;
+        for (int i = 0; i < a.k; ++i) {
+            for (int j = 0; j < a.k; ++j) {
+                const TI *s = src + i * prow + base + (size_t)j * a.C;
+                if constexpr (V == 1) {
+                    float v;
+                    if constexpr (!BF || IN_F32) v = s[0]; else v = bf2f(s[0]);
+                    m[0] = fmaxf(m[0], v);
+                } else {
+                    u4 raw = *reinterpret_cast<const u4 *>(s);
+                    if constexpr (BF) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            m[2 * e] = fmaxf(m[2 * e], bf2f((uint16_t)(raw[e] & 0xffffu)));
+                            m[2 * e + 1] = fmaxf(m[2 * e + 1], bf2f((uint16_t)(raw[e] >> 16)));
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) m[e] = fmaxf(m[e], __uint_as_float(raw[e]));
+                    }
+                }
+            }
+        }
+        TO *d = dst + (size_t)xbar * a.C + cv * V;
+        if constexpr (V == 1) {
+            if constexpr (BF) d[0] = f2bf(m[0]); else d[0] = m[0];
+        } else {
+            u4 w;
+            if constexpr (BF) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (uint32_t)f2bf(m[2 * e]) | ((uint32_t)f2bf(m[2 * e + 1]) << 16);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = __float_as_uint(m[e]);
+            }
+            *reinterpret_cast<u4 *>(d) = w;
+        }
+    }
+}
+
+template <bool BF, bool IN_F32, int V>
+hipError_t go(const PoolArgs &a, int grid, hipStream_t s)
+{
+    hipLaunchKernelGGL((pool_frag<BF, IN_F32, V>), dim3(grid), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s)
+{
+    if (dtype == DT_F32) return (a.C % 4 == 0) ? go<false, false, 4>(a, grid, s) : go<false, false, 1>(a, grid, s);
+    if (in_f32) return go<true, true, 1>(a, grid, s);
+    return (a.C % 8 == 0) ? go<true, false, 8>(a, grid, s) : go<true, false, 1>(a, grid, s);
+}
+
+const char *pool_kernel_name(int dtype, bool in_f32)
+{
+    return dtype == DT_F32 ? "pool_frag<f32>" : (in_f32 ? "pool_frag<bf16<-f32>" : "pool_frag<bf16>");
+}
+
+}  // namespace fs

@@ -1,0 +1,233 @@
+"""Python binding of libfragscan.so (include/fragscan.h).
+
+Argument marshalling only: PyTorch supplies device memory and the current
+stream; every step of the scan runs in the library's HIP kernels.  Names mirror
+the C entry points (fs_net_create -> Net, fs_scan -> Net.scan, ...).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfragscan.so")
+
+FS_OK, FS_ERR_INVALID_ARG, FS_ERR_SHAPE, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE, FS_ERR_OOM, FS_ERR_HIP = range(7)
+KIND = {"conv": 0, "pool": 1, "fc": 2}
+ACT = {"none": 0, "tanh": 1, "softmax": 2}
+DTYPE = {"f32": 0, "bf16": 1}
+
+
+class FsError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__("fragscan status %d: %s" % (status, msg))
+        self.status = status
+
+
+class fs_layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("k", ctypes.c_int32), ("c_in", ctypes.c_int32),
+                ("c_out", ctypes.c_int32), ("act", ctypes.c_int32),
+                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+
+
+class fs_net_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("patch", "in_channels", "n_classes", "n_layers",
+                                              "n_pools", "stride", "n_fragments", "dtype")]
+
+
+class fs_plan_info(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("out_h", ctypes.c_int32), ("out_w", ctypes.c_int32),
+                ("n_launches", ctypes.c_int32), ("workspace_bytes", ctypes.c_size_t),
+                ("flops", ctypes.c_double), ("min_bytes", ctypes.c_double)]
+
+
+class fs_launch_info(ctypes.Structure):
+    _fields_ = [("layer", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("kind", ctypes.c_int32),
+                ("fragments", ctypes.c_int32), ("out_pixels", ctypes.c_int64),
+                ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
+                ("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("name", ctypes.c_char * 64)]
+
+
+EXPORTS = ["fs_net_create", "fs_net_create_plan_only", "fs_net_destroy", "fs_net_query", "fs_scan_plan", "fs_scan_launches",
+           "fs_scan", "fs_scan_profile", "fs_fragment_table", "fs_reassembly_index",
+           "fs_status_str", "fs_last_error"]
+
+_lib = None
+
+
+def load():
+    """Load libfragscan.so; raises if it has not been built (no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libfragscan.so is not built (%s); run __graft_entry__.build() or "
+                           "python paper_1302_1700_amd/build.py" % LIB_PATH)
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, SZ, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
+    sig = {
+        "fs_net_create": [P(fs_layer), I32, I32, I32, I32, P(VP)],
+        "fs_net_create_plan_only": [P(fs_layer), I32, I32, I32, I32, P(VP)],
+        "fs_net_destroy": [VP],
+        "fs_net_query": [VP, P(fs_net_info)],
+        "fs_scan_plan": [VP, I32, I32, I32, P(fs_plan_info)],
+        "fs_scan_launches": [VP, I32, I32, I32, P(fs_launch_info), I32],
+        "fs_scan": [VP, VP, I32, I32, I32, VP, VP, SZ, VP],
+        "fs_scan_profile": [VP, VP, I32, I32, I32, VP, VP, SZ, VP, I32, P(ctypes.c_float), I32],
+        "fs_fragment_table": [VP, I32, I32, P(I32), SZ, P(SZ)],
+        "fs_reassembly_index": [VP, I32, I32, P(I32), SZ, P(SZ)],
+        "fs_status_str": [ctypes.c_int],
+        "fs_last_error": [],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.fs_net_destroy.restype = None
+    lib.fs_status_str.restype = ctypes.c_char_p
+    lib.fs_last_error.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def _check(st):
+    if st != FS_OK:
+        lib = load()
+        raise FsError(st, lib.fs_last_error().decode())
+
+
+def _stream_handle(stream=None):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Net:
+    """A net loaded into the library.
+
+    layers : list of layer dicts (kind, k, c_in, c_out, act), see workloads.py
+    params : per layer (weight OIHW float32, bias float32) or None for pools
+    in_channels, patch (0 = derive), dtype "f32" | "bf16".
+    Created on the current HIP device; plan_only=True makes a host-only handle
+    for planning and index queries (no device needed, cannot scan).
+    """
+
+    def __init__(self, layers, params, in_channels, patch=0, dtype="f32", plan_only=False):
+        lib = load()
+        self._keep = []
+        arr = (fs_layer * len(layers))()
+        for i, (L, p) in enumerate(zip(layers, params)):
+            arr[i].kind = KIND[L["kind"]]
+            arr[i].k = int(L["k"])
+            arr[i].c_in = int(L["c_in"])
+            arr[i].c_out = int(L["c_out"])
+            arr[i].act = ACT[L["act"]]
+            if p is not None:
+                w = np.ascontiguousarray(p[0], dtype=np.float32)
+                b = np.ascontiguousarray(p[1], dtype=np.float32) if p[1] is not None else None
+                self._keep += [w, b]
+                arr[i].weight = w.ctypes.data
+                arr[i].bias = b.ctypes.data if b is not None else None
+        h = ctypes.c_void_p()
+        create = lib.fs_net_create_plan_only if plan_only else lib.fs_net_create
+        _check(create(arr, len(layers), int(in_channels), int(patch), DTYPE[dtype], ctypes.byref(h)))
+        self._h = h
+        self._keep = None
+        self._ws = {}
+        info = fs_net_info()
+        _check(lib.fs_net_query(self._h, ctypes.byref(info)))
+        self.info = {n: getattr(info, n) for n, _ in fs_net_info._fields_}
+        self.patch = self.info["patch"]
+        self.n_classes = self.info["n_classes"]
+
+    def close(self):
+        if getattr(self, "_h", None):
+            load().fs_net_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # -- planning --------------------------------------------------------------
+    def plan(self, B, H, W):
+        p = fs_plan_info()
+        _check(load().fs_scan_plan(self._h, B, H, W, ctypes.byref(p)))
+        return {n: getattr(p, n) for n, _ in fs_plan_info._fields_}
+
+    def launches(self, B, H, W):
+        n = self.plan(B, H, W)["n_launches"]
+        arr = (fs_launch_info * n)()
+        _check(load().fs_scan_launches(self._h, B, H, W, arr, n))
+        out = []
+        for a in arr:
+            d = {n_: getattr(a, n_) for n_, _ in fs_launch_info._fields_}
+            d["name"] = a.name.decode()
+            out.append(d)
+        return out
+
+    def fragment_table(self, H, W):
+        lib = load()
+        need = ctypes.c_size_t()
+        _check(lib.fs_fragment_table(self._h, H, W, None, 0, ctypes.byref(need)))
+        buf = np.zeros(need.value, np.int32)
+        _check(lib.fs_fragment_table(self._h, H, W, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                     need.value, None))
+        rec = 5 + 2 * self.info["n_pools"]
+        return buf.reshape(-1, rec)
+
+    def reassembly_index(self, H, W):
+        lib = load()
+        need = ctypes.c_size_t()
+        _check(lib.fs_reassembly_index(self._h, H, W, None, 0, ctypes.byref(need)))
+        buf = np.zeros(need.value, np.int32)
+        _check(lib.fs_reassembly_index(self._h, H, W, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                       need.value, None))
+        return buf.reshape(H - self.patch + 1, W - self.patch + 1, 3)
+
+    # -- scanning --------------------------------------------------------------
+    def workspace(self, B, H, W, device=None):
+        import torch
+        nbytes = self.plan(B, H, W)["workspace_bytes"]
+        key = (nbytes, str(device))
+        ws = self._ws.get(key)
+        if ws is None:
+            self._ws.clear()
+            ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device or "cuda")
+            self._ws[key] = ws
+        return ws
+
+    def scan(self, image, out=None, workspace=None, stream=None):
+        """image: CUDA float32 tensor [B, H, W, C] (contiguous) -> [B, H-w0+1, W-w0+1, n]."""
+        import torch
+        if not image.is_cuda or image.dtype != torch.float32 or not image.is_contiguous():
+            raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
+        B, H, W, C = image.shape
+        if out is None:
+            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes),
+                              dtype=torch.float32, device=image.device)
+        ws = workspace if workspace is not None else self.workspace(B, H, W, image.device)
+        _check(load().fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                              ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                              ws.numel(), _stream_handle(stream)))
+        return out
+
+    def profile(self, image, reps=10, out=None, stream=None):
+        """Per-launch mean milliseconds of `reps` scans timed with HIP events
+        around every launch (synchronises)."""
+        import torch
+        B, H, W, C = image.shape
+        if out is None:
+            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes),
+                              dtype=torch.float32, device=image.device)
+        ws = self.workspace(B, H, W, image.device)
+        n = self.plan(B, H, W)["n_launches"]
+        ms = (ctypes.c_float * n)()
+        _check(load().fs_scan_profile(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                      ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                      ws.numel(), _stream_handle(stream), reps, ms, n))
+        return list(ms)

@@ -1,0 +1,178 @@
+"""Host-side checks of the C-ABI library (no GPU needed).
+
+The library must load and export every entry point include/fragscan.h
+declares; its host planner (fragment sizes, fragment table, reassembly index,
+work counts) must agree bit for bit with the oracle's independent index code;
+and its argument checks must reject bad input before any device work.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import index as ix
+from paper_1302_1700_amd import fragscan as fsb
+from paper_1302_1700_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "fragscan.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fs_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    lib = fsb.load()
+    names = _header_functions()
+    assert "fs_scan" in names and "fs_net_create" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) == set(fsb.EXPORTS)
+
+
+def _plan_net(layers, params=None, c0=1, patch=0, dtype="f32"):
+    if params is None:
+        params = wl.make_weights(layers, 0, 0.1)
+    return fsb.Net(layers, params, c0, patch, dtype, plan_only=True)
+
+
+def _check_tables(layers, H, W, c0=1):
+    net = _plan_net(layers, c0=c0)
+    w0 = ix.patch_size(layers)
+    assert net.patch == w0
+    # reassembly index, every output pixel
+    got = net.reassembly_index(H, W)
+    want = ix.reassembly_index(layers, H, W)
+    assert got.shape == want.shape
+    assert np.array_equal(got, want.astype(np.int32))
+    # fragment table
+    tab = net.fragment_table(H, W)
+    F = ix.n_fragments(layers)
+    assert tab.shape[0] == F
+    assert np.array_equal(tab[:, 0], np.arange(F))
+    ext = ix.fragment_extents(layers, H, W)[-1]
+    want_tab = ix.fragment_table(layers, H, W)
+    for row in tab:
+        f, h, w, Y0, X0 = (int(v) for v in row[:5])
+        assert (h, w) == ext[f]
+        if f in want_tab:
+            e = want_tab[f]
+            assert (h, w) == e["size"]
+            assert (Y0, X0) == e["base"]
+            offs = [(int(row[5 + 2 * m]), int(row[6 + 2 * m])) for m in range(len(e["offsets"]))]
+            assert offs == e["offsets"]
+        else:
+            assert h * w == 0
+    # plan: output size and algorithmic FLOPs
+    p = net.plan(2, H, W)
+    assert (p["out_h"], p["out_w"]) == (H - w0 + 1, W - w0 + 1)
+    assert p["flops"] == pytest.approx(sum(ix.algorithmic_flops(layers, 2, H, W)), rel=1e-12)
+    net.close()
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 5])
+def test_tables_workload_nets(wid):
+    w = wl.WORKLOADS[wid]
+    H = {1: 64, 2: 160, 3: 190, 5: 130}[wid]
+    _check_tables(w.layers, H, H + 7, w.channels)
+
+
+def test_tables_workload_full_sizes():
+    """Full-size workloads: sizes and work counts against the oracle's index
+    code (the per-pixel tables are compared on the smaller images above)."""
+    for wid, w in wl.WORKLOADS.items():
+        net = _plan_net(w.layers, c0=w.channels, dtype=w.dtype)
+        p = net.plan(w.batch, w.height, w.width)
+        assert p["out_h"] == w.out_h and p["out_w"] == w.out_w
+        assert p["flops"] == pytest.approx(sum(ix.algorithmic_flops(w.layers, w.batch, w.height, w.width)),
+                                           rel=1e-12)
+        ri = net.reassembly_index(w.height, w.width)
+        want = ix.reassembly_index(w.layers, w.height, w.width)
+        assert np.array_equal(ri, want.astype(np.int32))
+        net.close()
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_tables_random_nets(seed):
+    rng = np.random.default_rng(4000 + seed)
+    layers, w0, c0 = wl.random_net(rng)
+    H = w0 + int(rng.integers(0, 20))
+    W = w0 + int(rng.integers(0, 20))
+    _check_tables(layers, H, W, c0)
+
+
+def test_single_window_image():
+    """H = W = w_0: one output; all final fragments but one are empty."""
+    _check_tables(wl.WORKLOADS[2].layers, 95, 95)
+
+
+# ---- error paths (checked before any device work) ---------------------------
+
+def _status(layers, params=None, c0=1, patch=0, dtype="f32"):
+    try:
+        _plan_net(layers, params, c0, patch, dtype).close()
+        return fsb.FS_OK
+    except fsb.FsError as e:
+        return e.status
+
+
+def test_rejects_bad_nets():
+    # pool that does not divide the patch-level map (Section 2.1.2)
+    assert _status([wl.conv(2, 1, 2), wl.pool(2, 2), wl.fc(2, 2, 2)], patch=6) == fsb.FS_ERR_SHAPE
+    # workload 5 with its stated patch of 57: its 3x3 pool would see a 53 map
+    w5 = wl.WORKLOADS[5]
+    params5, _ = wl.workload_inputs(5, height=61, width=61)
+    assert _status(w5.layers, params5, 3, 57, "bf16") == fsb.FS_ERR_SHAPE
+    assert _status(w5.layers, params5, 3, 61, "bf16") == fsb.FS_OK
+    # channel mismatch
+    assert _status([wl.conv(2, 1, 3), wl.fc(2, 4, 2)]) == fsb.FS_ERR_SHAPE
+    # softmax before the last layer
+    assert _status([wl.conv(2, 1, 3, "softmax"), wl.fc(2, 3, 2)]) == fsb.FS_ERR_SHAPE
+    # last map not 1x1
+    assert _status([wl.conv(2, 1, 3), wl.fc(2, 3, 2)], patch=5) == fsb.FS_ERR_SHAPE
+    # convolution after a fully connected layer
+    assert _status([wl.fc(2, 1, 3), wl.conv(1, 3, 2)]) == fsb.FS_ERR_SHAPE
+    # more classes than the head supports
+    assert _status([wl.fc(2, 1, 17)]) == fsb.FS_ERR_UNSUPPORTED
+    # a net without pools is the plain whole-image case (Section 1)
+    assert _status([wl.conv(2, 1, 2, "none"), wl.fc(1, 2, 2)]) == fsb.FS_OK
+
+
+def test_image_smaller_than_patch_rejected():
+    net = _plan_net(wl.WORKLOADS[1].layers)
+    with pytest.raises(fsb.FsError) as e:
+        net.plan(1, 13, 64)
+    assert e.value.status == fsb.FS_ERR_SHAPE
+    net.close()
+
+
+def test_scan_argument_checks_without_device():
+    lib = fsb.load()
+    net = _plan_net(wl.WORKLOADS[1].layers)
+    p = net.plan(1, 64, 64)
+    img, out, ws = ctypes.c_void_p(1 << 20), ctypes.c_void_p(2 << 20), ctypes.c_void_p(4 << 20)
+    st = lib.fs_scan(net._h, img, 1, 64, 64, out, ws, p["workspace_bytes"] - 1, None)
+    assert st == fsb.FS_ERR_WORKSPACE
+    st = lib.fs_scan(net._h, ctypes.c_void_p((1 << 20) + 4), 1, 64, 64, out, ws, p["workspace_bytes"], None)
+    assert st == fsb.FS_ERR_INVALID_ARG
+    st = lib.fs_scan(net._h, img, 1, 64, 64, out, ctypes.c_void_p((4 << 20) + 16), p["workspace_bytes"], None)
+    assert st == fsb.FS_ERR_INVALID_ARG
+    st = lib.fs_scan(net._h, None, 1, 64, 64, out, ws, p["workspace_bytes"], None)
+    assert st == fsb.FS_ERR_INVALID_ARG
+    st = lib.fs_scan(net._h, img, 1, 10, 64, out, ws, p["workspace_bytes"], None)
+    assert st == fsb.FS_ERR_SHAPE
+    # a planning-only net never launches
+    st = lib.fs_scan(net._h, img, 1, 64, 64, out, ws, p["workspace_bytes"], None)
+    assert st == fsb.FS_ERR_INVALID_ARG
+    assert b"planning only" in lib.fs_last_error()
+    net.close()
+
+
+def test_status_strings():
+    lib = fsb.load()
+    for s in range(7):
+        assert lib.fs_status_str(s)
