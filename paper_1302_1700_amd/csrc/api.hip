@@ -16,6 +16,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -57,8 +58,9 @@ struct NetLayer {
     int w_in, w_out;      // patch-level map sizes (Sections 2.1.1, 2.1.2)
     // conv launch parameters fixed at creation
     bool vec = false;     // channel-vector path
-    int nb = 1;           // output-channel blocks per workgroup
-    int nbt = 0;          // channel blocks, padded to a multiple of nb
+    int nb = 1;           // output-channel blocks per wave
+    int wn = 1;           // waves across output channels
+    int nbt = 0;          // channel blocks, padded to a multiple of nb * wn
     int ksteps = 0;
     size_t w_off = 0, b_off = 0;  // offsets into the net's device block
 };
@@ -126,18 +128,42 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
                 }
 }
 
-int choose_nb(int nbt, bool vec)
+// Optional tile override for tuning sweeps: FRAGSCAN_TILE="L:MB,NB,WN[,BAND];..."
+// (L = layer index); any field <= 0 keeps the planner's choice.
+bool tile_override(int layer, int *mb, int *nb, int *wn, int *band)
 {
-    static const int cand_vec[] = {13, 8, 7, 4, 3, 2, 1};
-    static const int cand_gather[] = {4, 3, 2, 1};
-    const int *c = vec ? cand_vec : cand_gather;
-    const int nc = vec ? 7 : 4;
-    for (int i = 0; i < nc; ++i) {
-        const int nb = c[i];
-        const int pad = (nbt + nb - 1) / nb * nb;
-        if ((double)nbt / pad >= 0.8) return nb;
+    const char *env = getenv("FRAGSCAN_TILE");
+    if (!env) return false;
+    const char *p = env;
+    while (*p) {
+        int L = -1, a = 0, b = 0, c = 0, d = 0;
+        const int n = sscanf(p, "%d:%d,%d,%d,%d", &L, &a, &b, &c, &d);
+        if (n >= 4 && L == layer) {
+            if (mb && a > 0) *mb = a;
+            if (nb && b > 0) *nb = b;
+            if (wn && c > 0) *wn = c;
+            if (band && n >= 5 && d > 0) *band = d;
+            return true;
+        }
+        const char *semi = strchr(p, ';');
+        if (!semi) break;
+        p = semi + 1;
     }
-    return 1;
+    return false;
+}
+
+// Output-channel split of a conv layer: nb blocks of 16 channels per wave and
+// wn waves across the channels; the channel blocks are padded to nb * wn.
+void choose_channel_tile(int nbt, bool vec, int *nb, int *wn)
+{
+    if (!vec || nbt <= 4) {
+        *wn = 1;
+        *nb = std::min(nbt, 4);
+        if (*nb == 0) *nb = 1;
+        return;
+    }
+    *wn = 2;
+    *nb = nbt <= 8 ? 4 : 7;
 }
 
 // ---------------------------------------------------------------------------
@@ -159,7 +185,7 @@ struct Launch {
     ConvArgs conv;
     PoolArgs pool;
     HeadArgs head;
-    int mb = 0, nb = 0;
+    int mb = 0, nb = 0, wn = 1;
     bool vec = false, has_fc = false;
     int gx = 1, gy = 1;
     int frags = 0;
@@ -202,19 +228,35 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     const int hout_max = in.hmax - k + 1, wout_max = in.wmax - k + 1;
     const int es = elem_of(net->dtype);
     const int KSTEP = kstep_of(net->dtype);
-    const int cs = l.vec ? l.cin + 16 / es : l.cin;  // +16 bytes per pixel spreads LDS banks
+    // pixel stride in LDS: +16 bytes per pixel spreads 16 consecutive pixels'
+    // 16-byte reads over distinct banks (FRAGSCAN_LDS_PAD overrides, elements)
+    int pad = 16 / es;
+    if (const char *e = getenv("FRAGSCAN_LDS_PAD")) pad = atoi(e) / (l.vec ? 1 : 1);
+    if (l.vec && (pad * es) % 16) pad = 16 / es;
+    const int cs = l.vec ? l.cin + pad : l.cin;
     const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
     // distinct output widths present
     std::vector<int> wouts;
     for (int v : in.ex)
         if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
             wouts.push_back(v - k + 1);
-    const int mbs[3] = {2, 4, 1};
-    for (int mi = 0; mi < 3; ++mi) {
-        const int mb = mbs[mi];
-        if (!conv_tile_supported(mb, l.nb)) continue;
-        const int mt = 64 * mb;
-        int nbands = wout_max <= 64 ? 1 : (wout_max + 31) / 32;
+    const int wm = 4 / l.wn;
+    int mb_force = 0, band_force = 0;
+    tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
+    // two pixel blocks per wave first (measured best on the N4 layers), then
+    // the neighbours
+    const int mbs[4] = {2, 4, 1, 8};
+    for (int mi = 0; mi < 4; ++mi) {
+        const int mb = mb_force ? mb_force : mbs[mi];
+        if (!conv_tile_supported(mb, l.nb, l.wn, l.vec)) {
+            if (mb_force) break;
+            continue;
+        }
+        const int mt = 16 * mb * wm;
+        // bands of about 16 columns keep the window (and LDS) small enough
+        // for several workgroups per CU
+        int nbands = wout_max <= 32 ? 1 : (wout_max + 15) / 16;
+        if (band_force) nbands = (wout_max + band_force - 1) / band_force;
         for (; nbands <= wout_max; ++nbands) {
             const int band_w = (wout_max + nbands - 1) / nbands;
             int tmin = band_w;
@@ -230,15 +272,17 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                 if (band_w <= 8) break;
                 continue;
             }
+            const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;  // fused-head reduction
             L.mb = mb;
             L.conv.band_w = band_w;
             L.conv.nbands = nbands;
             L.conv.mt = mt;
             L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
             L.conv.lds_cs = cs;
-            L.conv.lds_bytes = (int)lds;
+            L.conv.lds_bytes = (int)std::max(lds, red);
             return FS_OK;
         }
+        if (mb_force) break;
     }
     return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile fits in LDS", L.layer);
 }
@@ -267,6 +311,13 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
 
     const int nl = (int)net->L.size();
     const int body = net->head_fc ? nl - 1 : nl;
+    // the last 1x1 layer goes into the epilogue of the layer before it when
+    // that is a convolution whose workgroups cover all its channels
+    bool fuse = false;
+    if (net->head_fc && net->ncls <= kMaxFusedClasses && nl >= 2) {
+        const NetLayer &pl = net->L[nl - 2];
+        fuse = pl.kind != FS_MAXPOOL && pl.nbt == pl.nb * pl.wn && !getenv("FRAGSCAN_NO_FUSED_HEAD");
+    }
     int cur = -1;  // where the current activations live
     size_t buf = 0;
     for (int li = 0; li < body; ++li) {
@@ -326,6 +377,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.type = 0;
             L.vec = l.vec;
             L.nb = l.nb;
+            L.wn = l.wn;
             ConvArgs &a = L.conv;
             a.nfrag = B * F;
             a.F = F;
@@ -347,17 +399,44 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             fs_status st = plan_conv_tiles(net, l, g, L);
             if (st != FS_OK) return st;
             L.gx = B * F * a.nbands * a.tiles_per_band;
-            L.gy = l.nbt / l.nb;
+            L.gy = l.nbt / (l.nb * l.wn);
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
-            L.name = conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.vec);
+            L.name = conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.vec);
+            if (fuse && li == body - 1) {
+                const NetLayer &hl = net->L[nl - 1];
+                a.head_ncls = net->ncls;
+                a.head_act = hl.act;
+                a.ny = P.ny;
+                a.nx = P.nx;
+                a.S = net->S;
+                for (int f = 0; f < o.Q; ++f) {  // first output coordinate of axis index f
+                    int rest = f, base = 0, S = net->S;
+                    for (int m = (int)net->pool_k.size() - 1; m >= 0; --m) {
+                        const int k2 = net->pool_k[m];
+                        S /= k2;
+                        base += (rest % k2) * S;
+                        rest /= k2;
+                    }
+                    a.base[f] = (uint16_t)base;
+                }
+                L.dst = 2;
+                L.n_layers = 2;
+                const long long npix = (long long)B * P.ny * P.nx;
+                L.flops += (double)npix * 2.0 * hl.cin * hl.cout;
+                L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)npix * net->ncls * 4 +
+                          (double)l.cin * k * k * l.cout * es;
+                L.name += "+head";
+            }
         }
         o.is_image = false;
-        const size_t out_bytes = (size_t)B * o.Q * o.Q * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
-        buf = std::max(buf, out_bytes);
+        if (L.dst != 2) {
+            const size_t out_bytes = (size_t)B * o.Q * o.Q * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
+            buf = std::max(buf, out_bytes);
+        }
         P.flops += L.flops;
         P.bytes += L.bytes;
         P.launches.push_back(L);
@@ -366,7 +445,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
     }
 
     // head: the (fused) last layer, its activation, and the reassembly
-    {
+    if (!fuse) {
         Launch L{};
         L.type = 2;
         L.layer = net->head_fc ? nl - 1 : nl;
@@ -457,7 +536,13 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
         L.conv.out = ptr(L.dst);
         L.conv.w = mem + l.w_off;
         L.conv.bias = reinterpret_cast<const float *>(mem + l.b_off);
-        return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.vec, L.gx, L.gy, s);
+        if (L.conv.head_ncls > 0) {
+            L.conv.head_w = reinterpret_cast<const float *>(mem + net->head_w_off);
+            L.conv.head_b = reinterpret_cast<const float *>(mem + net->head_b_off);
+            L.conv.head_out = d_out;
+            L.conv.out = nullptr;
+        }
+        return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.vec, L.gx, L.gy, s);
     }
     if (L.type == 1) {
         L.pool.in = ptr(L.src);
@@ -623,8 +708,16 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         // staging, which the gather path does
         l.vec = (l.cin % KSTEP) == 0 && !(dtype == FS_BF16 && i == 0);
         const int nbt0 = (l.cout + 15) / 16;
-        l.nb = choose_nb(nbt0, l.vec);
-        l.nbt = (nbt0 + l.nb - 1) / l.nb * l.nb;
+        choose_channel_tile(nbt0, l.vec, &l.nb, &l.wn);
+        tile_override(i, nullptr, &l.nb, &l.wn, nullptr);
+        if (!conv_tile_supported(1, l.nb, l.wn, l.vec) && !conv_tile_supported(2, l.nb, l.wn, l.vec) &&
+            !conv_tile_supported(4, l.nb, l.wn, l.vec) && !conv_tile_supported(8, l.nb, l.wn, l.vec)) {
+            delete net;
+            return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile with %d x %d channel blocks", i,
+                        l.nb, l.wn);
+        }
+        const int grp = l.nb * l.wn;
+        l.nbt = (nbt0 + grp - 1) / grp * grp;
         l.ksteps = l.vec ? l.k * l.k * (l.cin / KSTEP) : (l.k * l.k * l.cin + KSTEP - 1) / KSTEP;
         std::vector<uint8_t> pw;
         pack_conv_weights(l, s.weight, dtype, pw);

@@ -1,0 +1,42 @@
+// float32 instances of the fragment-batched convolution (conv_impl.h) and the
+// convolution launcher.
+#include "conv_impl.h"
+
+#include <cstdio>
+
+namespace fs {
+
+hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int wn, bool vec, int gx, int gy,
+                            hipStream_t s);
+
+bool conv_tile_supported(int mb, int nb, int wn, bool vec)
+{
+#define FS_CONV_HAS(M, N, W) \
+    if (mb == M && nb == N && wn == W) return true;
+    if (vec) {
+        FS_CONV_TILES_VEC(FS_CONV_HAS)
+    } else {
+        FS_CONV_TILES_GATHER(FS_CONV_HAS)
+    }
+#undef FS_CONV_HAS
+    return false;
+}
+
+hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, bool vec, int gx,
+                       int gy, hipStream_t s)
+{
+    if (dtype == DT_BF16) return launch_conv_bf16(a, in_f32, mb, nb, wn, vec, gx, gy, s);
+    return vec ? conv::dispatch_tile<false, false, true>(a, mb, nb, wn, gx, gy, s)
+               : conv::dispatch_tile<false, false, false>(a, mb, nb, wn, gx, gy, s);
+}
+
+std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, bool vec)
+{
+    char buf[96];
+    const bool bf = dtype == DT_BF16;
+    snprintf(buf, sizeof buf, "conv_frag_mfma<%d, %d, %d, %s, %s, %s>", mb, nb, wn, bf ? "true" : "false",
+             bf && in_f32 ? "true" : "false", vec ? "true" : "false");
+    return buf;
+}
+
+}  // namespace fs

@@ -1,0 +1,458 @@
+// Fragment-batched convolution on the CDNA4 matrix cores (implicit GEMM).
+// Included by conv_f32.hip and conv_bf16.hip, which instantiate it.
+//
+// Section 2.2.1: a convolutional layer keeps the fragment count and convolves
+// each fragment's extended maps exactly as a patch is convolved; the sizes
+// shrink by k - 1 per axis (Eqs. 3-4).  Fully connected layers run through the
+// same kernel as convolutions whose kernel covers the patch-level map.
+//
+// As a matrix product, per layer: M = output pixels of all fragments (the
+// fragments are the batch), N = c_out, K = c_in * k * k, with
+//   out[q, y, x, co] = act(bias[co] + sum_{dy, dx, ci} W[co, ci, dy, dx] * in[q, y+dy, x+dx, ci]).
+//
+// Work split
+//   - A fragment's output columns are cut into bands of `band_w` columns; the
+//     pixels of a band are numbered row-major and cut into tiles of `mt`
+//     pixels.  Tiles follow the fragment's true size, with waste only at the
+//     end of a band.
+//   - The workgroup (4 waves) stages the input window its tile needs (the
+//     rows its pixels touch plus k - 1, band + k - 1 columns, all c_in
+//     channels) in LDS once, zero-filled outside the fragment's true size.
+//   - The 4 waves form a WM x WN grid: wave (wm, wn) computes MB blocks of 16
+//     pixels (m-blocks wm*MB ..) times NB blocks of 16 output channels
+//     (n-blocks wn*NB ..), so waves in a row share pixels and waves in a
+//     column share weights.  Products use v_mfma_f32_16x16x4_f32 (float32) or
+//     v_mfma_f32_16x16x32_bf16 (bfloat16 operands, float32 accumulate).
+//   - A lane (lm = lane % 16, g = lane / 16) feeds pixel lm of each m-block and
+//     16 bytes of consecutive K values starting at g * (KSTEP / 4); float32
+//     uses element e of that vector in the e-th of 4 products, so each product
+//     sums over K indices {4g + e}.  The weights are pre-arranged on the host
+//     so that each (K step, channel block) is one contiguous 1 KB run, read by
+//     a wave in one coalesced load; the next step's weights and pixels are
+//     loaded while the current step's products run.
+//   - Vector path (c_in a multiple of KSTEP): K is walked tap by tap, KSTEP
+//     channels at a time, and a lane's A operand is one 16-byte LDS read.
+//     Gather path (small c_in, e.g. the first layer): K = (tap, channel)
+//     flattened and padded to KSTEP, gathered through an LDS offset table.
+//   - Epilogue: bias and tanh in float32; stores (bf16: round to nearest even)
+//     only inside the fragment's true size.
+#pragma once
+
+#include "fs_internal.h"
+
+#include <type_traits>
+
+namespace fs {
+namespace conv {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f2bf(float f)
+{
+    // round to nearest even; inputs here are finite
+    uint32_t u = __float_as_uint(f);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <bool BF>
+struct Elem;
+template <>
+struct Elem<false> {
+    using T = float;
+    static constexpr int KSTEP = 16;
+};
+template <>
+struct Elem<true> {
+    using T = uint16_t;
+    static constexpr int KSTEP = 32;
+};
+
+// Fused last layer.  The tile's activations act(acc + bias) never leave the
+// registers: every lane multiplies its values (pixels 4g + e of each m-block,
+// channel lm of each n-block) by the last layer's weights, the 16 lanes of a
+// row (same pixels, 16 channels) are summed with xor shuffles, the waves that
+// split the channels add up through LDS, and one thread per pixel applies the
+// last activation (softmax: exp(z - max z) / sum) and writes the pixel's
+// classes to the dense map at the window corner the pixel stands for: final
+// fragment (fy, fx) position (y, x) holds window (base[fy] + S*y, base[fx] + S*x).
+template <int MB, int NB, int WN>
+__device__ __forceinline__ void fused_head(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm, int wn,
+                                           int lm, int g, int q, int fy, int fx, int l0, int lend, int twb,
+                                           int c0, float *red)
+{
+    constexpr int NC = kMaxFusedClasses;
+    const int ncls = a.head_ncls;
+    float part[MB][4][NC];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) part[i][e][c] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int co = (nb0 + j) * 16 + lm;
+        if (co >= a.cout) continue;
+        const float bv = a.bias[co];
+        float w2[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) w2[c] = c < ncls ? a.head_w[c * a.cout + co] : 0.f;
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                float v = acc[i][j][e] + bv;
+                if (a.act == ACT_TANH) v = tanhf(v);
+#pragma unroll
+                for (int c = 0; c < NC; ++c) part[i][e][c] = fmaf(w2[c], v, part[i][e][c]);
+            }
+    }
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                float t = part[i][e][c];
+                t += __shfl_xor(t, 8);
+                t += __shfl_xor(t, 4);
+                t += __shfl_xor(t, 2);
+                t += __shfl_xor(t, 1);
+                part[i][e][c] = t;
+            }
+    const int mt = a.mt;
+    __syncthreads();  // the LDS window is no longer read
+    if (lm == 0) {
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int m = (wm * MB + i) * 16 + 4 * g + e;
+#pragma unroll
+                for (int c = 0; c < NC; ++c) red[((size_t)wn * mt + m) * NC + c] = part[i][e][c];
+            }
+    }
+    __syncthreads();
+    const int b = q / a.F;
+    for (int m = threadIdx.x; m < mt; m += 256) {
+        const int l = l0 + m;
+        if (l >= lend) break;
+        float z[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            float t = c < ncls ? a.head_b[c] : 0.f;
+#pragma unroll
+            for (int w = 0; w < WN; ++w) t += red[((size_t)w * mt + m) * NC + c];
+            z[c] = t;
+        }
+        if (a.head_act == ACT_SOFTMAX) {
+            float mx = z[0];
+#pragma unroll
+            for (int c = 1; c < NC; ++c)
+                if (c < ncls) mx = fmaxf(mx, z[c]);
+            float sum = 0.f;
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                if (c < ncls) {
+                    z[c] = expf(z[c] - mx);
+                    sum += z[c];
+                }
+            const float inv = 1.0f / sum;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) z[c] *= inv;
+        } else if (a.head_act == ACT_TANH) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c) z[c] = tanhf(z[c]);
+        }
+        const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+        const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
+        float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * ncls;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            if (c < ncls) dst[c] = z[c];
+    }
+}
+
+template <int MB, int NB, int WN, bool BF, bool IN_F32, bool VEC>
+__global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
+{
+    using TC = typename Elem<BF>::T;                                // LDS / operand element
+    using TI = typename std::conditional<IN_F32, float, TC>::type;  // global input element
+    constexpr int KSTEP = Elem<BF>::KSTEP;
+    constexpr int LPE = KSTEP / 4;  // elements per lane per K step (16 bytes)
+
+    extern __shared__ __align__(16) unsigned char smem[];
+
+    int bid = blockIdx.x;
+    const int t = bid % a.tiles_per_band;
+    bid /= a.tiles_per_band;
+    const int band = bid % a.nbands;
+    const int q = bid / a.nbands;
+
+    const int rem = q % a.F;
+    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
+    const int hin = a.ext.y[fy], win = a.ext.x[fx];
+    const int hout = hin - a.k + 1, wout = win - a.k + 1;
+    if (hout <= 0 || wout <= 0) return;
+    const int c0 = band * a.band_w;
+    const int twb = min(a.band_w, wout - c0);
+    if (twb <= 0) return;
+    const int npix = hout * twb;
+    const int l0 = t * a.mt;
+    if (l0 >= npix) return;
+    const int lend = min(l0 + a.mt, npix);
+    const int yfirst = l0 / twb;
+    const int ylast = (lend - 1) / twb;
+    const int R = ylast - yfirst + a.k;  // window rows
+    const int Cc = twb + a.k - 1;        // window columns
+    const int CS = a.lds_cs;
+    const int kk_total = a.ksteps * KSTEP;
+
+    int *offtab = reinterpret_cast<int *>(smem);
+    TC *win_lds = reinterpret_cast<TC *>(smem + (VEC ? 0 : ((kk_total * 4 + 15) & ~15)));
+
+    // ---- stage the input window ----------------------------------------------
+    const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * a.in_h * a.in_w * a.in_c;
+    if constexpr (VEC && !IN_F32) {
+        const int nvec = a.cin / LPE;
+        const int total = R * Cc * nvec;
+        for (int idx = threadIdx.x; idx < total; idx += 256) {
+            const int v = idx % nvec;
+            const int p = idx / nvec;
+            const int c = p % Cc, r = p / Cc;
+            const int gy = yfirst + r, gx = c0 + c;
+            u4 val = {0u, 0u, 0u, 0u};
+            if (gy < hin && gx < win)
+                val = *reinterpret_cast<const u4 *>(inp + ((size_t)gy * a.in_w + gx) * a.in_c + v * LPE);
+            *reinterpret_cast<u4 *>(win_lds + (r * Cc + c) * CS + v * LPE) = val;
+        }
+    } else {
+        const int total = R * Cc * a.cin;
+        for (int idx = threadIdx.x; idx < total; idx += 256) {
+            const int ci = idx % a.cin;
+            const int p = idx / a.cin;
+            const int c = p % Cc, r = p / Cc;
+            const int gy = yfirst + r, gx = c0 + c;
+            TC val = 0;
+            if (gy < hin && gx < win) {
+                TI x = inp[((size_t)gy * a.in_w + gx) * a.in_c + ci];
+                if constexpr (BF && IN_F32)
+                    val = f2bf(x);
+                else
+                    val = x;
+            }
+            win_lds[(r * Cc + c) * CS + ci] = val;
+        }
+    }
+    if constexpr (!VEC) {
+        for (int kk = threadIdx.x; kk < kk_total; kk += 256) {
+            const int tap = kk / a.cin, ci = kk - (kk / a.cin) * a.cin;
+            int off = -1;
+            if (tap < a.k * a.k) {
+                const int dy = tap / a.k, dx = tap - (tap / a.k) * a.k;
+                off = (dy * Cc + dx) * CS + ci;
+            }
+            offtab[kk] = off;
+        }
+    }
+    __syncthreads();
+
+    // ---- matrix-core main loop ----------------------------------------------
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int wm = wv / WN, wn = wv - (wv / WN) * WN;
+    const int lm = lane & 15, g = lane >> 4;
+    const int nb0 = blockIdx.y * (WN * NB) + wn * NB;
+
+    int abase[MB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+        const int l = l0 + (wm * MB + i) * 16 + lm;
+        if (l < lend) {
+            const int y = l / twb - yfirst, x = l - (l / twb) * twb;
+            abase[i] = (y * Cc + x) * CS + g * LPE;
+        } else {
+            abase[i] = g * LPE;  // any in-window address; the result is not stored
+        }
+    }
+
+    f4 acc[MB][NB];
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+
+    const u4 *wp = reinterpret_cast<const u4 *>(a.w) + (size_t)nb0 * 64 + lane;
+    const size_t wstep = (size_t)a.nbt * 64;  // u4 per K step
+
+    auto mma = [&](const u4(&av)[MB], const u4(&bv)[NB]) {
+        if constexpr (BF) {
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                        __builtin_bit_cast(bf8, av[i]), __builtin_bit_cast(bf8, bv[j]), acc[i][j], 0, 0, 0);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
+                            __uint_as_float(av[i][e]), __uint_as_float(bv[j][e]), acc[i][j], 0, 0, 0);
+        }
+    };
+
+    if constexpr (VEC) {
+        // K step s covers tap (dy, dx) and channels cc*KSTEP ..; the three
+        // indices advance incrementally.  Weights are loaded two steps ahead
+        // (two register buffers, the loop unrolled by two) and pixels one step
+        // ahead, so the products of a step never wait on the loads it needs.
+        const int ncc = a.cin / KSTEP;
+        const int nsteps = a.ksteps;
+        int dy = 0, dx = 0, cc = 0;
+        auto advance = [&](int off) {
+            if (++cc < ncc) return off + KSTEP;
+            cc = 0;
+            if (++dx < a.k) return off - (ncc - 1) * KSTEP + CS;
+            dx = 0;
+            ++dy;
+            return dy * Cc * CS;
+        };
+        u4 b0[NB], b1[NB], a0[MB], a1[MB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) b0[j] = wp[j * 64];
+        if (nsteps > 1) {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) b1[j] = wp[wstep + j * 64];
+        }
+#pragma unroll
+        for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i]);
+        int off = 0;
+        int s = 0;
+        for (; s + 1 < nsteps; s += 2) {
+            off = advance(off);  // step s + 1
+#pragma unroll
+            for (int i = 0; i < MB; ++i) a1[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off);
+            mma(a0, b0);
+            const bool more2 = s + 2 < nsteps;
+            if (more2) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) b0[j] = wp[(size_t)(s + 2) * wstep + j * 64];
+            }
+            off = advance(off);  // step s + 2
+            if (more2) {
+#pragma unroll
+                for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off);
+            }
+            mma(a1, b1);
+            if (s + 3 < nsteps) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) b1[j] = wp[(size_t)(s + 3) * wstep + j * 64];
+            }
+        }
+        if (s < nsteps) mma(a0, b0);
+    } else {
+        u4 bcur[NB], bnxt[NB];
+#pragma unroll
+        for (int j = 0; j < NB; ++j) bcur[j] = wp[j * 64];
+        for (int s = 0; s < a.ksteps; ++s) {
+            const bool more = s + 1 < a.ksteps;
+            if (more) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) bnxt[j] = wp[(size_t)(s + 1) * wstep + j * 64];
+            }
+            int offs[LPE];
+#pragma unroll
+            for (int e = 0; e < LPE; ++e) offs[e] = offtab[s * KSTEP + g * LPE + e];
+            u4 av[MB];
+#pragma unroll
+            for (int i = 0; i < MB; ++i) {
+                TC v[LPE];
+                const int base = abase[i] - g * LPE;
+#pragma unroll
+                for (int e = 0; e < LPE; ++e) v[e] = offs[e] >= 0 ? win_lds[base + offs[e]] : TC(0);
+                __builtin_memcpy(&av[i], v, 16);
+            }
+            mma(av, bcur);
+            if (more) {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) bcur[j] = bnxt[j];
+            }
+        }
+    }
+
+    // ---- epilogue -------------------------------------------------------------
+    if (a.head_ncls > 0) {
+        fused_head<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, q, fy, fx, l0, lend, twb, c0,
+                               reinterpret_cast<float *>(smem));
+        return;
+    }
+    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int co = (nb0 + j) * 16 + lm;
+        if (co >= a.cout) continue;
+        const float bv = a.bias[co];
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int l = l0 + (wm * MB + i) * 16 + 4 * g + e;
+                if (l >= lend) continue;
+                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+                float v = acc[i][j][e] + bv;
+                if (a.act == ACT_TANH) v = tanhf(v);
+                TC *dst = outp + ((size_t)y * a.out_w + x) * a.cout + co;
+                if constexpr (BF)
+                    *dst = f2bf(v);
+                else
+                    *dst = v;
+            }
+        }
+    }
+}
+
+template <int MB, int NB, int WN, bool BF, bool IN_F32, bool VEC>
+hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
+{
+    auto kern = conv_frag_mfma<MB, NB, WN, BF, IN_F32, VEC>;
+    if (a.lds_bytes > 65536) {
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(256), a.lds_bytes, s, a);
+    return hipGetLastError();
+}
+
+// The register tiles each operand variant is built for.
+#define FS_CONV_TILES_VEC(X)                                                                   \
+    X(1, 1, 1) X(1, 2, 1) X(1, 3, 1) X(1, 4, 1) X(2, 1, 1) X(2, 2, 1) X(2, 3, 1) X(2, 4, 1)     \
+    X(4, 1, 1) X(4, 2, 1) X(4, 3, 1) X(4, 4, 1) X(1, 7, 1) X(1, 8, 1) X(1, 13, 1) X(2, 7, 1)   \
+    X(2, 8, 1) X(2, 13, 1) X(2, 2, 2) X(2, 4, 2) X(2, 7, 2) X(4, 2, 2) X(4, 4, 2) X(4, 7, 2)   \
+    X(4, 2, 4) X(4, 4, 4) X(8, 2, 4) X(8, 4, 4)
+#define FS_CONV_TILES_GATHER(X)                                                                \
+    X(1, 1, 1) X(1, 2, 1) X(1, 3, 1) X(1, 4, 1) X(2, 1, 1) X(2, 2, 1) X(2, 3, 1) X(2, 4, 1)     \
+    X(4, 1, 1) X(4, 2, 1) X(4, 3, 1) X(4, 4, 1)
+
+template <bool BF, bool IN_F32, bool VEC>
+hipError_t dispatch_tile(const ConvArgs &a, int mb, int nb, int wn, int gx, int gy, hipStream_t s)
+{
+#define FS_CONV_CASE(M, N, W) \
+    if (mb == M && nb == N && wn == W) return launch_one<M, N, W, BF, IN_F32, VEC>(a, gx, gy, s);
+    if constexpr (VEC) {
+        FS_CONV_TILES_VEC(FS_CONV_CASE)
+    } else {
+        FS_CONV_TILES_GATHER(FS_CONV_CASE)
+    }
+#undef FS_CONV_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace conv
+}  // namespace fs

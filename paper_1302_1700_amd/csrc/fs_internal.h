@@ -15,11 +15,14 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace fs {
 
 constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of pool sizes)
 constexpr int kMaxHeadClasses = 16;
 constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
+constexpr int kMaxFusedClasses = 4;   // classes of a last layer fused into a conv epilogue
 
 enum ActKind { ACT_NONE = 0, ACT_TANH = 1, ACT_SOFTMAX = 2 };
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
@@ -35,7 +38,7 @@ struct AxisTable {
 struct ConvArgs {
     const void *in;       // [nfrag][in_h][in_w][in_c] (float or bf16; first layer: the image)
     void *out;            // [nfrag][out_h][out_w][cout]
-    const void *w;        // swizzled weights (see api.hip: swizzle_conv_weights)
+    const void *w;        // packed weights (api.hip: pack_conv_weights)
     const float *bias;    // [nbt * 16], zero padded
     int nfrag;            // B * F
     int F, Q;             // fragments per image, per axis
@@ -47,10 +50,19 @@ struct ConvArgs {
     int band_w;           // output columns per band
     int nbands;           // bands per fragment
     int tiles_per_band;   // tiles per band (enough for the tallest fragment)
-    int mt;               // output pixels per tile (64 * MB)
+    int mt;               // output pixels per tile (16 * MB * 4 / WN)
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
     AxisTable ext;        // true sizes of the input fragments
+    // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
+    // activation, and the reassembly are applied in the epilogue, which then
+    // writes the dense output map instead of `out`'s fragment batch.
+    int head_ncls, head_act;
+    const float *head_w;  // [head_ncls][cout]
+    const float *head_b;  // [head_ncls]
+    float *head_out;      // [B][ny][nx][head_ncls]
+    int ny, nx, S;
+    uint16_t base[kMaxAxis];  // per-axis fragment index -> its first output coordinate
 };
 
 struct PoolArgs {
@@ -80,19 +92,18 @@ struct HeadArgs {
 
 // Launchers (return hipSuccess or the launch error).  `dtype` selects the
 // operand type; `in_f32` says the input is float32 even in a bf16 net (the
-// image).
-hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, bool vec,
+// image).  Convolution register tiles: mb pixel blocks x nb channel blocks per
+// wave, wn waves across the output channels (4 / wn across the pixels).
+hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
+bool conv_tile_supported(int mb, int nb, int wn, bool vec);
 
-// Names the profiler shows for a launch (best effort, for reports).
-const char *conv_kernel_name(int dtype, bool in_f32, int mb, int nb, bool vec);
+// Kernel names as the profiler reports them (for measurement reports).
+std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, bool vec);
 const char *pool_kernel_name(int dtype, bool in_f32);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
-
-// Supported (mb, nb) register tiles of the convolution kernel.
-bool conv_tile_supported(int mb, int nb);
 
 }  // namespace fs

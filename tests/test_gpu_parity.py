@@ -273,3 +273,25 @@ def test_repeat_is_deterministic(fsb):
     ms = net.profile(x, reps=2)
     assert len(ms) == len(net.launches(1, 200, 180)) and all(m > 0 for m in ms)
     net.close()
+
+
+def test_unfused_head_paths(fsb, monkeypatch):
+    """The separate head kernel (last layer not folded into the convolution
+    before it): forced off by the environment switch, and by a last layer with
+    more classes than the fused epilogue takes."""
+    w = wl.WORKLOADS[2]
+    params, img = wl.workload_inputs(2, height=140, width=150)
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    monkeypatch.setenv("FRAGSCAN_NO_FUSED_HEAD", "1")
+    got = _scan(fsb, w.layers, params, img, 1)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+    monkeypatch.delenv("FRAGSCAN_NO_FUSED_HEAD")
+    layers = [wl.conv(3, 2, 16), wl.pool(2, 16), wl.conv(2, 16, 32), wl.pool(2, 32),
+              wl.fc(2, 32, 24), wl.fc(1, 24, 7, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 3, 0.3)
+    img = wl.make_image(4, 2, w0 + 29, w0 + 33, 2)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    for dt in ("f32", "bf16"):
+        got = _scan(fsb, layers, params, img, 2, dtype=dt)
+        assert np.abs(got - ref).max() <= TOL[dt], dt
