@@ -73,6 +73,7 @@ struct fs_net {
     std::vector<int> pool_k;
     int S = 1, F = 1;
     int device = 0;
+    int ncu = 256;            // compute units of the device (persistent grids)
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
     int head_cin = 0;
@@ -187,6 +188,8 @@ struct Launch {
     HeadArgs head;
     int mb = 0, nb = 0, wn = 1;
     bool vec = false, has_fc = false;
+    bool ws = false;          // persistent wave-specialised convolution
+    int ws_slots = 0;         // resident workgroups of the persistent kernel
     int gx = 1, gy = 1;
     int frags = 0;
     long long out_pixels = 0;
@@ -243,6 +246,48 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     const int wm = 4 / l.wn;
     int mb_force = 0, band_force = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
+    if (l.vec && getenv("FRAGSCAN_WS")) {  // opt-in: not yet faster than the 4-wave kernel
+        // persistent kernel: two window buffers and the fused-head reduction
+        const int mbs_ws[3] = {2, 1, 4};
+        for (int mi = 0; mi < 3; ++mi) {
+            const int mb = mb_force ? mb_force : mbs_ws[mi];
+            if (!conv_ws_supported(mb, l.nb, l.wn)) {
+                if (mb_force) break;
+                continue;
+            }
+            const int mt = 16 * mb * wm;
+            int nbands = wout_max <= 32 ? 1 : (wout_max + 15) / 16;
+            if (band_force) nbands = (wout_max + band_force - 1) / band_force;
+            const int band_w = (wout_max + nbands - 1) / nbands;
+            int tmin = band_w;
+            for (int wo : wouts)
+                for (int b = 0; b < nbands; ++b) {
+                    const int twb = std::min(band_w, wo - b * band_w);
+                    if (twb > 0) tmin = std::min(tmin, twb);
+                }
+            const int rmax = std::min((mt - 1 + tmin - 1) / tmin + k, in.hmax);
+            const size_t win = align_up((size_t)rmax * (band_w + k - 1) * cs * es, 16);
+            const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;
+            const size_t lds = 2 * win + red;
+            if (lds > 160 * 1024) {
+                if (mb_force) break;
+                continue;
+            }
+            L.ws = true;
+            L.mb = mb;
+            L.conv.band_w = band_w;
+            L.conv.nbands = nbands;
+            L.conv.mt = mt;
+            L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
+            L.conv.lds_cs = cs;
+            L.conv.win_bytes = (int)win;
+            L.conv.lds_bytes = (int)lds;
+            int occ = net->device >= 0 ? conv_ws_occupancy(net->dtype, mb, l.nb, l.wn, (int)lds) : 0;
+            if (occ <= 0) occ = std::max(1, std::min(2, (int)((160 * 1024) / lds)));
+            L.ws_slots = net->ncu * occ;
+            return FS_OK;
+        }
+    }
     // two pixel blocks per wave first (measured best on the N4 layers), then
     // the neighbours
     const int mbs[4] = {2, 4, 1, 8};
@@ -400,12 +445,14 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             if (st != FS_OK) return st;
             L.gx = B * F * a.nbands * a.tiles_per_band;
             L.gy = l.nbt / (l.nb * l.wn);
+            if (L.ws) L.gx = std::max(1, std::min(L.gx, L.ws_slots / L.gy));
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
-            L.name = conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.vec);
+            L.name = L.ws ? conv_ws_kernel_name(net->dtype, L.mb, L.nb, L.wn)
+                          : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.vec);
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
                 a.head_ncls = net->ncls;
@@ -542,6 +589,7 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
             L.conv.head_out = d_out;
             L.conv.out = nullptr;
         }
+        if (L.ws) return launch_conv_ws(L.conv, net->dtype, L.mb, L.nb, L.wn, L.gx, L.gy, s);
         return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.vec, L.gx, L.gy, s);
     }
     if (L.type == 1) {
@@ -743,6 +791,11 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         return hip_fail(e, "hipGetDevice");
     }
     net->mem_bytes = blob.size();
+    {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, net->device) == hipSuccess && n > 0)
+            net->ncu = n;
+    }
     e = hipMalloc(&net->d_mem, blob.size());
     if (e != hipSuccess) {
         delete net;
@@ -827,7 +880,7 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, f
         o.flops = L.flops;
         o.bytes = L.bytes;
         o.grid = L.gx * L.gy;
-        o.block = 256;
+        o.block = L.ws ? 512 : 256;
         std::snprintf(o.name, sizeof o.name, "%s", L.name.c_str());
     }
     return FS_OK;

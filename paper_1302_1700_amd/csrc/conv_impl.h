@@ -57,6 +57,14 @@ __device__ __forceinline__ uint16_t f2bf(float f)
     return (uint16_t)(u >> 16);
 }
 
+// tanh(x) = 1 - 2 / (exp(2x) + 1), with the hardware exp2 and reciprocal:
+// absolute error a few 1e-7, saturates cleanly to +-1 for large |x|.
+__device__ __forceinline__ float tanh_fast(float x)
+{
+    const float t = __builtin_amdgcn_exp2f(x * 2.8853900817779268f);  // exp(2x)
+    return 1.0f - 2.0f * __builtin_amdgcn_rcpf(t + 1.0f);
+}
+
 template <bool BF>
 struct Elem;
 template <>
@@ -72,16 +80,17 @@ struct Elem<true> {
 
 // Fused last layer.  The tile's activations act(acc + bias) never leave the
 // registers: every lane multiplies its values (pixels 4g + e of each m-block,
-// channel lm of each n-block) by the last layer's weights, the 16 lanes of a
-// row (same pixels, 16 channels) are summed with xor shuffles, the waves that
-// split the channels add up through LDS, and one thread per pixel applies the
-// last activation (softmax: exp(z - max z) / sum) and writes the pixel's
-// classes to the dense map at the window corner the pixel stands for: final
-// fragment (fy, fx) position (y, x) holds window (base[fy] + S*y, base[fx] + S*x).
+// channel lm of each n-block) by the last layer's weights and the 16 lanes of
+// a row (same pixels, 16 channels) are summed with xor shuffles
+// (fused_head_partials); the waves that split the channels add up through LDS
+// and one thread per pixel applies the last activation (softmax: exp(z - max
+// z) / sum) and writes the pixel's classes to the dense map at the window
+// corner the pixel stands for: final fragment (fy, fx) position (y, x) holds
+// window (base[fy] + S*y, base[fx] + S*x) (fused_head_finish).  A workgroup
+// barrier separates the two.
 template <int MB, int NB, int WN>
-__device__ __forceinline__ void fused_head(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm, int wn,
-                                           int lm, int g, int q, int fy, int fx, int l0, int lend, int twb,
-                                           int c0, float *red)
+__device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm,
+                                                    int wn, int lm, int g, float *red)
 {
     constexpr int NC = kMaxFusedClasses;
     const int ncls = a.head_ncls;
@@ -105,7 +114,7 @@ __device__ __forceinline__ void fused_head(const ConvArgs &a, const f4 (&acc)[MB
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 float v = acc[i][j][e] + bv;
-                if (a.act == ACT_TANH) v = tanhf(v);
+                if (a.act == ACT_TANH) v = tanh_fast(v);
 #pragma unroll
                 for (int c = 0; c < NC; ++c) part[i][e][c] = fmaf(w2[c], v, part[i][e][c]);
             }
@@ -123,8 +132,6 @@ __device__ __forceinline__ void fused_head(const ConvArgs &a, const f4 (&acc)[MB
                 t += __shfl_xor(t, 1);
                 part[i][e][c] = t;
             }
-    const int mt = a.mt;
-    __syncthreads();  // the LDS window is no longer read
     if (lm == 0) {
 #pragma unroll
         for (int i = 0; i < MB; ++i)
@@ -132,12 +139,20 @@ __device__ __forceinline__ void fused_head(const ConvArgs &a, const f4 (&acc)[MB
             for (int e = 0; e < 4; ++e) {
                 const int m = (wm * MB + i) * 16 + 4 * g + e;
 #pragma unroll
-                for (int c = 0; c < NC; ++c) red[((size_t)wn * mt + m) * NC + c] = part[i][e][c];
+                for (int c = 0; c < NC; ++c) red[((size_t)wn * a.mt + m) * NC + c] = part[i][e][c];
             }
     }
-    __syncthreads();
+}
+
+template <int WN>
+__device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int fy, int fx, int l0, int lend,
+                                                  int twb, int c0, const float *red)
+{
+    constexpr int NC = kMaxFusedClasses;
+    const int ncls = a.head_ncls;
+    const int mt = a.mt;
     const int b = q / a.F;
-    for (int m = threadIdx.x; m < mt; m += 256) {
+    for (int m = threadIdx.x; m < mt; m += blockDim.x) {
         const int l = l0 + m;
         if (l >= lend) break;
         float z[NC];
@@ -217,17 +232,28 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     // ---- stage the input window ----------------------------------------------
     const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * a.in_h * a.in_w * a.in_c;
     if constexpr (VEC && !IN_F32) {
+        // batches of 8 loads in flight per thread before their LDS stores
         const int nvec = a.cin / LPE;
         const int total = R * Cc * nvec;
-        for (int idx = threadIdx.x; idx < total; idx += 256) {
-            const int v = idx % nvec;
-            const int p = idx / nvec;
-            const int c = p % Cc, r = p / Cc;
-            const int gy = yfirst + r, gx = c0 + c;
-            u4 val = {0u, 0u, 0u, 0u};
-            if (gy < hin && gx < win)
-                val = *reinterpret_cast<const u4 *>(inp + ((size_t)gy * a.in_w + gx) * a.in_c + v * LPE);
-            *reinterpret_cast<u4 *>(win_lds + (r * Cc + c) * CS + v * LPE) = val;
+        constexpr int UN = 8;
+        for (int base = threadIdx.x; base < total; base += 256 * UN) {
+            u4 val[UN];
+            int dsto[UN];
+#pragma unroll
+            for (int u = 0; u < UN; ++u) {
+                const int idx = base + u * 256;
+                const int v = idx % nvec;
+                const int p = idx / nvec;
+                const int c = p % Cc, r = p / Cc;
+                const int gy = yfirst + r, gx = c0 + c;
+                val[u] = u4{0u, 0u, 0u, 0u};
+                if (idx < total && gy < hin && gx < win)
+                    val[u] = *reinterpret_cast<const u4 *>(inp + ((size_t)gy * a.in_w + gx) * a.in_c + v * LPE);
+                dsto[u] = idx < total ? (r * Cc + c) * CS + v * LPE : -1;
+            }
+#pragma unroll
+            for (int u = 0; u < UN; ++u)
+                if (dsto[u] >= 0) *reinterpret_cast<u4 *>(win_lds + dsto[u]) = val[u];
         }
     } else {
         const int total = R * Cc * a.cin;
@@ -314,46 +340,58 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         // ahead, so the products of a step never wait on the loads it needs.
         const int ncc = a.cin / KSTEP;
         const int nsteps = a.ksteps;
+        // (branch-free: a straight-line loop body lets the compiler wait only
+        // for the operands each product needs)
         int dy = 0, dx = 0, cc = 0;
-        auto advance = [&](int off) {
-            if (++cc < ncc) return off + KSTEP;
-            cc = 0;
-            if (++dx < a.k) return off - (ncc - 1) * KSTEP + CS;
-            dx = 0;
-            ++dy;
-            return dy * Cc * CS;
+        auto advance = [&](int) {
+            ++cc;
+            const int w1 = cc == ncc;
+            cc = w1 ? 0 : cc;
+            dx += w1;
+            const int w2 = dx == a.k;
+            dx = w2 ? 0 : dx;
+            dy += w2;
+            return (dy * Cc + dx) * CS + cc * KSTEP;
         };
         u4 b0[NB], b1[NB], a0[MB], a1[MB];
 #pragma unroll
         for (int j = 0; j < NB; ++j) b0[j] = wp[j * 64];
-        if (nsteps > 1) {
+        // unconditional (clamped) so every path reaches the loop with the same
+        // loads in flight
 #pragma unroll
-            for (int j = 0; j < NB; ++j) b1[j] = wp[wstep + j * 64];
-        }
+        for (int j = 0; j < NB; ++j) b1[j] = wp[(nsteps > 1 ? wstep : 0) + j * 64];
 #pragma unroll
         for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i]);
+        // The prefetches are issued on every iteration (past the end they
+        // re-read the last step's weights and the window's first pixel), so
+        // every path through the loop has the same loads in flight and the
+        // waits before the products only cover the operands they use.
+        const int last = nsteps - 1;
         int off = 0;
         int s = 0;
         for (; s + 1 < nsteps; s += 2) {
+            // scheduling barriers keep each prefetch ahead of the products
+            // that do not need it (left alone, the compiler sinks the loads
+            // below them to share registers, exposing their latency)
             off = advance(off);  // step s + 1
 #pragma unroll
             for (int i = 0; i < MB; ++i) a1[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off);
+            __builtin_amdgcn_sched_barrier(0);
             mma(a0, b0);
-            const bool more2 = s + 2 < nsteps;
-            if (more2) {
+            __builtin_amdgcn_sched_barrier(0);
+            const size_t w2 = (size_t)min(s + 2, last) * wstep;
 #pragma unroll
-                for (int j = 0; j < NB; ++j) b0[j] = wp[(size_t)(s + 2) * wstep + j * 64];
-            }
+            for (int j = 0; j < NB; ++j) b0[j] = wp[w2 + j * 64];
             off = advance(off);  // step s + 2
-            if (more2) {
+            const int offa = s + 2 < nsteps ? off : 0;
 #pragma unroll
-                for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off);
-            }
+            for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
+            __builtin_amdgcn_sched_barrier(0);
             mma(a1, b1);
-            if (s + 3 < nsteps) {
+            __builtin_amdgcn_sched_barrier(0);
+            const size_t w3 = (size_t)min(s + 3, last) * wstep;
 #pragma unroll
-                for (int j = 0; j < NB; ++j) b1[j] = wp[(size_t)(s + 3) * wstep + j * 64];
-            }
+            for (int j = 0; j < NB; ++j) b1[j] = wp[w3 + j * 64];
         }
         if (s < nsteps) mma(a0, b0);
     } else {
@@ -388,8 +426,11 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 
     // ---- epilogue -------------------------------------------------------------
     if (a.head_ncls > 0) {
-        fused_head<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, q, fy, fx, l0, lend, twb, c0,
-                               reinterpret_cast<float *>(smem));
+        float *red = reinterpret_cast<float *>(smem);
+        __syncthreads();  // the LDS window (which red reuses) is no longer read
+        fused_head_partials<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, red);
+        __syncthreads();
+        fused_head_finish<WN>(a, q, fy, fx, l0, lend, twb, c0, red);
         return;
     }
     TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
@@ -406,7 +447,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 if (l >= lend) continue;
                 const int y = l / twb, x = c0 + (l - (l / twb) * twb);
                 float v = acc[i][j][e] + bv;
-                if (a.act == ACT_TANH) v = tanhf(v);
+                if (a.act == ACT_TANH) v = tanh_fast(v);
                 TC *dst = outp + ((size_t)y * a.out_w + x) * a.cout + co;
                 if constexpr (BF)
                     *dst = f2bf(v);

@@ -53,6 +53,7 @@ struct ConvArgs {
     int mt;               // output pixels per tile (16 * MB * 4 / WN)
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
+    int win_bytes;        // one window buffer (persistent kernel: two of them)
     AxisTable ext;        // true sizes of the input fragments
     // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
     // activation, and the reassembly are applied in the epilogue, which then
@@ -96,6 +97,12 @@ struct HeadArgs {
 // wave, wn waves across the output channels (4 / wn across the pixels).
 hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
+// Persistent wave-specialised variant (vector path; 512 threads).
+hipError_t launch_conv_ws(const ConvArgs &a, int dtype, int mb, int nb, int wn, int grid_x, int grid_y,
+                          hipStream_t s);
+bool conv_ws_supported(int mb, int nb, int wn);
+// Workgroups of the persistent kernel that fit on one CU (0: unknown / none).
+int conv_ws_occupancy(int dtype, int mb, int nb, int wn, int lds_bytes);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
@@ -103,6 +110,7 @@ bool conv_tile_supported(int mb, int nb, int wn, bool vec);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, bool vec);
+std::string conv_ws_kernel_name(int dtype, int mb, int nb, int wn);
 const char *pool_kernel_name(int dtype, bool in_f32);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
