@@ -446,6 +446,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.gx = B * F * a.nbands * a.tiles_per_band;
             L.gy = l.nbt / (l.nb * l.wn);
             if (L.ws) L.gx = std::max(1, std::min(L.gx, L.ws_slots / L.gy));
+            else L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;

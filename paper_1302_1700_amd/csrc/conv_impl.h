@@ -201,7 +201,13 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 
     extern __shared__ __align__(16) unsigned char smem[];
 
-    int bid = blockIdx.x;
+    // Workgroups are dealt to the 8 XCDs round-robin; renumber them so each
+    // XCD gets a contiguous run of tiles, whose shared window rows and
+    // columns then meet in that XCD's L2 (the grid is padded to a multiple of
+    // 8; the padding tiles exit).
+    const int per_xcd = gridDim.x / 8;
+    int bid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
+    if (bid >= a.nfrag * a.nbands * a.tiles_per_band) return;
     const int t = bid % a.tiles_per_band;
     bid /= a.tiles_per_band;
     const int band = bid % a.nbands;

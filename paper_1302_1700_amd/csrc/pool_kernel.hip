@@ -15,6 +15,8 @@
 // stored back unchanged.
 #include "fs_internal.h"
 
+#include <type_traits>
+
 namespace fs {
 namespace {
 
@@ -109,20 +111,137 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
     }
 }
 
-template <bool BF, bool IN_F32, int V>
-hipError_t go(const PoolArgs &a, int grid, hipStream_t s)
+// Row-band version for pool sizes 2..4 (the common case).  The k x k maxima
+// at every position of the parent, M[y][x] = max_{i,j<k} P[y+i][x+j], are
+// exactly the children's pixels: M[y][x] is pixel (y div k, x div k) of the
+// child with offset (x mod k, y mod k).  A thread owns one (x, channel vector)
+// column of a band of RB rows of M: it walks the parent rows once, keeps the
+// last k horizontal maxima in registers, and writes each M row to its child.
+// So a parent element is fetched from memory once (its k horizontal
+// neighbours share it through the cache) and every child row is written with
+// contiguous stores; the k^2 siblings no longer re-read the parent.
+template <int K, bool BF, bool IN_F32, int V>
+__global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nbands, int nchunks)
 {
+    using TO = typename std::conditional<BF, uint16_t, float>::type;
+    using TI = typename std::conditional<IN_F32, float, TO>::type;
+    int bid = blockIdx.x;
+    const int chunk = bid % nchunks;
+    bid /= nchunks;
+    const int band = bid % nbands;
+    const int p = bid / nbands;  // parent batch index b * F + fy * Q + fx
+    const int b = p / a.F;
+    const int rem = p - b * a.F;
+    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
+    const int hp = a.ext.y[fy], wp = a.ext.x[fx];
+    const int nv = a.C / V;
+    const int pi = chunk * 256 + threadIdx.x;
+    const int x = pi / nv, cv = pi - (pi / nv) * nv;
+    const int y0 = band * rb;
+    const int yend = min(y0 + rb, hp - K + 1);  // M rows [y0, yend)
+    if (x > wp - K || y0 >= yend) return;
+
+    const TI *src = reinterpret_cast<const TI *>(a.in) + (size_t)p * a.in_h * a.in_w * a.C + (size_t)x * a.C + cv * V;
+    const size_t prow = (size_t)a.in_w * a.C;
+    const int Qc = a.Q * K;
+    const size_t cbase = (size_t)b * a.F * K * K;
+    TO *out = reinterpret_cast<TO *>(a.out);
+
+    auto hmax = [&](int row, float (&h)[V]) {
+        const TI *r = src + (size_t)row * prow;
+#pragma unroll
+        for (int e = 0; e < V; ++e) h[e] = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            const TI *s = r + (size_t)j * a.C;
+            if constexpr (V == 1) {
+                float v;
+                if constexpr (!BF || IN_F32) v = s[0]; else v = bf2f(s[0]);
+                h[0] = fmaxf(h[0], v);
+            } else {
+                u4 raw = *reinterpret_cast<const u4 *>(s);
+                if constexpr (BF) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        h[2 * e] = fmaxf(h[2 * e], bf2f((uint16_t)(raw[e] & 0xffffu)));
+                        h[2 * e + 1] = fmaxf(h[2 * e + 1], bf2f((uint16_t)(raw[e] >> 16)));
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) h[e] = fmaxf(h[e], __uint_as_float(raw[e]));
+                }
+            }
+        }
+    };
+    float win[K][V];  // horizontal maxima of the last K parent rows (ring by shifting)
+#pragma unroll
+    for (int i = 0; i < K - 1; ++i) hmax(y0 + i, win[i + 1]);
+    const int ox = x % K, xbar = x / K;
+    for (int y = y0; y < yend; ++y) {
+#pragma unroll
+        for (int i = 0; i < K - 1; ++i)
+#pragma unroll
+            for (int e = 0; e < V; ++e) win[i][e] = win[i + 1][e];
+        hmax(y + K - 1, win[K - 1]);
+        float m[V];
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+            m[e] = win[0][e];
+#pragma unroll
+            for (int i = 1; i < K; ++i) m[e] = fmaxf(m[e], win[i][e]);
+        }
+        const int oy = y % K, ybar = y / K;
+        const size_t child = cbase + (size_t)(fy * K + oy) * Qc + (fx * K + ox);
+        TO *d = out + ((child * a.out_h + ybar) * a.out_w + xbar) * a.C + cv * V;
+        if constexpr (V == 1) {
+            if constexpr (BF) d[0] = f2bf(m[0]); else d[0] = m[0];
+        } else {
+            u4 w;
+            if constexpr (BF) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[e] = (uint32_t)f2bf(m[2 * e]) | ((uint32_t)f2bf(m[2 * e + 1]) << 16);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) w[e] = __float_as_uint(m[e]);
+            }
+            *reinterpret_cast<u4 *>(d) = w;
+        }
+    }
+}
+
+template <int K, bool BF, bool IN_F32, int V>
+hipError_t go_rows(const PoolArgs &a, hipStream_t s)
+{
+    const int nv = a.C / V;
+    const int rb = 8;
+    const int nbands = (a.in_h + rb - 1) / rb;
+    const int nchunks = (a.in_w * nv + 255) / 256;
+    const long long grid = (long long)a.n_children / (K * K) * nbands * nchunks;
+    if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((pool_frag_rows<K, BF, IN_F32, V>), dim3((unsigned)grid), dim3(256), 0, s, a, rb, nbands,
+                       nchunks);
+    return hipGetLastError();
+}
+
+template <bool BF, bool IN_F32, int V>
+hipError_t go_k(const PoolArgs &a, int grid, hipStream_t s)
+{
+    if (a.k == 2) return go_rows<2, BF, IN_F32, V>(a, s);
+    if (a.k == 3) return go_rows<3, BF, IN_F32, V>(a, s);
+    if (a.k == 4) return go_rows<4, BF, IN_F32, V>(a, s);
     hipLaunchKernelGGL((pool_frag<BF, IN_F32, V>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }
+
 
 }  // namespace
 
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s)
 {
-    if (dtype == DT_F32) return (a.C % 4 == 0) ? go<false, false, 4>(a, grid, s) : go<false, false, 1>(a, grid, s);
-    if (in_f32) return go<true, true, 1>(a, grid, s);
-    return (a.C % 8 == 0) ? go<true, false, 8>(a, grid, s) : go<true, false, 1>(a, grid, s);
+    if (dtype == DT_F32) return (a.C % 4 == 0) ? go_k<false, false, 4>(a, grid, s) : go_k<false, false, 1>(a, grid, s);
+    if (in_f32) return go_k<true, true, 1>(a, grid, s);
+    return (a.C % 8 == 0) ? go_k<true, false, 8>(a, grid, s) : go_k<true, false, 1>(a, grid, s);
 }
 
 const char *pool_kernel_name(int dtype, bool in_f32)

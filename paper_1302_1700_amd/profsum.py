@@ -2,9 +2,12 @@
 table: per kernel name, calls, total and mean duration.
 
     python -m paper_1302_1700_amd.profsum <results.db | kernel_trace.csv | dir> [--pmc]
+    python -m paper_1302_1700_amd.profsum copy <MiB>
 
 With --pmc, counter values per kernel dispatch are averaged per kernel name
-(FETCH_SIZE / WRITE_SIZE and the like).
+(FETCH_SIZE / WRITE_SIZE and the like).  `copy` runs a plain device-to-device
+copy of a tensor of the given size (read once, written once): the calibration
+point for the FETCH_SIZE / WRITE_SIZE counters.
 """
 import csv
 import glob
@@ -67,8 +70,23 @@ def pmc_stats(path):
     return {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in acc.items()}
 
 
+def copy_probe(mib):
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.rand(n, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print("copied %d MiB x 3" % mib)
+
+
 def main():
     args = [a for a in sys.argv[1:] if not a.startswith("--")]
+    if args and args[0] == "copy":
+        copy_probe(int(args[1]))
+        return
     if "--pmc" in sys.argv:
         for k, cs in pmc_stats(args[0]).items():
             print(k)
