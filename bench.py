@@ -16,7 +16,6 @@ Default workload: net N4 (the paper's Table 1 net) on a 512 x 512 greyscale
 image, 418 x 418 windows.
 """
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -32,27 +31,20 @@ PEAK = {  # MI355X published dense peaks
 }
 
 
-def kernel_source_digest():
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_1302_1700_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            with open(os.path.join(csrc, f), "rb") as fh:
-                h.update(f.encode() + fh.read())
-    return h.hexdigest()[:16]
-
-
 def measured_traffic(kernel_name, workload):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
-    was taken on the current kernel sources; else None."""
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (profiles/traffic.json), if it was taken on the current kernel sources;
+    else None."""
+    from paper_1302_1700_amd.profsum import source_digest
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         entries = json.load(f)
+    base = kernel_name.split("+")[0]
     for e in entries:
-        if e.get("kernel") == kernel_name and e.get("workload") == workload \
-                and e.get("source_digest") == kernel_source_digest():
+        if base in e.get("kernel", "") and e.get("workload") == workload \
+                and e.get("source_digest") == source_digest():
             return e.get("bytes_per_launch")
     return None
 

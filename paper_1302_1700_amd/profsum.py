@@ -3,11 +3,17 @@ table: per kernel name, calls, total and mean duration.
 
     python -m paper_1302_1700_amd.profsum <results.db | kernel_trace.csv | dir> [--pmc]
     python -m paper_1302_1700_amd.profsum copy <MiB>
+    python -m paper_1302_1700_amd.profsum traffic <fetch_dir> <write_dir> <copy_fetch_dir>
+           <copy_write_dir> <copy_MiB> <workload> [--out profiles/traffic.json]
 
 With --pmc, counter values per kernel dispatch are averaged per kernel name
 (FETCH_SIZE / WRITE_SIZE and the like).  `copy` runs a plain device-to-device
 copy of a tensor of the given size (read once, written once): the calibration
-point for the FETCH_SIZE / WRITE_SIZE counters.
+point for the FETCH_SIZE / WRITE_SIZE counters.  `traffic` turns a FETCH_SIZE
+pass and a WRITE_SIZE pass of a workload, plus the same two passes of the copy
+probe, into HBM bytes per launch: each counter is scaled by (bytes the copy
+moved) / (what the counter read for it), and the entry records the digest of
+the kernel sources it was taken on.
 """
 import csv
 import glob
@@ -82,8 +88,55 @@ def copy_probe(mib):
     print("copied %d MiB x 3" % mib)
 
 
+def source_digest():
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc")
+    for f in sorted(os.listdir(csrc)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, workload, out):
+    import json
+    copy_bytes = copy_mib * (1 << 20)
+    cf = pmc_stats(cfetch_dir)
+    cw = pmc_stats(cwrite_dir)
+    ck = [k for k in cf if "copyBuffer" in k or "copy" in k.lower()]
+    fscale = copy_bytes / (cf[ck[0]]["FETCH_SIZE"] * 1024.0)
+    wscale = copy_bytes / (cw[ck[0]]["WRITE_SIZE"] * 1024.0)
+    fe = pmc_stats(fetch_dir)
+    wr = pmc_stats(write_dir)
+    entries = []
+    if os.path.exists(out):
+        with open(out) as f:
+            entries = [e for e in json.load(f) if e.get("workload") != workload]
+    dig = source_digest()
+    for k in fe:
+        if not k or not k.startswith("void fs::"):
+            continue
+        fb = fe[k]["FETCH_SIZE"] * 1024.0 * fscale
+        wb = wr.get(k, {}).get("WRITE_SIZE", 0.0) * 1024.0 * wscale
+        entries.append({"kernel": k, "workload": workload, "source_digest": dig,
+                        "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                        "bytes_per_launch": fb + wb, "fetch_scale": fscale, "write_scale": wscale})
+        print("%-80s fetch %10.3f MB  write %10.3f MB" % (k[:80], fb / 1e6, wb / 1e6))
+    with open(out, "w") as f:
+        json.dump(entries, f, indent=1)
+    print("scales: FETCH x%.4f  WRITE x%.4f  -> %s" % (fscale, wscale, out))
+
+
 def main():
     args = [a for a in sys.argv[1:] if not a.startswith("--")]
+    if args and args[0] == "traffic":
+        out = "profiles/traffic.json"
+        if "--out" in sys.argv:
+            out = sys.argv[sys.argv.index("--out") + 1]
+            args = [a for a in args if a != out]
+        traffic(args[1], args[2], args[3], args[4], int(args[5]), args[6], out)
+        return
     if args and args[0] == "copy":
         copy_probe(int(args[1]))
         return
