@@ -25,18 +25,26 @@ class _OLayer(ctypes.Structure):
                 ("b", ctypes.POINTER(ctypes.c_double))]
 
 
-def _load():
+def _open(path):
+    lib = ctypes.CDLL(path)
+    lib.oracle_patch_forward.restype = ctypes.c_int
+    lib.oracle_patch_forward.argtypes = [
+        ctypes.POINTER(_OLayer), ctypes.c_int, ctypes.POINTER(ctypes.c_double),
+        ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
+        ctypes.POINTER(ctypes.c_int), ctypes.c_long, ctypes.POINTER(ctypes.c_double)]
+    return lib
+
+
+def _load(path=None):
+    """The compiled oracle (built on first use); `path` loads another build of
+    the same source, which the planted-mistake tests use."""
     global _lib
+    if path is not None:
+        return _open(path)
     if _lib is None:
         if not os.path.exists(ORACLE_LIB):
             _build.build(force=True, quiet=True)
-        lib = ctypes.CDLL(ORACLE_LIB)
-        lib.oracle_patch_forward.restype = ctypes.c_int
-        lib.oracle_patch_forward.argtypes = [
-            ctypes.POINTER(_OLayer), ctypes.c_int, ctypes.POINTER(ctypes.c_double),
-            ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int,
-            ctypes.POINTER(ctypes.c_int), ctypes.c_long, ctypes.POINTER(ctypes.c_double)]
-        _lib = lib
+        _lib = _open(ORACLE_LIB)
     return _lib
 
 
@@ -44,7 +52,7 @@ def _dptr(a):
     return a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
 
 
-def patch_forward(layers, params, image, patch, patches=None):
+def patch_forward(layers, params, image, patch, patches=None, lib_path=None):
     """Outputs of the net on the requested patches, in float64.
 
     layers  : layer dicts (kind, k, c_in, c_out, act)
@@ -54,7 +62,7 @@ def patch_forward(layers, params, image, patch, patches=None):
     patches : int array [n, 3] of (b, Y, X) top-left corners; None = all of them
     Returns [n, n_out] float64, or, when patches is None, [B, H-w0+1, W-w0+1, n_out].
     """
-    lib = _load()
+    lib = _load(lib_path)
     img = np.ascontiguousarray(image, dtype=np.float64)
     B, H, W, C = img.shape
     keep = []

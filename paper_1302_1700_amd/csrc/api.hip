@@ -60,6 +60,7 @@ struct NetLayer {
     bool vec = false;     // channel-vector path
     int nb = 1;           // output-channel blocks per wave
     int wn = 1;           // waves across output channels
+    int wk = 1;           // waves splitting the K steps
     int nbt = 0;          // channel blocks, padded to a multiple of nb * wn
     int ksteps = 0;
     size_t w_off = 0, b_off = 0;  // offsets into the net's device block
@@ -129,21 +130,22 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
                 }
 }
 
-// Optional tile override for tuning sweeps: FRAGSCAN_TILE="L:MB,NB,WN[,BAND];..."
+// Optional tile override for tuning sweeps: FRAGSCAN_TILE="L:MB,NB,WN[,BAND[,WK]];..."
 // (L = layer index); any field <= 0 keeps the planner's choice.
-bool tile_override(int layer, int *mb, int *nb, int *wn, int *band)
+bool tile_override(int layer, int *mb, int *nb, int *wn, int *band, int *wk = nullptr)
 {
     const char *env = getenv("FRAGSCAN_TILE");
     if (!env) return false;
     const char *p = env;
     while (*p) {
-        int L = -1, a = 0, b = 0, c = 0, d = 0;
-        const int n = sscanf(p, "%d:%d,%d,%d,%d", &L, &a, &b, &c, &d);
+        int L = -1, a = 0, b = 0, c = 0, d = 0, e = 0;
+        const int n = sscanf(p, "%d:%d,%d,%d,%d,%d", &L, &a, &b, &c, &d, &e);
         if (n >= 4 && L == layer) {
             if (mb && a > 0) *mb = a;
             if (nb && b > 0) *nb = b;
             if (wn && c > 0) *wn = c;
             if (band && n >= 5 && d > 0) *band = d;
+            if (wk && n >= 6 && e > 0) *wk = e;
             return true;
         }
         const char *semi = strchr(p, ';');
@@ -186,7 +188,7 @@ struct Launch {
     ConvArgs conv;
     PoolArgs pool;
     HeadArgs head;
-    int mb = 0, nb = 0, wn = 1;
+    int mb = 0, nb = 0, wn = 1, wk = 1;
     bool vec = false, has_fc = false;
     bool ws = false;          // persistent wave-specialised convolution
     int ws_slots = 0;         // resident workgroups of the persistent kernel
@@ -243,10 +245,10 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     for (int v : in.ex)
         if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
             wouts.push_back(v - k + 1);
-    const int wm = 4 / l.wn;
+    const int wm = 4 / (l.wn * l.wk);
     int mb_force = 0, band_force = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
-    if (l.vec && getenv("FRAGSCAN_WS")) {  // opt-in: not yet faster than the 4-wave kernel
+    if (l.vec && l.wk == 1 && getenv("FRAGSCAN_WS")) {  // opt-in: not yet faster than the 4-wave kernel
         // persistent kernel: two window buffers and the fused-head reduction
         const int mbs_ws[3] = {2, 1, 4};
         for (int mi = 0; mi < 3; ++mi) {
@@ -288,12 +290,11 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             return FS_OK;
         }
     }
-    // two pixel blocks per wave first (measured best on the N4 layers), then
-    // the neighbours
-    const int mbs[4] = {2, 4, 1, 8};
+    // two pixel blocks per wave first (four with split K), then the neighbours
+    const int mbs[4] = {l.wk == 2 ? 4 : 2, l.wk == 2 ? 2 : 4, 1, 8};
     for (int mi = 0; mi < 4; ++mi) {
         const int mb = mb_force ? mb_force : mbs[mi];
-        if (!conv_tile_supported(mb, l.nb, l.wn, l.vec)) {
+        if (!conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
             if (mb_force) break;
             continue;
         }
@@ -318,13 +319,17 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                 continue;
             }
             const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;  // fused-head reduction
+            // output tile restaged through LDS: [mt][wn * nb * 16 + 16 bytes]
+            const size_t otile = (size_t)mt * (l.wn * l.nb * 16 + 16 / es) * es;
+            // split-K partial sums of the waves with wk > 0
+            const size_t part = (size_t)(l.wk - 1) * (4 / l.wk) * mb * l.nb * 4 * 64 * 4;
             L.mb = mb;
             L.conv.band_w = band_w;
             L.conv.nbands = nbands;
             L.conv.mt = mt;
             L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
             L.conv.lds_cs = cs;
-            L.conv.lds_bytes = (int)std::max(lds, red);
+            L.conv.lds_bytes = (int)std::max(std::max(lds, part), std::max(red, otile));
             return FS_OK;
         }
         if (mb_force) break;
@@ -423,6 +428,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.vec = l.vec;
             L.nb = l.nb;
             L.wn = l.wn;
+            L.wk = l.wk;
             ConvArgs &a = L.conv;
             a.nfrag = B * F;
             a.F = F;
@@ -453,7 +459,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
             L.name = L.ws ? conv_ws_kernel_name(net->dtype, L.mb, L.nb, L.wn)
-                          : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.vec);
+                          : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
                 a.head_ncls = net->ncls;
@@ -591,7 +597,7 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
             L.conv.out = nullptr;
         }
         if (L.ws) return launch_conv_ws(L.conv, net->dtype, L.mb, L.nb, L.wn, L.gx, L.gy, s);
-        return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.vec, L.gx, L.gy, s);
+        return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.wk, L.vec, L.gx, L.gy, s);
     }
     if (L.type == 1) {
         L.pool.in = ptr(L.src);
@@ -758,9 +764,14 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         l.vec = (l.cin % KSTEP) == 0 && !(dtype == FS_BF16 && i == 0);
         const int nbt0 = (l.cout + 15) / 16;
         choose_channel_tile(nbt0, l.vec, &l.nb, &l.wn);
-        tile_override(i, nullptr, &l.nb, &l.wn, nullptr);
-        if (!conv_tile_supported(1, l.nb, l.wn, l.vec) && !conv_tile_supported(2, l.nb, l.wn, l.vec) &&
-            !conv_tile_supported(4, l.nb, l.wn, l.vec) && !conv_tile_supported(8, l.nb, l.wn, l.vec)) {
+        // narrow channel tiles with a long K walk: two waves split K so each
+        // wave owns 4 pixel blocks (more products per operand load, measured
+        // faster on the 48 -> 48 layers of N4) without a larger LDS window
+        l.wk = (l.vec && l.wn == 1 && l.nb == 3 && l.k * l.k * l.cin >= 16 * 16) ? 2 : 1;
+        tile_override(i, nullptr, &l.nb, &l.wn, nullptr, &l.wk);
+        bool any = false;
+        for (int mb : {1, 2, 4, 8}) any = any || conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec);
+        if (!any) {
             delete net;
             return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile with %d x %d channel blocks", i,
                         l.nb, l.wn);

@@ -6,8 +6,8 @@
 
 namespace fs {
 
-hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int wn, bool vec, int gx, int gy,
-                            hipStream_t s);
+hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int wn, int wk, bool vec, int gx,
+                            int gy, hipStream_t s);
 hipError_t launch_conv_ws_bf16(const ConvArgs &a, int mb, int nb, int wn, int gx, int gy, hipStream_t s);
 
 bool conv_ws_supported(int mb, int nb, int wn)
@@ -50,10 +50,10 @@ std::string conv_ws_kernel_name(int dtype, int mb, int nb, int wn)
     return buf;
 }
 
-bool conv_tile_supported(int mb, int nb, int wn, bool vec)
+bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec)
 {
-#define FS_CONV_HAS(M, N, W) \
-    if (mb == M && nb == N && wn == W) return true;
+#define FS_CONV_HAS(M, N, W, K) \
+    if (mb == M && nb == N && wn == W && wk == K) return true;
     if (vec) {
         FS_CONV_TILES_VEC(FS_CONV_HAS)
     } else {
@@ -63,19 +63,19 @@ bool conv_tile_supported(int mb, int nb, int wn, bool vec)
     return false;
 }
 
-hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, bool vec, int gx,
-                       int gy, hipStream_t s)
+hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec,
+                       int gx, int gy, hipStream_t s)
 {
-    if (dtype == DT_BF16) return launch_conv_bf16(a, in_f32, mb, nb, wn, vec, gx, gy, s);
-    return vec ? conv::dispatch_tile<false, false, true>(a, mb, nb, wn, gx, gy, s)
-               : conv::dispatch_tile<false, false, false>(a, mb, nb, wn, gx, gy, s);
+    if (dtype == DT_BF16) return launch_conv_bf16(a, in_f32, mb, nb, wn, wk, vec, gx, gy, s);
+    return vec ? conv::dispatch_tile<false, false, true>(a, mb, nb, wn, wk, gx, gy, s)
+               : conv::dispatch_tile<false, false, false>(a, mb, nb, wn, wk, gx, gy, s);
 }
 
-std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, bool vec)
+std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec)
 {
     char buf[96];
     const bool bf = dtype == DT_BF16;
-    snprintf(buf, sizeof buf, "conv_frag_mfma<%d, %d, %d, %s, %s, %s>", mb, nb, wn, bf ? "true" : "false",
+    snprintf(buf, sizeof buf, "conv_frag_mfma<%d, %d, %d, %d, %s, %s, %s>", mb, nb, wn, wk, bf ? "true" : "false",
              bf && in_f32 ? "true" : "false", vec ? "true" : "false");
     return buf;
 }

@@ -191,7 +191,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int 
     }
 }
 
-template <int MB, int NB, int WN, bool BF, bool IN_F32, bool VEC>
+template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC>
 __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 {
     using TC = typename Elem<BF>::T;                                // LDS / operand element
@@ -293,8 +293,13 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     __syncthreads();
 
     // ---- matrix-core main loop ----------------------------------------------
+    // wave (wm, wn, wk): pixel blocks wm*MB.., channel blocks wn*NB.., and the
+    // wk-th of WK equal parts of the K steps (their partial sums are added up
+    // through LDS after the loop)
+    constexpr int WMN = 4 / WK;
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-    const int wm = wv / WN, wn = wv - (wv / WN) * WN;
+    const int wk = wv / WMN, wmn = wv - (wv / WMN) * WMN;
+    const int wm = wmn / WN, wn = wmn - (wmn / WN) * WN;
     const int lm = lane & 15, g = lane >> 4;
     const int nb0 = blockIdx.y * (WN * NB) + wn * NB;
 
@@ -345,10 +350,11 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         // (two register buffers, the loop unrolled by two) and pixels one step
         // ahead, so the products of a step never wait on the loads it needs.
         const int ncc = a.cin / KSTEP;
-        const int nsteps = a.ksteps;
+        const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
+        const int nsteps = s_end - s_begin;
         // (branch-free: a straight-line loop body lets the compiler wait only
         // for the operands each product needs)
-        int dy = 0, dx = 0, cc = 0;
+        int cc = s_begin % ncc, dx = (s_begin / ncc) % a.k, dy = (s_begin / ncc) / a.k;
         auto advance = [&](int) {
             ++cc;
             const int w1 = cc == ncc;
@@ -360,20 +366,22 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             return (dy * Cc + dx) * CS + cc * KSTEP;
         };
         u4 b0[NB], b1[NB], a0[MB], a1[MB];
+        const u4 *wpk = wp + (size_t)s_begin * wstep;
+        const int off0 = (dy * Cc + dx) * CS + cc * KSTEP;
 #pragma unroll
-        for (int j = 0; j < NB; ++j) b0[j] = wp[j * 64];
+        for (int j = 0; j < NB; ++j) b0[j] = wpk[j * 64];
         // unconditional (clamped) so every path reaches the loop with the same
         // loads in flight
 #pragma unroll
-        for (int j = 0; j < NB; ++j) b1[j] = wp[(nsteps > 1 ? wstep : 0) + j * 64];
+        for (int j = 0; j < NB; ++j) b1[j] = wpk[(nsteps > 1 ? wstep : 0) + j * 64];
 #pragma unroll
-        for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i]);
+        for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
         // The prefetches are issued on every iteration (past the end they
         // re-read the last step's weights and the window's first pixel), so
         // every path through the loop has the same loads in flight and the
         // waits before the products only cover the operands they use.
         const int last = nsteps - 1;
-        int off = 0;
+        int off = off0;
         int s = 0;
         for (; s + 1 < nsteps; s += 2) {
             // scheduling barriers keep each prefetch ahead of the products
@@ -387,9 +395,9 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             __builtin_amdgcn_sched_barrier(0);
             const size_t w2 = (size_t)min(s + 2, last) * wstep;
 #pragma unroll
-            for (int j = 0; j < NB; ++j) b0[j] = wp[w2 + j * 64];
+            for (int j = 0; j < NB; ++j) b0[j] = wpk[w2 + j * 64];
             off = advance(off);  // step s + 2
-            const int offa = s + 2 < nsteps ? off : 0;
+            const int offa = s + 2 < nsteps ? off : off0;
 #pragma unroll
             for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
             __builtin_amdgcn_sched_barrier(0);
@@ -397,15 +405,16 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             __builtin_amdgcn_sched_barrier(0);
             const size_t w3 = (size_t)min(s + 3, last) * wstep;
 #pragma unroll
-            for (int j = 0; j < NB; ++j) b1[j] = wp[w3 + j * 64];
+            for (int j = 0; j < NB; ++j) b1[j] = wpk[w3 + j * 64];
         }
         if (s < nsteps) mma(a0, b0);
     } else {
+        const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
         u4 bcur[NB], bnxt[NB];
 #pragma unroll
-        for (int j = 0; j < NB; ++j) bcur[j] = wp[j * 64];
-        for (int s = 0; s < a.ksteps; ++s) {
-            const bool more = s + 1 < a.ksteps;
+        for (int j = 0; j < NB; ++j) bcur[j] = wp[(size_t)s_begin * wstep + j * 64];
+        for (int s = s_begin; s < s_end; ++s) {
+            const bool more = s + 1 < s_end;
             if (more) {
 #pragma unroll
                 for (int j = 0; j < NB; ++j) bnxt[j] = wp[(size_t)(s + 1) * wstep + j * 64];
@@ -430,44 +439,100 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
     }
 
-    // ---- epilogue -------------------------------------------------------------
+    // ---- split-K reduction ----------------------------------------------------
+    if constexpr (WK > 1) {
+        constexpr int RV = MB * NB * 4;  // accumulator floats per lane
+        float *part = reinterpret_cast<float *>(smem);
+        __syncthreads();  // the window is no longer read
+        if (wk > 0) {
+            float *dst = part + ((size_t)((wk - 1) * WMN + wmn) * RV) * 64 + lane;
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) dst[(size_t)((i * NB + j) * 4 + e) * 64] = acc[i][j][e];
+        }
+        __syncthreads();
+        if (wk == 0) {
+#pragma unroll
+            for (int w = 1; w < WK; ++w) {
+                const float *src = part + ((size_t)((w - 1) * WMN + wmn) * RV) * 64 + lane;
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+#pragma unroll
+                    for (int j = 0; j < NB; ++j)
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) acc[i][j][e] += src[(size_t)((i * NB + j) * 4 + e) * 64];
+            }
+        }
+    }
+
+    // ---- epilogue (only the wk == 0 waves hold the sums) ----------------------
     if (a.head_ncls > 0) {
         float *red = reinterpret_cast<float *>(smem);
-        __syncthreads();  // the LDS window (which red reuses) is no longer read
-        fused_head_partials<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, red);
+        __syncthreads();  // the LDS window / partial sums (which red reuses) are no longer read
+        if (wk == 0) fused_head_partials<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, red);
         __syncthreads();
         fused_head_finish<WN>(a, q, fy, fx, l0, lend, twb, c0, red);
         return;
     }
-    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
+    // Outputs go back through LDS: each lane drops its act(acc + bias) values
+    // into a [pixel][channel] tile, then all threads copy the tile out with
+    // 16-byte stores; the pixels of a band row are contiguous in memory, so a
+    // tile row leaves as one contiguous run.
+    constexpr int NW = WN * NB * 16;              // channels this workgroup owns
+    constexpr int TPAD = 16 / (int)sizeof(TC);    // 16 bytes of row padding
+    constexpr int TS = NW + TPAD;
+    const int nbase = blockIdx.y * NW;
+    TC *tile = reinterpret_cast<TC *>(smem);
+    __syncthreads();  // every wave is done with the window / partial sums
+    if (wk == 0) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        const int co = (nb0 + j) * 16 + lm;
-        if (co >= a.cout) continue;
-        const float bv = a.bias[co];
+        const int col = (wn * NB + j) * 16 + lm;
+        const float bv = a.bias[nbase + col];  // zero padded past cout
 #pragma unroll
-        for (int i = 0; i < MB; ++i) {
+        for (int i = 0; i < MB; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int l = l0 + (wm * MB + i) * 16 + 4 * g + e;
-                if (l >= lend) continue;
-                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
                 float v = acc[i][j][e] + bv;
                 if (a.act == ACT_TANH) v = tanh_fast(v);
-                TC *dst = outp + ((size_t)y * a.out_w + x) * a.cout + co;
+                const int m = (wm * MB + i) * 16 + 4 * g + e;
                 if constexpr (BF)
-                    *dst = f2bf(v);
+                    tile[m * TS + col] = f2bf(v);
                 else
-                    *dst = v;
+                    tile[m * TS + col] = v;
             }
+    }
+    }
+    __syncthreads();
+    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
+    const int nch = min(NW, a.cout - nbase);
+    const int npx = lend - l0;
+    if ((a.cout % TPAD) == 0 && (nch % TPAD) == 0) {
+        const int nv = nch / TPAD;
+        for (int idx = threadIdx.x; idx < npx * nv; idx += 256) {
+            const int m = idx / nv, v = idx - (idx / nv) * nv;
+            const int l = l0 + m;
+            const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+            *reinterpret_cast<u4 *>(outp + ((size_t)y * a.out_w + x) * a.cout + v * TPAD) =
+                *reinterpret_cast<const u4 *>(tile + m * TS + v * TPAD);
+        }
+    } else {
+        for (int idx = threadIdx.x; idx < npx * nch; idx += 256) {
+            const int m = idx / nch, c = idx - (idx / nch) * nch;
+            const int l = l0 + m;
+            const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+            outp[((size_t)y * a.out_w + x) * a.cout + c] = tile[m * TS + c];
         }
     }
 }
 
-template <int MB, int NB, int WN, bool BF, bool IN_F32, bool VEC>
+template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC>
 hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
 {
-    auto kern = conv_frag_mfma<MB, NB, WN, BF, IN_F32, VEC>;
+    auto kern = conv_frag_mfma<MB, NB, WN, WK, BF, IN_F32, VEC>;
     if (a.lds_bytes > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
@@ -477,21 +542,25 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
     return hipGetLastError();
 }
 
-// The register tiles each operand variant is built for.
-#define FS_CONV_TILES_VEC(X)                                                                   \
-    X(1, 1, 1) X(1, 2, 1) X(1, 3, 1) X(1, 4, 1) X(2, 1, 1) X(2, 2, 1) X(2, 3, 1) X(2, 4, 1)     \
-    X(4, 1, 1) X(4, 2, 1) X(4, 3, 1) X(4, 4, 1) X(1, 7, 1) X(1, 8, 1) X(1, 13, 1) X(2, 7, 1)   \
-    X(2, 8, 1) X(2, 13, 1) X(2, 2, 2) X(2, 4, 2) X(2, 7, 2) X(4, 2, 2) X(4, 4, 2) X(4, 7, 2)   \
-    X(4, 2, 4) X(4, 4, 4) X(8, 2, 4) X(8, 4, 4)
-#define FS_CONV_TILES_GATHER(X)                                                                \
-    X(1, 1, 1) X(1, 2, 1) X(1, 3, 1) X(1, 4, 1) X(2, 1, 1) X(2, 2, 1) X(2, 3, 1) X(2, 4, 1)     \
-    X(4, 1, 1) X(4, 2, 1) X(4, 3, 1) X(4, 4, 1)
+// The register tiles each operand variant is built for: (MB, NB, WN, WK).
+#define FS_CONV_TILES_VEC(X)                                                                    \
+    X(1, 1, 1, 1) X(1, 2, 1, 1) X(1, 3, 1, 1) X(1, 4, 1, 1) X(2, 1, 1, 1) X(2, 2, 1, 1)          \
+    X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 1) X(4, 4, 1, 1)          \
+    X(1, 7, 1, 1) X(1, 8, 1, 1) X(1, 13, 1, 1) X(2, 7, 1, 1) X(2, 8, 1, 1) X(2, 13, 1, 1)        \
+    X(2, 2, 2, 1) X(2, 4, 2, 1) X(2, 7, 2, 1) X(4, 2, 2, 1) X(4, 4, 2, 1) X(4, 7, 2, 1)          \
+    X(4, 2, 4, 1) X(4, 4, 4, 1) X(8, 2, 4, 1) X(8, 4, 4, 1)                                      \
+    X(4, 1, 1, 2) X(4, 2, 1, 2) X(4, 3, 1, 2) X(4, 4, 1, 2) X(8, 1, 1, 4) X(8, 2, 1, 4)          \
+    X(8, 3, 1, 4) X(8, 4, 1, 4) X(4, 7, 2, 2) X(4, 4, 2, 2) X(4, 2, 2, 2) X(4, 7, 1, 2)          \
+    X(2, 13, 1, 2)
+#define FS_CONV_TILES_GATHER(X)                                                                 \
+    X(1, 1, 1, 1) X(1, 2, 1, 1) X(1, 3, 1, 1) X(1, 4, 1, 1) X(2, 1, 1, 1) X(2, 2, 1, 1)          \
+    X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 1) X(4, 4, 1, 1)
 
 template <bool BF, bool IN_F32, bool VEC>
-hipError_t dispatch_tile(const ConvArgs &a, int mb, int nb, int wn, int gx, int gy, hipStream_t s)
+hipError_t dispatch_tile(const ConvArgs &a, int mb, int nb, int wn, int wk, int gx, int gy, hipStream_t s)
 {
-#define FS_CONV_CASE(M, N, W) \
-    if (mb == M && nb == N && wn == W) return launch_one<M, N, W, BF, IN_F32, VEC>(a, gx, gy, s);
+#define FS_CONV_CASE(M, N, W, K) \
+    if (mb == M && nb == N && wn == W && wk == K) return launch_one<M, N, W, K, BF, IN_F32, VEC>(a, gx, gy, s);
     if constexpr (VEC) {
         FS_CONV_TILES_VEC(FS_CONV_CASE)
     } else {

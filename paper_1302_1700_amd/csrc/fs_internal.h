@@ -50,7 +50,7 @@ struct ConvArgs {
     int band_w;           // output columns per band
     int nbands;           // bands per fragment
     int tiles_per_band;   // tiles per band (enough for the tallest fragment)
-    int mt;               // output pixels per tile (16 * MB * 4 / WN)
+    int mt;               // output pixels per tile (16 * MB * 4 / (WN * WK))
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
     int win_bytes;        // one window buffer (persistent kernel: two of them)
@@ -94,8 +94,9 @@ struct HeadArgs {
 // Launchers (return hipSuccess or the launch error).  `dtype` selects the
 // operand type; `in_f32` says the input is float32 even in a bf16 net (the
 // image).  Convolution register tiles: mb pixel blocks x nb channel blocks per
-// wave, wn waves across the output channels (4 / wn across the pixels).
-hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, bool vec,
+// wave, wn waves across the output channels, wk waves splitting the K steps,
+// 4 / (wn * wk) across the pixels.
+hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
 // Persistent wave-specialised variant (vector path; 512 threads).
 hipError_t launch_conv_ws(const ConvArgs &a, int dtype, int mb, int nb, int wn, int grid_x, int grid_y,
@@ -106,10 +107,10 @@ int conv_ws_occupancy(int dtype, int mb, int nb, int wn, int lds_bytes);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
-bool conv_tile_supported(int mb, int nb, int wn, bool vec);
+bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);
 
 // Kernel names as the profiler reports them (for measurement reports).
-std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, bool vec);
+std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec);
 std::string conv_ws_kernel_name(int dtype, int mb, int nb, int wn);
 const char *pool_kernel_name(int dtype, bool in_f32);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);

@@ -295,3 +295,16 @@ def test_unfused_head_paths(fsb, monkeypatch):
     for dt in ("f32", "bf16"):
         got = _scan(fsb, layers, params, img, 2, dtype=dt)
         assert np.abs(got - ref).max() <= TOL[dt], dt
+
+
+@pytest.mark.parametrize("tile", ["2:4,3,1,16,2;4:8,3,1,16,4;6:4,3,1,0,2;8:4,7,2,0,2",
+                                  "2:8,3,1,0,4;4:4,3,1,0,2;8:2,13,1,0,2"])
+def test_split_k_tiles(fsb, monkeypatch, tile):
+    """Register tiles whose waves split the K steps (partial sums reduced
+    through LDS), forced through the tile override on net N4."""
+    w = wl.WORKLOADS[2]
+    params, img = wl.workload_inputs(2, height=171, width=160)
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    monkeypatch.setenv("FRAGSCAN_TILE", tile)
+    got = _scan(fsb, w.layers, params, img, 1)
+    assert np.abs(got - ref).max() <= TOL["f32"]
