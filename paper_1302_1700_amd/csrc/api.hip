@@ -64,6 +64,8 @@ struct NetLayer {
     int nbt = 0;          // channel blocks, padded to a multiple of nb * wn
     int ksteps = 0;
     size_t w_off = 0, b_off = 0;  // offsets into the net's device block
+    bool has_w32 = false;         // OIHW float32 copy for the direct kernel
+    size_t w32_off = 0;
 };
 
 }  // namespace
@@ -165,6 +167,11 @@ void choose_channel_tile(int nbt, bool vec, int *nb, int *wn)
         if (*nb == 0) *nb = 1;
         return;
     }
+    if (nbt == 7) {  // one wave owns all seven blocks (no padding block)
+        *wn = 1;
+        *nb = 7;
+        return;
+    }
     *wn = 2;
     *nb = nbt <= 8 ? 4 : 7;
 }
@@ -191,6 +198,7 @@ struct Launch {
     int mb = 0, nb = 0, wn = 1, wk = 1;
     bool vec = false, has_fc = false;
     bool ws = false;          // persistent wave-specialised convolution
+    bool direct = false;      // vector-ALU convolution for tiny K
     int ws_slots = 0;         // resident workgroups of the persistent kernel
     int gx = 1, gy = 1;
     int frags = 0;
@@ -290,8 +298,11 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             return FS_OK;
         }
     }
-    // two pixel blocks per wave first (four with split K), then the neighbours
-    const int mbs[4] = {l.wk == 2 ? 4 : 2, l.wk == 2 ? 2 : 4, 1, 8};
+    // pixel blocks per wave: four when a wave owns at most four channel
+    // blocks (more products per operand load; measured faster on every such
+    // layer), else two; then the neighbours
+    const int mb_pref = (l.vec && l.nb <= 4) ? 4 : 2;
+    const int mbs[4] = {mb_pref, mb_pref == 4 ? 2 : 4, 1, 8};
     for (int mi = 0; mi < 4; ++mi) {
         const int mb = mb_force ? mb_force : mbs[mi];
         if (!conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
@@ -447,19 +458,32 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             a.ksteps = l.ksteps;
             a.nbt = l.nbt;
             fill_axis(a.ext, g);
-            fs_status st = plan_conv_tiles(net, l, g, L);
-            if (st != FS_OK) return st;
-            L.gx = B * F * a.nbands * a.tiles_per_band;
-            L.gy = l.nbt / (l.nb * l.wn);
+            const bool fused_here = fuse && li == body - 1;
+            // Small-K layers with one 16-channel output block reuse each
+            // gathered A fragment only once on the matrix cores; there the
+            // per-pixel vector-ALU kernel is faster.  FRAGSCAN_DIRECT=1 takes
+            // it for every layer it supports, =0 for none.
+            const char *dv = getenv("FRAGSCAN_DIRECT");
+            const bool want_direct = dv ? dv[0] == '1' : l.cout <= 16;
+            if (l.has_w32 && !fused_here && want_direct) {
+                L.direct = true;
+                L.conv.lds_bytes = 0;
+            } else {
+                fs_status st = plan_conv_tiles(net, l, g, L);
+                if (st != FS_OK) return st;
+            }
+            L.gx = L.direct ? B * F * ((a.out_h * a.out_w + 255) / 256) : B * F * a.nbands * a.tiles_per_band;
+            L.gy = L.direct ? 1 : l.nbt / (l.nb * l.wn);
             if (L.ws) L.gx = std::max(1, std::min(L.gx, L.ws_slots / L.gy));
-            else L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
+            else if (!L.direct) L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
-            L.name = L.ws ? conv_ws_kernel_name(net->dtype, L.mb, L.nb, L.wn)
-                          : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
+            L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, k)
+                     : L.ws   ? conv_ws_kernel_name(net->dtype, L.mb, L.nb, L.wn)
+                              : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
                 a.head_ncls = net->ncls;
@@ -596,6 +620,9 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
             L.conv.head_out = d_out;
             L.conv.out = nullptr;
         }
+        if (L.direct)
+            return launch_conv_direct(L.conv, reinterpret_cast<const float *>(mem + l.w32_off), net->dtype,
+                                      L.in_f32, L.gx, s);
         if (L.ws) return launch_conv_ws(L.conv, net->dtype, L.mb, L.nb, L.wn, L.gx, L.gy, s);
         return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.wk, L.vec, L.gx, L.gy, s);
     }
@@ -785,6 +812,24 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         std::vector<float> bp((size_t)l.nbt * 16, 0.f);
         std::copy(bias.begin(), bias.end(), bp.begin());
         l.b_off = push(bp.data(), bp.size() * 4);
+        if (!l.vec && conv_direct_supported(l.cin, l.k, l.cout)) {
+            // [c_out][KP] copy for the direct kernel, K index (dy * k + dx) * c_in + ci
+            const int kp = conv_direct_kp(l.cin, l.k);
+            std::vector<float> wd((size_t)l.cout * kp, 0.f);
+            for (int co = 0; co < l.cout; ++co)
+                for (int dy = 0; dy < l.k; ++dy)
+                    for (int dx = 0; dx < l.k; ++dx)
+                        for (int ci = 0; ci < l.cin; ++ci) {
+                            float v = s.weight[(((size_t)co * l.cin + ci) * l.k + dy) * l.k + dx];
+                            if (dtype == FS_BF16) {
+                                const uint32_t u = (uint32_t)host_f2bf(v) << 16;
+                                std::memcpy(&v, &u, 4);
+                            }
+                            wd[(size_t)co * kp + (dy * l.k + dx) * l.cin + ci] = v;
+                        }
+            l.has_w32 = true;
+            l.w32_off = push(wd.data(), wd.size() * 4);
+        }
     }
     if (!net->head_fc) {  // the head still takes a (unused) bias pointer
         std::vector<float> z(kMaxHeadClasses, 0.f);

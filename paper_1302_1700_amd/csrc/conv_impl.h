@@ -551,7 +551,7 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
     X(4, 2, 4, 1) X(4, 4, 4, 1) X(8, 2, 4, 1) X(8, 4, 4, 1)                                      \
     X(4, 1, 1, 2) X(4, 2, 1, 2) X(4, 3, 1, 2) X(4, 4, 1, 2) X(8, 1, 1, 4) X(8, 2, 1, 4)          \
     X(8, 3, 1, 4) X(8, 4, 1, 4) X(4, 7, 2, 2) X(4, 4, 2, 2) X(4, 2, 2, 2) X(4, 7, 1, 2)          \
-    X(2, 13, 1, 2)
+    X(2, 13, 1, 2) X(8, 1, 1, 1) X(8, 2, 1, 1) X(4, 7, 1, 1) X(4, 8, 1, 1) X(8, 2, 2, 1)
 #define FS_CONV_TILES_GATHER(X)                                                                 \
     X(1, 1, 1, 1) X(1, 2, 1, 1) X(1, 3, 1, 1) X(1, 4, 1, 1) X(2, 1, 1, 1) X(2, 2, 1, 1)          \
     X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 1) X(4, 4, 1, 1)

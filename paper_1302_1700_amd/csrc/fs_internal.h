@@ -108,6 +108,14 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);
+// Direct (vector-ALU) convolution for tiny K = c_in * k * k (<= 64) and
+// c_out <= 64; wpk = weights as [c_out][KP] float32, K index
+// (dy * k + dx) * c_in + ci, zero padded to KP = conv_direct_kp(c_in, k)
+// (bf16 nets: values rounded to bf16).  One thread per pixel.
+bool conv_direct_supported(int cin, int k, int cout);
+int conv_direct_kp(int cin, int k);
+hipError_t launch_conv_direct(const ConvArgs &a, const float *wpk, int dtype, bool in_f32, int grid, hipStream_t s);
+std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int k);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec);

@@ -177,6 +177,7 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
 #pragma unroll
     for (int i = 0; i < K - 1; ++i) hmax(y0 + i, win[i + 1]);
     const int ox = x % K, xbar = x / K;
+#pragma unroll 8
     for (int y = y0; y < yend; ++y) {
 #pragma unroll
         for (int i = 0; i < K - 1; ++i)

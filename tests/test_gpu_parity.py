@@ -308,3 +308,17 @@ def test_split_k_tiles(fsb, monkeypatch, tile):
     monkeypatch.setenv("FRAGSCAN_TILE", tile)
     got = _scan(fsb, w.layers, params, img, 1)
     assert np.abs(got - ref).max() <= TOL["f32"]
+
+
+@pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
+def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
+    """Small-K layers take either the per-pixel vector-ALU kernel or the
+    matrix-core gather kernel; force the one the planner does not pick by
+    default for the workload's first layers."""
+    w = wl.WORKLOADS[wid]
+    H = {1: 64, 2: 140, 3: 150, 5: 120}[wid]
+    params, img = wl.workload_inputs(wid, height=H, width=H + 9)
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    monkeypatch.setenv("FRAGSCAN_DIRECT", mode)
+    got = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    assert np.abs(got - ref).max() <= TOL[w.dtype]
