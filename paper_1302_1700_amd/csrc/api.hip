@@ -76,9 +76,9 @@ struct fs_net {
     std::vector<int> pool_k;
     int S = 1, F = 1;
     int device = 0;
-    int ncu = 256;            // compute units of the device (persistent grids)
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
+    size_t head_wp_off = 0;   // head weights in the previous layer's (block, row) order
     int head_cin = 0;
     void *d_mem = nullptr;
     size_t mem_bytes = 0;
@@ -95,6 +95,20 @@ int elem_of(int dtype) { return dtype == DT_BF16 ? 2 : 4; }
 //   vector path: tap = s / (cin / KSTEP), ci = (s % (cin / KSTEP)) * KSTEP + g*LPE + e
 //   gather path: kk = s*KSTEP + g*LPE + e, tap = kk / cin, ci = kk % cin
 // with tap = dy * k + dx; zero where the channel or K index is past the end.
+// Output channel computed by row `row` of channel block `blk`.  The products
+// leave row 4g + e of a block in lane (pixel, g), element e, so a lane holds
+// four rows of every block.  bfloat16 layers whose waves own an even number
+// of blocks pair blocks (2p, 2p + 1): rows 4g .. 4g + 3 of the pair are
+// channels 32p + 8g + 0..3 and 32p + 8g + 4..7, eight consecutive channels
+// that leave in one 16-byte store; otherwise block rows are channels in order
+// (four consecutive float32 channels are 16 bytes already).
+int chan_of(const NetLayer &l, int dtype, int blk, int row)
+{
+    if (dtype != DT_BF16 || (l.nb % 2) != 0) return blk * 16 + row;
+    const int p = blk / 2, h = blk % 2, g = row / 4, e = row % 4;
+    return 32 * p + 8 * g + 4 * h + e;
+}
+
 void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector<uint8_t> &out)
 {
     const int KSTEP = kstep_of(dtype), LPE = KSTEP / 4, es = elem_of(dtype);
@@ -106,7 +120,7 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
             for (int lane = 0; lane < 64; ++lane)
                 for (int e = 0; e < LPE; ++e) {
                     const int g = lane / 16, nn = lane % 16;
-                    const int co = nb * 16 + nn;
+                    const int co = chan_of(l, dtype, nb, nn);
                     int tap, ci;
                     if (l.vec) {
                         const int ncc = l.cin / KSTEP;
@@ -132,22 +146,25 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
                 }
 }
 
-// Optional tile override for tuning sweeps: FRAGSCAN_TILE="L:MB,NB,WN[,BAND[,WK]];..."
-// (L = layer index); any field <= 0 keeps the planner's choice.
-bool tile_override(int layer, int *mb, int *nb, int *wn, int *band, int *wk = nullptr)
+// Optional tile override for tuning sweeps:
+// FRAGSCAN_TILE="L:MB,NB,WN[,BAND[,WK[,LDS]]];..." (L = layer index, LDS = least
+// dynamic LDS bytes per workgroup, which caps the workgroups per CU); any
+// field <= 0 keeps the planner's choice.
+bool tile_override(int layer, int *mb, int *nb, int *wn, int *band, int *wk = nullptr, int *lds = nullptr)
 {
     const char *env = getenv("FRAGSCAN_TILE");
     if (!env) return false;
     const char *p = env;
     while (*p) {
-        int L = -1, a = 0, b = 0, c = 0, d = 0, e = 0;
-        const int n = sscanf(p, "%d:%d,%d,%d,%d,%d", &L, &a, &b, &c, &d, &e);
+        int L = -1, a = 0, b = 0, c = 0, d = 0, e = 0, f = 0;
+        const int n = sscanf(p, "%d:%d,%d,%d,%d,%d,%d", &L, &a, &b, &c, &d, &e, &f);
         if (n >= 4 && L == layer) {
             if (mb && a > 0) *mb = a;
             if (nb && b > 0) *nb = b;
             if (wn && c > 0) *wn = c;
             if (band && n >= 5 && d > 0) *band = d;
             if (wk && n >= 6 && e > 0) *wk = e;
+            if (lds && n >= 7 && f > 0) *lds = f;
             return true;
         }
         const char *semi = strchr(p, ';');
@@ -197,9 +214,7 @@ struct Launch {
     HeadArgs head;
     int mb = 0, nb = 0, wn = 1, wk = 1;
     bool vec = false, has_fc = false;
-    bool ws = false;          // persistent wave-specialised convolution
     bool direct = false;      // vector-ALU convolution for tiny K
-    int ws_slots = 0;         // resident workgroups of the persistent kernel
     int gx = 1, gy = 1;
     int frags = 0;
     long long out_pixels = 0;
@@ -244,7 +259,7 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     // pixel stride in LDS: +16 bytes per pixel spreads 16 consecutive pixels'
     // 16-byte reads over distinct banks (FRAGSCAN_LDS_PAD overrides, elements)
     int pad = 16 / es;
-    if (const char *e = getenv("FRAGSCAN_LDS_PAD")) pad = atoi(e) / (l.vec ? 1 : 1);
+    if (const char *e = getenv("FRAGSCAN_LDS_PAD")) pad = atoi(e);
     if (l.vec && (pad * es) % 16) pad = 16 / es;
     const int cs = l.vec ? l.cin + pad : l.cin;
     const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
@@ -254,50 +269,8 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
         if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
             wouts.push_back(v - k + 1);
     const int wm = 4 / (l.wn * l.wk);
-    int mb_force = 0, band_force = 0;
-    tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
-    if (l.vec && l.wk == 1 && getenv("FRAGSCAN_WS")) {  // opt-in: not yet faster than the 4-wave kernel
-        // persistent kernel: two window buffers and the fused-head reduction
-        const int mbs_ws[3] = {2, 1, 4};
-        for (int mi = 0; mi < 3; ++mi) {
-            const int mb = mb_force ? mb_force : mbs_ws[mi];
-            if (!conv_ws_supported(mb, l.nb, l.wn)) {
-                if (mb_force) break;
-                continue;
-            }
-            const int mt = 16 * mb * wm;
-            int nbands = wout_max <= 32 ? 1 : (wout_max + 15) / 16;
-            if (band_force) nbands = (wout_max + band_force - 1) / band_force;
-            const int band_w = (wout_max + nbands - 1) / nbands;
-            int tmin = band_w;
-            for (int wo : wouts)
-                for (int b = 0; b < nbands; ++b) {
-                    const int twb = std::min(band_w, wo - b * band_w);
-                    if (twb > 0) tmin = std::min(tmin, twb);
-                }
-            const int rmax = std::min((mt - 1 + tmin - 1) / tmin + k, in.hmax);
-            const size_t win = align_up((size_t)rmax * (band_w + k - 1) * cs * es, 16);
-            const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;
-            const size_t lds = 2 * win + red;
-            if (lds > 160 * 1024) {
-                if (mb_force) break;
-                continue;
-            }
-            L.ws = true;
-            L.mb = mb;
-            L.conv.band_w = band_w;
-            L.conv.nbands = nbands;
-            L.conv.mt = mt;
-            L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
-            L.conv.lds_cs = cs;
-            L.conv.win_bytes = (int)win;
-            L.conv.lds_bytes = (int)lds;
-            int occ = net->device >= 0 ? conv_ws_occupancy(net->dtype, mb, l.nb, l.wn, (int)lds) : 0;
-            if (occ <= 0) occ = std::max(1, std::min(2, (int)((160 * 1024) / lds)));
-            L.ws_slots = net->ncu * occ;
-            return FS_OK;
-        }
-    }
+    int mb_force = 0, band_force = 0, lds_min = 0;
+    tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force, nullptr, &lds_min);
     // pixel blocks per wave: four when a wave owns at most four channel
     // blocks (more products per operand load; measured faster on every such
     // layer), else two; then the neighbours
@@ -330,8 +303,6 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                 continue;
             }
             const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;  // fused-head reduction
-            // output tile restaged through LDS: [mt][wn * nb * 16 + 16 bytes]
-            const size_t otile = (size_t)mt * (l.wn * l.nb * 16 + 16 / es) * es;
             // split-K partial sums of the waves with wk > 0
             const size_t part = (size_t)(l.wk - 1) * (4 / l.wk) * mb * l.nb * 4 * 64 * 4;
             L.mb = mb;
@@ -340,7 +311,20 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             L.conv.mt = mt;
             L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
             L.conv.lds_cs = cs;
-            L.conv.lds_bytes = (int)std::max(std::max(lds, part), std::max(red, otile));
+            // Stores: straight from the registers when a pixel's channels
+            // fit in 64 bytes (each store instruction then covers whole
+            // pixels), else restaged through an LDS tile [mt][wn*nb*16 + 16
+            // bytes] (FRAGSCAN_STORE=direct / lds overrides, for tuning).
+            int direct = l.nbt * 16 * es <= 64;
+            if (const char *e = getenv("FRAGSCAN_STORE"); e && e[0]) direct = e[0] == 'd';
+            const size_t otile = direct ? 0 : (size_t)mt * (l.wn * l.nb * 16 + 16 / es) * es;
+            L.conv.direct_store = direct;
+            const size_t need = std::max(std::max(std::max(lds, part), std::max(red, otile)), (size_t)lds_min);
+            if (need > kMaxLdsBytes) {
+                if (mb_force) break;
+                continue;
+            }
+            L.conv.lds_bytes = (int)need;
             return FS_OK;
         }
         if (mb_force) break;
@@ -474,15 +458,13 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             }
             L.gx = L.direct ? B * F * ((a.out_h * a.out_w + 255) / 256) : B * F * a.nbands * a.tiles_per_band;
             L.gy = L.direct ? 1 : l.nbt / (l.nb * l.wn);
-            if (L.ws) L.gx = std::max(1, std::min(L.gx, L.ws_slots / L.gy));
-            else if (!L.direct) L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
+            if (!L.direct) L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
             L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, k)
-                     : L.ws   ? conv_ws_kernel_name(net->dtype, L.mb, L.nb, L.wn)
                               : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
@@ -615,7 +597,7 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
         L.conv.w = mem + l.w_off;
         L.conv.bias = reinterpret_cast<const float *>(mem + l.b_off);
         if (L.conv.head_ncls > 0) {
-            L.conv.head_w = reinterpret_cast<const float *>(mem + net->head_w_off);
+            L.conv.head_w = reinterpret_cast<const float *>(mem + net->head_wp_off);
             L.conv.head_b = reinterpret_cast<const float *>(mem + net->head_b_off);
             L.conv.head_out = d_out;
             L.conv.out = nullptr;
@@ -623,7 +605,6 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
         if (L.direct)
             return launch_conv_direct(L.conv, reinterpret_cast<const float *>(mem + l.w32_off), net->dtype,
                                       L.in_f32, L.gx, s);
-        if (L.ws) return launch_conv_ws(L.conv, net->dtype, L.mb, L.nb, L.wn, L.gx, L.gy, s);
         return launch_conv(L.conv, net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.wk, L.vec, L.gx, L.gy, s);
     }
     if (L.type == 1) {
@@ -784,6 +765,19 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
             std::memcpy(w.data(), s.weight, sizeof(float) * w.size());
             net->head_w_off = push(w.data(), w.size() * 4);
             net->head_b_off = push(bias.data(), bias.size() * 4);
+            // the same weights over the previous layer's (block, row) order,
+            // for the head fused into that layer's epilogue
+            if (i >= 1 && L[i - 1].kind != FS_MAXPOOL && L[i - 1].nbt > 0) {
+                const NetLayer &pl = L[i - 1];
+                // at least kMaxFusedClasses rows (zero past the classes)
+                std::vector<float> wp((size_t)std::max(l.cout, kMaxFusedClasses) * pl.nbt * 16, 0.f);
+                for (int c = 0; c < l.cout; ++c)
+                    for (int r = 0; r < pl.nbt * 16; ++r) {
+                        const int ci = chan_of(pl, dtype, r / 16, r % 16);
+                        if (ci < l.cin) wp[(size_t)c * pl.nbt * 16 + r] = w[(size_t)c * l.cin + ci];
+                    }
+                net->head_wp_off = push(wp.data(), wp.size() * 4);
+            }
             continue;
         }
         // the layer that reads the float32 image of a bf16 net converts while
@@ -809,13 +803,20 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         std::vector<uint8_t> pw;
         pack_conv_weights(l, s.weight, dtype, pw);
         l.w_off = push(pw.data(), pw.size());
+        // bias in (block, row) order
         std::vector<float> bp((size_t)l.nbt * 16, 0.f);
-        std::copy(bias.begin(), bias.end(), bp.begin());
+        for (int r = 0; r < l.nbt * 16; ++r) {
+            const int co = chan_of(l, dtype, r / 16, r % 16);
+            if (co < l.cout) bp[r] = bias[co];
+        }
         l.b_off = push(bp.data(), bp.size() * 4);
         if (!l.vec && conv_direct_supported(l.cin, l.k, l.cout)) {
-            // [c_out][KP] copy for the direct kernel, K index (dy * k + dx) * c_in + ci
+            // [rows][KP] copy for the direct kernel, K index (dy * k + dx) * c_in + ci,
+            // then the biases in channel order
             const int kp = conv_direct_kp(l.cin, l.k);
-            std::vector<float> wd((size_t)l.cout * kp, 0.f);
+            const int rows = (l.cout + 7) / 8 * 8;
+            std::vector<float> wd((size_t)rows * kp + l.cout, 0.f);
+            std::copy(bias.begin(), bias.end(), wd.begin() + (size_t)rows * kp);
             for (int co = 0; co < l.cout; ++co)
                 for (int dy = 0; dy < l.k; ++dy)
                     for (int dx = 0; dx < l.k; ++dx)
@@ -848,11 +849,6 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         return hip_fail(e, "hipGetDevice");
     }
     net->mem_bytes = blob.size();
-    {
-        int n = 0;
-        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, net->device) == hipSuccess && n > 0)
-            net->ncu = n;
-    }
     e = hipMalloc(&net->d_mem, blob.size());
     if (e != hipSuccess) {
         delete net;
@@ -937,7 +933,7 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, f
         o.flops = L.flops;
         o.bytes = L.bytes;
         o.grid = L.gx * L.gy;
-        o.block = L.ws ? 512 : 256;
+        o.block = 256;
         std::snprintf(o.name, sizeof o.name, "%s", L.name.c_str());
     }
     return FS_OK;

@@ -1,5 +1,5 @@
 // bfloat16 instances of the fragment-batched convolution (conv_impl.h).
-#include "conv_ws.h"
+#include "conv_impl.h"
 
 namespace fs {
 
@@ -12,11 +12,6 @@ hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int 
     }
     return vec ? conv::dispatch_tile<true, false, true>(a, mb, nb, wn, wk, gx, gy, s)
                : conv::dispatch_tile<true, false, false>(a, mb, nb, wn, wk, gx, gy, s);
-}
-
-hipError_t launch_conv_ws_bf16(const ConvArgs &a, int mb, int nb, int wn, int gx, int gy, hipStream_t s)
-{
-    return conv::dispatch_ws<true>(a, mb, nb, wn, gx, gy, s);
 }
 
 }  // namespace fs

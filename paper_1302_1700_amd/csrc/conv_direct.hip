@@ -58,7 +58,8 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
         }
         offs[kk] = o;
     }
-    if (threadIdx.x < 64) bl[threadIdx.x] = threadIdx.x < a.cout ? a.bias[threadIdx.x] : 0.f;
+    const int rows = (a.cout + 7) / 8 * 8;  // weight rows (zero past c_out), then the bias
+    if (threadIdx.x < 64) bl[threadIdx.x] = threadIdx.x < a.cout ? wpk[(size_t)rows * KP + threadIdx.x] : 0.f;
     __syncthreads();
 
     // blockIdx.x -> (fragment q, chunk of 256 pixels of the padded output box)

@@ -22,20 +22,26 @@
 //     pixels (m-blocks wm*MB ..) times NB blocks of 16 output channels
 //     (n-blocks wn*NB ..), so waves in a row share pixels and waves in a
 //     column share weights.  Products use v_mfma_f32_16x16x4_f32 (float32) or
-//     v_mfma_f32_16x16x32_bf16 (bfloat16 operands, float32 accumulate).
+//     v_mfma_f32_16x16x32_bf16 (bfloat16 operands, float32 accumulate), with
+//     the weights as the row operand and the pixels as the column operand, so
+//     the 16 x 16 result of a (channel block, pixel block) pair leaves row
+//     4g + e (a channel) of column lm (a pixel) in lane lm + 16g, element e.
 //   - A lane (lm = lane % 16, g = lane / 16) feeds pixel lm of each m-block and
 //     16 bytes of consecutive K values starting at g * (KSTEP / 4); float32
 //     uses element e of that vector in the e-th of 4 products, so each product
 //     sums over K indices {4g + e}.  The weights are pre-arranged on the host
 //     so that each (K step, channel block) is one contiguous 1 KB run, read by
 //     a wave in one coalesced load; the next step's weights and pixels are
-//     loaded while the current step's products run.
+//     loaded while the current step's products run.  Which channel a block
+//     row computes is fixed by the host's packing (api.hip: chan_of).
 //   - Vector path (c_in a multiple of KSTEP): K is walked tap by tap, KSTEP
 //     channels at a time, and a lane's A operand is one 16-byte LDS read.
 //     Gather path (small c_in, e.g. the first layer): K = (tap, channel)
 //     flattened and padded to KSTEP, gathered through an LDS offset table.
-//   - Epilogue: bias and tanh in float32; stores (bf16: round to nearest even)
-//     only inside the fragment's true size.
+//   - Epilogue: bias and tanh in float32, then each lane stores its four
+//     (bf16 with paired channel blocks: eight) consecutive channels of a
+//     pixel straight from its registers (bf16: round to nearest even), only
+//     inside the fragment's true size.
 #pragma once
 
 #include "fs_internal.h"
@@ -79,68 +85,60 @@ struct Elem<true> {
 };
 
 // Fused last layer.  The tile's activations act(acc + bias) never leave the
-// registers: every lane multiplies its values (pixels 4g + e of each m-block,
-// channel lm of each n-block) by the last layer's weights and the 16 lanes of
-// a row (same pixels, 16 channels) are summed with xor shuffles
-// (fused_head_partials); the waves that split the channels add up through LDS
-// and one thread per pixel applies the last activation (softmax: exp(z - max
-// z) / sum) and writes the pixel's classes to the dense map at the window
-// corner the pixel stands for: final fragment (fy, fx) position (y, x) holds
-// window (base[fy] + S*y, base[fx] + S*x) (fused_head_finish).  A workgroup
-// barrier separates the two.
+// registers: every lane multiplies its values (rows 4g .. 4g + 3 of each
+// channel block, for pixel lm of each m-block) by the last layer's weights
+// (stored over the same (block, row) order), the four lanes of a pixel add up
+// with xor shuffles (fused_head_partials); the waves that split the channels
+// add up through LDS and one thread per pixel applies the last activation
+// (softmax: exp(z - max z) / sum) and writes the pixel's classes to the dense
+// map at the window corner the pixel stands for: final fragment (fy, fx)
+// position (y, x) holds window (base[fy] + S*y, base[fx] + S*x)
+// (fused_head_finish).  A workgroup barrier separates the two.
 template <int MB, int NB, int WN>
 __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm,
                                                     int wn, int lm, int g, float *red)
 {
     constexpr int NC = kMaxFusedClasses;
-    const int ncls = a.head_ncls;
-    float part[MB][4][NC];
+    const int ldw = a.nbt * 16;
+    float part[MB][NC];
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-#pragma unroll
-            for (int c = 0; c < NC; ++c) part[i][e][c] = 0.f;
+        for (int c = 0; c < NC; ++c) part[i][c] = 0.f;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-        const int co = (nb0 + j) * 16 + lm;
-        if (co >= a.cout) continue;
-        const float bv = a.bias[co];
-        float w2[NC];
+        const int r0 = (nb0 + j) * 16 + 4 * g;  // (block, row) index of element 0
+        const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
+        // (rows past head_ncls are zero on the device: unconditional loads)
+        f4 w2[NC];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) w2[c] = c < ncls ? a.head_w[c * a.cout + co] : 0.f;
+        for (int c = 0; c < NC; ++c) w2[c] = *reinterpret_cast<const f4 *>(a.head_w + (size_t)c * ldw + r0);
 #pragma unroll
         for (int i = 0; i < MB; ++i)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                float v = acc[i][j][e] + bv;
+                float v = acc[i][j][e] + bv[e];
                 if (a.act == ACT_TANH) v = tanh_fast(v);
 #pragma unroll
-                for (int c = 0; c < NC; ++c) part[i][e][c] = fmaf(w2[c], v, part[i][e][c]);
+                for (int c = 0; c < NC; ++c) part[i][c] = fmaf(w2[c][e], v, part[i][c]);
             }
     }
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
+        for (int c = 0; c < NC; ++c) {
+            float t = part[i][c];
+            t += __shfl_xor(t, 16);
+            t += __shfl_xor(t, 32);
+            part[i][c] = t;
+        }
+    if (g == 0) {
 #pragma unroll
-            for (int c = 0; c < NC; ++c) {
-                float t = part[i][e][c];
-                t += __shfl_xor(t, 8);
-                t += __shfl_xor(t, 4);
-                t += __shfl_xor(t, 2);
-                t += __shfl_xor(t, 1);
-                part[i][e][c] = t;
-            }
-    if (lm == 0) {
+        for (int i = 0; i < MB; ++i) {
+            const int m = (wm * MB + i) * 16 + lm;
 #pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int m = (wm * MB + i) * 16 + 4 * g + e;
-#pragma unroll
-                for (int c = 0; c < NC; ++c) red[((size_t)wn * a.mt + m) * NC + c] = part[i][e][c];
-            }
+            for (int c = 0; c < NC; ++c) red[((size_t)wn * a.mt + m) * NC + c] = part[i][c];
+        }
     }
 }
 
@@ -331,7 +329,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
                 for (int j = 0; j < NB; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                        __builtin_bit_cast(bf8, av[i]), __builtin_bit_cast(bf8, bv[j]), acc[i][j], 0, 0, 0);
+                        __builtin_bit_cast(bf8, bv[j]), __builtin_bit_cast(bf8, av[i]), acc[i][j], 0, 0, 0);
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -340,7 +338,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
                     for (int j = 0; j < NB; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
-                            __uint_as_float(av[i][e]), __uint_as_float(bv[j][e]), acc[i][j], 0, 0, 0);
+                            __uint_as_float(bv[j][e]), __uint_as_float(av[i][e]), acc[i][j], 0, 0, 0);
         }
     };
 
@@ -477,54 +475,157 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         fused_head_finish<WN>(a, q, fy, fx, l0, lend, twb, c0, red);
         return;
     }
-    // Outputs go back through LDS: each lane drops its act(acc + bias) values
-    // into a [pixel][channel] tile, then all threads copy the tile out with
-    // 16-byte stores; the pixels of a band row are contiguous in memory, so a
-    // tile row leaves as one contiguous run.
-    constexpr int NW = WN * NB * 16;              // channels this workgroup owns
-    constexpr int TPAD = 16 / (int)sizeof(TC);    // 16 bytes of row padding
-    constexpr int TS = NW + TPAD;
-    const int nbase = blockIdx.y * NW;
-    TC *tile = reinterpret_cast<TC *>(smem);
-    __syncthreads();  // every wave is done with the window / partial sums
-    if (wk == 0) {
+    // Lane (lm, g) holds, for pixel lm of each m-block, rows 4g .. 4g + 3 of
+    // each channel block: four consecutive channels (float32: 16 bytes) or,
+    // with paired blocks in bf16, eight (16 bytes); other bf16 tiles hold 8
+    // bytes per block.  Channels past c_out (padding blocks) and pixels past
+    // the tile are not written.
+    const bool act_tanh = a.act == ACT_TANH;
+    auto act = [&](float v) { return act_tanh ? tanh_fast(v) : v; };
+    constexpr bool PAIRED = BF && (NB % 2) == 0;
+    constexpr int RUN = PAIRED ? 8 : 4;  // consecutive channels per lane and block (pair)
+    f4 bv[NB];
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        const int col = (wn * NB + j) * 16 + lm;
-        const float bv = a.bias[nbase + col];  // zero padded past cout
+    for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
+
+    if (!a.direct_store) {
+        // Wide pixels: the runs go to an LDS [pixel][channel] tile (one 8- or
+        // 16-byte write each), then all threads copy the tile out in 16-byte
+        // pieces; the pixels of a band row are contiguous in memory, so a tile
+        // row leaves as one contiguous run.
+        constexpr int NW = WN * NB * 16;            // channels this workgroup owns
+        constexpr int TPAD = 16 / (int)sizeof(TC);  // 16 bytes of row padding
+        constexpr int TS = NW + TPAD;
+        const int nbase = blockIdx.y * NW;
+        TC *tile = reinterpret_cast<TC *>(smem);
+        __syncthreads();  // every wave is done with the window / partial sums
+        if (wk == 0) {
 #pragma unroll
-        for (int i = 0; i < MB; ++i)
+            for (int i = 0; i < MB; ++i) {
+                TC *row = tile + ((wm * MB + i) * 16 + lm) * TS;
+                if constexpr (PAIRED) {
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float v = acc[i][j][e] + bv;
-                if (a.act == ACT_TANH) v = tanh_fast(v);
-                const int m = (wm * MB + i) * 16 + 4 * g + e;
-                if constexpr (BF)
-                    tile[m * TS + col] = f2bf(v);
-                else
-                    tile[m * TS + col] = v;
+                    for (int p = 0; p < NB / 2; ++p) {
+                        // channels 8g .. 8g + 3 from block 2p, 8g + 4 .. 8g + 7 from 2p + 1
+                        uint16_t h[8];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            h[e] = f2bf(act(acc[i][2 * p][e] + bv[2 * p][e]));
+                            h[4 + e] = f2bf(act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]));
+                        }
+                        u4 pk;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)h[2 * e] | ((uint32_t)h[2 * e + 1] << 16);
+                        *reinterpret_cast<u4 *>(row + (wn * NB + 2 * p) * 16 + 8 * g) = pk;
+                    }
+                } else {
+#pragma unroll
+                    for (int j = 0; j < NB; ++j) {
+                        TC *dst = row + (wn * NB + j) * 16 + 4 * g;
+                        if constexpr (BF) {
+                            uint2 pk;
+                            pk.x = (uint32_t)f2bf(act(acc[i][j][0] + bv[j][0])) |
+                                   ((uint32_t)f2bf(act(acc[i][j][1] + bv[j][1])) << 16);
+                            pk.y = (uint32_t)f2bf(act(acc[i][j][2] + bv[j][2])) |
+                                   ((uint32_t)f2bf(act(acc[i][j][3] + bv[j][3])) << 16);
+                            *reinterpret_cast<uint2 *>(dst) = pk;
+                        } else {
+                            *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]),
+                                                              act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3])};
+                        }
+                    }
+                }
             }
-    }
-    }
-    __syncthreads();
-    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
-    const int nch = min(NW, a.cout - nbase);
-    const int npx = lend - l0;
-    if ((a.cout % TPAD) == 0 && (nch % TPAD) == 0) {
-        const int nv = nch / TPAD;
-        for (int idx = threadIdx.x; idx < npx * nv; idx += 256) {
-            const int m = idx / nv, v = idx - (idx / nv) * nv;
-            const int l = l0 + m;
-            const int y = l / twb, x = c0 + (l - (l / twb) * twb);
-            *reinterpret_cast<u4 *>(outp + ((size_t)y * a.out_w + x) * a.cout + v * TPAD) =
-                *reinterpret_cast<const u4 *>(tile + m * TS + v * TPAD);
         }
-    } else {
-        for (int idx = threadIdx.x; idx < npx * nch; idx += 256) {
-            const int m = idx / nch, c = idx - (idx / nch) * nch;
-            const int l = l0 + m;
-            const int y = l / twb, x = c0 + (l - (l / twb) * twb);
-            outp[((size_t)y * a.out_w + x) * a.cout + c] = tile[m * TS + c];
+        __syncthreads();
+        TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
+        const int nch = min(NW, a.cout - nbase);
+        const int npx = lend - l0;
+        if ((a.cout % TPAD) == 0 && (nch % TPAD) == 0) {
+            const int nv = nch / TPAD;
+            for (int idx = threadIdx.x; idx < npx * nv; idx += 256) {
+                const int m = idx / nv, v = idx - (idx / nv) * nv;
+                const int l = l0 + m;
+                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+                *reinterpret_cast<u4 *>(outp + ((size_t)y * a.out_w + x) * a.cout + v * TPAD) =
+                    *reinterpret_cast<const u4 *>(tile + m * TS + v * TPAD);
+            }
+        } else {
+            for (int idx = threadIdx.x; idx < npx * nch; idx += 256) {
+                const int m = idx / nch, c = idx - (idx / nch) * nch;
+                const int l = l0 + m;
+                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+                outp[((size_t)y * a.out_w + x) * a.cout + c] = tile[m * TS + c];
+            }
+        }
+        return;
+    }
+
+    // Narrow pixels: every store instruction of a wave covers whole pixels
+    // (16 consecutive pixels of a band row), so the runs go straight out.
+    if (wk != 0) return;
+    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
+    const bool full = (a.cout % RUN) == 0;
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+        const int l = l0 + (wm * MB + i) * 16 + lm;
+        if (l >= lend) continue;
+        const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+        TC *px = outp + ((size_t)y * a.out_w + x) * a.cout;
+        if constexpr (PAIRED) {
+#pragma unroll
+            for (int p = 0; p < NB / 2; ++p) {
+                const int ch = (nb0 + 2 * p) * 16 + 8 * g;
+                if (ch >= a.cout) continue;
+                uint16_t h[8];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    h[e] = f2bf(act(acc[i][2 * p][e] + bv[2 * p][e]));
+                    h[4 + e] = f2bf(act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]));
+                }
+                if (full) {
+                    u4 pk;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)h[2 * e] | ((uint32_t)h[2 * e + 1] << 16);
+                    *reinterpret_cast<u4 *>(px + ch) = pk;
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        if (ch + e < a.cout) px[ch + e] = h[e];
+                }
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const int ch = (nb0 + j) * 16 + 4 * g;
+                if (ch >= a.cout) continue;
+                float v[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j][e]);
+                if constexpr (BF) {
+                    uint16_t h[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) h[e] = f2bf(v[e]);
+                    if (full) {
+                        uint2 pk;
+                        pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
+                        pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
+                        *reinterpret_cast<uint2 *>(px + ch) = pk;
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (ch + e < a.cout) px[ch + e] = h[e];
+                    }
+                } else {
+                    if (full) {
+                        *reinterpret_cast<f4 *>(px + ch) = f4{v[0], v[1], v[2], v[3]};
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (ch + e < a.cout) px[ch + e] = v[e];
+                    }
+                }
+            }
         }
     }
 }
@@ -536,7 +637,10 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
     if (a.lds_bytes > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
-        if (e != hipSuccess) return e;
+        if (e != hipSuccess) {
+            (void)hipGetLastError();  // do not leave it to be reported by a later launch
+            return e;
+        }
     }
     hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(256), a.lds_bytes, s, a);
     return hipGetLastError();

@@ -22,6 +22,7 @@ namespace fs {
 constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of pool sizes)
 constexpr int kMaxHeadClasses = 16;
 constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
+constexpr size_t kMaxLdsBytes = 160 * 1024;  // LDS of one CDNA4 compute unit
 constexpr int kMaxFusedClasses = 4;   // classes of a last layer fused into a conv epilogue
 
 enum ActKind { ACT_NONE = 0, ACT_TANH = 1, ACT_SOFTMAX = 2 };
@@ -39,7 +40,7 @@ struct ConvArgs {
     const void *in;       // [nfrag][in_h][in_w][in_c] (float or bf16; first layer: the image)
     void *out;            // [nfrag][out_h][out_w][cout]
     const void *w;        // packed weights (api.hip: pack_conv_weights)
-    const float *bias;    // [nbt * 16], zero padded
+    const float *bias;    // [nbt * 16] in (block, row) order, zero padded
     int nfrag;            // B * F
     int F, Q;             // fragments per image, per axis
     int in_h, in_w, in_c; // padded input dims; in_c = channel pitch of the input
@@ -53,13 +54,15 @@ struct ConvArgs {
     int mt;               // output pixels per tile (16 * MB * 4 / (WN * WK))
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
-    int win_bytes;        // one window buffer (persistent kernel: two of them)
+    int direct_store;     // 1: lanes store their channel runs straight to memory
+                          // (a pixel's channels fit in 64 bytes); 0: restaged
+                          // through LDS and written as whole rows
     AxisTable ext;        // true sizes of the input fragments
     // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
     // activation, and the reassembly are applied in the epilogue, which then
     // writes the dense output map instead of `out`'s fragment batch.
     int head_ncls, head_act;
-    const float *head_w;  // [head_ncls][cout]
+    const float *head_w;  // [max(head_ncls, kMaxFusedClasses)][nbt * 16], columns in (block, row) order, zero rows past head_ncls
     const float *head_b;  // [head_ncls]
     float *head_out;      // [B][ny][nx][head_ncls]
     int ny, nx, S;
@@ -98,20 +101,15 @@ struct HeadArgs {
 // 4 / (wn * wk) across the pixels.
 hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
-// Persistent wave-specialised variant (vector path; 512 threads).
-hipError_t launch_conv_ws(const ConvArgs &a, int dtype, int mb, int nb, int wn, int grid_x, int grid_y,
-                          hipStream_t s);
-bool conv_ws_supported(int mb, int nb, int wn);
-// Workgroups of the persistent kernel that fit on one CU (0: unknown / none).
-int conv_ws_occupancy(int dtype, int mb, int nb, int wn, int lds_bytes);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);
 // Direct (vector-ALU) convolution for tiny K = c_in * k * k (<= 64) and
-// c_out <= 64; wpk = weights as [c_out][KP] float32, K index
-// (dy * k + dx) * c_in + ci, zero padded to KP = conv_direct_kp(c_in, k)
-// (bf16 nets: values rounded to bf16).  One thread per pixel.
+// c_out <= 48; wpk = weights as [rows][KP] float32 with rows = c_out rounded
+// up to 8 (zero rows past c_out), K index (dy * k + dx) * c_in + ci, zero
+// padded to KP = conv_direct_kp(c_in, k) (bf16 nets: values rounded to bf16),
+// followed by the c_out biases in channel order.  One thread per pixel.
 bool conv_direct_supported(int cin, int k, int cout);
 int conv_direct_kp(int cin, int k);
 hipError_t launch_conv_direct(const ConvArgs &a, const float *wpk, int dtype, bool in_f32, int grid, hipStream_t s);
@@ -119,7 +117,6 @@ std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int k);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec);
-std::string conv_ws_kernel_name(int dtype, int mb, int nb, int wn);
 const char *pool_kernel_name(int dtype, bool in_f32);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
