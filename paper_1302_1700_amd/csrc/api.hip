@@ -273,8 +273,10 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force, nullptr, &lds_min);
     // pixel blocks per wave: four when a wave owns at most four channel
     // blocks (more products per operand load; measured faster on every such
-    // layer), else two; then the neighbours
-    const int mb_pref = (l.vec && l.nb <= 4) ? 4 : 2;
+    // layer) or the K walk is long (N4's 3x3x48 -> 200 layer); else two, so
+    // that three waves per SIMD overlap the epilogues of short-K layers;
+    // then the neighbours
+    const int mb_pref = (l.vec && (l.nb <= 4 || l.ksteps >= 16)) ? 4 : 2;
     const int mbs[4] = {mb_pref, mb_pref == 4 ? 2 : 4, 1, 8};
     for (int mi = 0; mi < 4; ++mi) {
         const int mb = mb_force ? mb_force : mbs[mi];

@@ -310,6 +310,24 @@ def test_split_k_tiles(fsb, monkeypatch, tile):
     assert np.abs(got - ref).max() <= TOL["f32"]
 
 
+@pytest.mark.parametrize("store", ["direct", "lds"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_store_modes(fsb, monkeypatch, store, dt):
+    """Both epilogue store paths on every layer: channel counts that pair
+    bf16 blocks (32, 64), leave them unpaired (40), and are not multiples of
+    8 or 4 (18), on the vector and the gather path, several tiles and ragged
+    fragment sizes."""
+    layers = [wl.conv(3, 3, 32), wl.conv(2, 32, 64), wl.pool(2, 64), wl.conv(2, 64, 40),
+              wl.conv(1, 40, 18), wl.pool(2, 18), wl.fc(2, 18, 24), wl.fc(1, 24, 3, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 11, 0.2)
+    img = wl.make_image(12, 2, w0 + 41, w0 + 29, 3)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    monkeypatch.setenv("FRAGSCAN_STORE", store)
+    got = _scan(fsb, layers, params, img, 3, dtype=dt)
+    assert np.abs(got - ref).max() <= TOL[dt]
+
+
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
 def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     """Small-K layers take either the per-pixel vector-ALU kernel or the
