@@ -7,8 +7,9 @@ workload's synthetic image batch, already resident in device memory.  Prints
 one JSON line:
   value        output pixels per second (windows classified per second)
   roofline     the launch that takes the most time, its algorithmic work per
-               launch over its mean duration (HIP events around each launch on
-               the scan's stream), against the MI355X peak for its bound
+               launch over its mean duration (HIP events around repeated
+               back-to-back runs of that launch on the scan's stream), against
+               the MI355X peak for its bound
   launches     the same for every launch of the scan
   cpu_baseline the per-patch CPU oracle on a bounded sample of windows, on
                this host's cores
@@ -132,7 +133,8 @@ def main():
     ms = t0.elapsed_time(t1) / args.steps
     pixels = w.batch * w.out_h * w.out_w
 
-    # per-launch times, HIP events around every launch on the same stream
+    # per-launch mean durations: HIP events around --profile-reps back-to-back
+    # runs of each launch on the scan's stream
     per = net.profile(x, reps=args.profile_reps, out=out)
     peak_mm = PEAK["bf16_tflops"] if w.dtype == "bf16" else PEAK["f32_tflops"]
     rows = []

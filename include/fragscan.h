@@ -175,10 +175,12 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W,
 fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
                   float *d_out, void *d_workspace, size_t workspace_bytes, void *stream);
 
-/* fs_scan, repeated `reps` times, with a HIP event recorded before and after
- * every launch; synchronises the stream and writes, per launch, the mean of
- * its event-to-event times over the repetitions in milliseconds into
- * h_launch_ms[0 .. min(capacity, n_launches)).  For measurement only. */
+/* fs_scan with every launch repeated `reps` times back to back between two
+ * HIP events on `stream` (a repetition recomputes the same values, so d_out
+ * ends as after fs_scan); synchronises the stream and writes, per launch,
+ * the events' elapsed time / reps in milliseconds (the launch's mean
+ * duration) into h_launch_ms[0 .. min(capacity, n_launches)).  For
+ * measurement only. */
 fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, int32_t H,
                           int32_t W, float *d_out, void *d_workspace, size_t workspace_bytes,
                           void *stream, int32_t reps, float *h_launch_ms, int32_t capacity);

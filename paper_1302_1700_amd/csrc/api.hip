@@ -967,34 +967,32 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
     if (st != FS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int n = (int)P.launches.size();
-    std::vector<hipEvent_t> ev((size_t)(n + 1) * reps, nullptr);
+    // Launch i runs `reps` times back to back between two events.  Every
+    // launch reads one buffer and writes another (or the output), so a
+    // repetition recomputes the same values and the launches that follow see
+    // exactly what a plain scan leaves them.
+    std::vector<hipEvent_t> ev((size_t)n * 2, nullptr);
     hipError_t e = hipSuccess;
     for (auto &x : ev) {
         e = hipEventCreate(&x);
         if (e != hipSuccess) break;
     }
-    for (int r = 0; r < reps && e == hipSuccess; ++r) {
-        hipEvent_t *E = &ev[(size_t)r * (n + 1)];
-        e = hipEventRecord(E[0], s);
-        for (int i = 0; i < n && e == hipSuccess; ++i) {
-            e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
-            if (e == hipSuccess) e = hipEventRecord(E[i + 1], s);
-        }
+    for (int i = 0; i < n && e == hipSuccess; ++i) {
+        e = hipEventRecord(ev[2 * i], s);
+        for (int r = 0; r < reps && e == hipSuccess; ++r) e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+        if (e == hipSuccess) e = hipEventRecord(ev[2 * i + 1], s);
     }
     if (e == hipSuccess) e = hipStreamSynchronize(s);
-    std::vector<double> acc(n, 0.0);
-    for (int r = 0; r < reps && e == hipSuccess; ++r) {
-        hipEvent_t *E = &ev[(size_t)r * (n + 1)];
-        for (int i = 0; i < n && e == hipSuccess; ++i) {
-            float ms = 0.f;
-            e = hipEventElapsedTime(&ms, E[i], E[i + 1]);
-            acc[i] += ms;
-        }
+    std::vector<double> ms_i(n, 0.0);
+    for (int i = 0; i < n && e == hipSuccess; ++i) {
+        float ms = 0.f;
+        e = hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]);
+        ms_i[i] = ms;
     }
     for (auto &x : ev)
         if (x) (void)hipEventDestroy(x);
     if (e != hipSuccess) return hip_fail(e, "profiled scan");
-    for (int i = 0; i < std::min(n, (int)capacity); ++i) h_launch_ms[i] = (float)(acc[i] / reps);
+    for (int i = 0; i < std::min(n, (int)capacity); ++i) h_launch_ms[i] = (float)(ms_i[i] / reps);
     return FS_OK;
 }
 

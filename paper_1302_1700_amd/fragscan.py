@@ -217,8 +217,9 @@ class Net:
         return out
 
     def profile(self, image, reps=10, out=None, stream=None):
-        """Per-launch mean milliseconds of `reps` scans timed with HIP events
-        around every launch (synchronises)."""
+        """Per-launch mean duration in milliseconds: each launch runs `reps`
+        times back to back between two HIP events on the stream
+        (synchronises; `out` ends as after one scan)."""
         import torch
         B, H, W, C = image.shape
         if out is None:

@@ -270,8 +270,13 @@ def test_repeat_is_deterministic(fsb):
     b = net.scan(x).clone()
     torch.cuda.synchronize()
     assert torch.equal(a, b)
-    ms = net.profile(x, reps=2)
+    # the profiled scan repeats every launch back to back; its output is the
+    # plain scan's
+    c = torch.full_like(a, float("nan"))
+    ms = net.profile(x, reps=3, out=c)
+    torch.cuda.synchronize()
     assert len(ms) == len(net.launches(1, 200, 180)) and all(m > 0 for m in ms)
+    assert torch.equal(a, c)
     net.close()
 
 
