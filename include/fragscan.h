@@ -134,7 +134,8 @@ typedef struct {
  * pool must divide the patch-level map it receives (Section 2.1.2:
  * mod(w_{l-1}, k) = 0); the patch-level map after the last layer must be
  * 1 x 1.  `patch` is w_0 (0: derive it from the stack).  A patch that does
- * not agree with the stack gives FS_ERR_SHAPE.  Weights are converted (and
+ * not agree with the stack gives FS_ERR_SHAPE; more than 16384 channels in a
+ * layer gives FS_ERR_UNSUPPORTED.  Weights are converted (and
  * for FS_BF16 rounded) and uploaded to the current HIP device, which the net
  * is then bound to.  On success *out receives the handle. */
 fs_status fs_net_create(const fs_layer *layers, int32_t n_layers, int32_t in_channels,

@@ -300,6 +300,9 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             int rmax = (mt - 1 + tmin - 1) / tmin + k;
             rmax = std::min(rmax, in.hmax);
             const size_t lds = offtab + (size_t)rmax * (band_w + k - 1) * cs * es;
+            // the kernel's index arithmetic (Div in conv_impl.h) takes pixel
+            // numbers within a band below 2^20
+            if ((long long)hout_max * band_w >= (1 << 20)) continue;
             if (lds > 96 * 1024) {
                 if (band_w <= 8) break;
                 continue;
@@ -313,11 +316,12 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             L.conv.mt = mt;
             L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
             L.conv.lds_cs = cs;
-            // Stores: straight from the registers when a pixel's channels
-            // fit in 64 bytes (each store instruction then covers whole
-            // pixels), else restaged through an LDS tile [mt][wn*nb*16 + 16
-            // bytes] (FRAGSCAN_STORE=direct / lds overrides, for tuning).
-            int direct = l.nbt * 16 * es <= 64;
+            // Stores: straight from the registers (16-byte runs of 4 f32 or
+            // 8 bf16 channels per lane; measured no slower than restaging on
+            // every conv layer of the five workloads, faster on the bf16 and
+            // 16-channel ones); FRAGSCAN_STORE=lds restages through an LDS
+            // tile [mt][wn*nb*16 + 16 bytes] and writes whole rows instead.
+            int direct = 1;
             if (const char *e = getenv("FRAGSCAN_STORE"); e && e[0]) direct = e[0] == 'd';
             const size_t otile = direct ? 0 : (size_t)mt * (l.wn * l.nb * 16 + 16 / es) * es;
             L.conv.direct_store = direct;
@@ -495,6 +499,10 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             }
         }
         o.is_image = false;
+        // kernels address within one fragment (or image) with 32-bit offsets
+        if ((long long)std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C >= (1LL << 31) ||
+            (long long)std::max(g.hmax, 1) * std::max(g.wmax, 1) * g.C >= (1LL << 31))
+            return fail(FS_ERR_UNSUPPORTED, "layer %d: a fragment holds 2^31 or more elements", li);
         if (L.dst != 2) {
             const size_t out_bytes = (size_t)B * o.Q * o.Q * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
             buf = std::max(buf, out_bytes);
@@ -675,6 +683,8 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
             return fail(FS_ERR_SHAPE, "layer %d: softmax is allowed on the last layer only", i);
         if (s.c_in != c) return fail(FS_ERR_SHAPE, "layer %d: c_in %d, the layer below gives %d", i, s.c_in, c);
         if (s.c_in < 1 || s.c_out < 1) return fail(FS_ERR_SHAPE, "layer %d: channel counts must be >= 1", i);
+        if (s.c_in > kMaxChannels || s.c_out > kMaxChannels)
+            return fail(FS_ERR_UNSUPPORTED, "layer %d: more than %d channels", i, kMaxChannels);
         if (s.kind == FS_MAXPOOL) {
             if (seen_fc) return fail(FS_ERR_SHAPE, "layer %d: pooling after a fully connected layer", i);
             if (s.k < 1) return fail(FS_ERR_SHAPE, "layer %d: pool size must be >= 1", i);

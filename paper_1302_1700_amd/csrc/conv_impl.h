@@ -55,13 +55,39 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint16_t f2bf(float f)
+typedef float f2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
+
+// float -> bfloat16, round to nearest even (one v_cvt_pk_bf16_f32 per pair)
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
 {
-    // round to nearest even; inputs here are finite
-    uint32_t u = __float_as_uint(f);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return (uint16_t)(u >> 16);
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2v{lo, hi}, bf2v));
 }
+
+// Quotient and remainder of the small non-negative integers of the tile
+// index arithmetic (n < 2^20, 1 <= d < 2^16; the planner keeps tiles within
+// that) by a divisor fixed for the tile: one multiply by a float reciprocal,
+// truncated, then one correction either way (the product's error is below
+// 1/4 for such n).  The general 32-bit division the compiler emits costs
+// ~25 instructions; this ~7, which matters in the per-element loops.
+struct Div {
+    int d;
+    float r;
+    __device__ explicit Div(int d_) : d(d_), r(__builtin_amdgcn_rcpf((float)d_)) {}
+    __device__ int quo(int n) const
+    {
+        int q = (int)((float)n * r);
+        const int t = n - __mul24(q, d);
+        return q + (t >= d) - (t < 0);
+    }
+    // n = q * d + m, 0 <= m < d
+    __device__ void qr(int n, int &q, int &m) const
+    {
+        q = quo(n);
+        m = n - __mul24(q, d);
+    }
+};
 
 // tanh(x) = 1 - 2 / (exp(2x) + 1), with the hardware exp2 and reciprocal:
 // absolute error a few 1e-7, saturates cleanly to +-1 for large |x|.
@@ -150,6 +176,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int 
     const int ncls = a.head_ncls;
     const int mt = a.mt;
     const int b = q / a.F;
+    const Div dtw(twb);
     for (int m = threadIdx.x; m < mt; m += blockDim.x) {
         const int l = l0 + m;
         if (l >= lend) break;
@@ -180,7 +207,9 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int 
 #pragma unroll
             for (int c = 0; c < NC; ++c) z[c] = tanhf(z[c]);
         }
-        const int y = l / twb, x = c0 + (l - (l / twb) * twb);
+        int y, x;
+        dtw.qr(l, y, x);
+        x += c0;
         const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
         float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * ncls;
 #pragma unroll
@@ -239,6 +268,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         // batches of 8 loads in flight per thread before their LDS stores
         const int nvec = a.cin / LPE;
         const int total = R * Cc * nvec;
+        const Div dnv(nvec), dcc(Cc);
+        const int rowp = a.in_w * a.in_c;  // elements per input row (fragments stay below 2^31)
         constexpr int UN = 8;
         for (int base = threadIdx.x; base < total; base += 256 * UN) {
             u4 val[UN];
@@ -246,14 +277,14 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
                 const int idx = base + u * 256;
-                const int v = idx % nvec;
-                const int p = idx / nvec;
-                const int c = p % Cc, r = p / Cc;
+                int p, v, r, c;
+                dnv.qr(idx, p, v);
+                dcc.qr(p, r, c);
                 const int gy = yfirst + r, gx = c0 + c;
                 val[u] = u4{0u, 0u, 0u, 0u};
                 if (idx < total && gy < hin && gx < win)
-                    val[u] = *reinterpret_cast<const u4 *>(inp + ((size_t)gy * a.in_w + gx) * a.in_c + v * LPE);
-                dsto[u] = idx < total ? (r * Cc + c) * CS + v * LPE : -1;
+                    val[u] = *reinterpret_cast<const u4 *>(inp + (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
+                dsto[u] = idx < total ? __mul24(__mul24(r, Cc) + c, CS) + v * LPE : -1;
             }
 #pragma unroll
             for (int u = 0; u < UN; ++u)
@@ -261,28 +292,33 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
     } else {
         const int total = R * Cc * a.cin;
+        const Div dci(a.cin), dcc(Cc);
+        const int rowp = a.in_w * a.in_c;
         for (int idx = threadIdx.x; idx < total; idx += 256) {
-            const int ci = idx % a.cin;
-            const int p = idx / a.cin;
-            const int c = p % Cc, r = p / Cc;
+            int p, ci, r, c;
+            dci.qr(idx, p, ci);
+            dcc.qr(p, r, c);
             const int gy = yfirst + r, gx = c0 + c;
             TC val = 0;
             if (gy < hin && gx < win) {
-                TI x = inp[((size_t)gy * a.in_w + gx) * a.in_c + ci];
+                TI x = inp[gy * rowp + __mul24(gx, a.in_c) + ci];
                 if constexpr (BF && IN_F32)
                     val = f2bf(x);
                 else
                     val = x;
             }
-            win_lds[(r * Cc + c) * CS + ci] = val;
+            win_lds[__mul24(__mul24(r, Cc) + c, CS) + ci] = val;
         }
     }
     if constexpr (!VEC) {
+        const Div dci(a.cin), dk(a.k);
         for (int kk = threadIdx.x; kk < kk_total; kk += 256) {
-            const int tap = kk / a.cin, ci = kk - (kk / a.cin) * a.cin;
+            int tap, ci;
+            dci.qr(kk, tap, ci);
             int off = -1;
             if (tap < a.k * a.k) {
-                const int dy = tap / a.k, dx = tap - (tap / a.k) * a.k;
+                int dy, dx;
+                dk.qr(tap, dy, dx);
                 off = (dy * Cc + dx) * CS + ci;
             }
             offtab[kk] = off;
@@ -301,12 +337,15 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const int lm = lane & 15, g = lane >> 4;
     const int nb0 = blockIdx.y * (WN * NB) + wn * NB;
 
+    const Div dtw(twb);
     int abase[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int l = l0 + (wm * MB + i) * 16 + lm;
         if (l < lend) {
-            const int y = l / twb - yfirst, x = l - (l / twb) * twb;
+            int y, x;
+            dtw.qr(l, y, x);
+            y -= yfirst;
             abase[i] = (y * Cc + x) * CS + g * LPE;
         } else {
             abase[i] = g * LPE;  // any in-window address; the result is not stored
@@ -344,9 +383,14 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 
     if constexpr (VEC) {
         // K step s covers tap (dy, dx) and channels cc*KSTEP ..; the three
-        // indices advance incrementally.  Weights are loaded two steps ahead
-        // (two register buffers, the loop unrolled by two) and pixels one step
-        // ahead, so the products of a step never wait on the loads it needs.
+        // indices advance incrementally.  Weights are loaded PD steps ahead
+        // (a ring of PD register buffers, the loop unrolled by PD) and pixels
+        // one step ahead, so the products of a step never wait on the loads
+        // it needs.
+        // (four-deep rings measured slower for bf16: the extra registers
+        // cost a wave per SIMD)
+        constexpr int PD = 2;
+        static_assert(PD % 2 == 0, "the pixel double buffer needs an even unroll");
         const int ncc = a.cin / KSTEP;
         const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
         const int nsteps = s_end - s_begin;
@@ -363,49 +407,55 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             dy += w2;
             return (dy * Cc + dx) * CS + cc * KSTEP;
         };
-        u4 b0[NB], b1[NB], a0[MB], a1[MB];
+        u4 b[PD][NB], av[2][MB];
         const u4 *wpk = wp + (size_t)s_begin * wstep;
         const int off0 = (dy * Cc + dx) * CS + cc * KSTEP;
-#pragma unroll
-        for (int j = 0; j < NB; ++j) b0[j] = wpk[j * 64];
+        const int last = nsteps - 1;
         // unconditional (clamped) so every path reaches the loop with the same
         // loads in flight
 #pragma unroll
-        for (int j = 0; j < NB; ++j) b1[j] = wpk[(nsteps > 1 ? wstep : 0) + j * 64];
+        for (int t = 0; t < PD; ++t)
 #pragma unroll
-        for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
-        // The prefetches are issued on every iteration (past the end they
-        // re-read the last step's weights and the window's first pixel), so
-        // every path through the loop has the same loads in flight and the
-        // waits before the products only cover the operands they use.
-        const int last = nsteps - 1;
+            for (int j = 0; j < NB; ++j) b[t][j] = wpk[(size_t)min(t, last) * wstep + j * 64];
+#pragma unroll
+        for (int i = 0; i < MB; ++i) av[0][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
+        // The prefetches are issued on every step (past the end they re-read
+        // the last step's weights and the window's first pixel), so every
+        // path through the loop has the same loads in flight and the waits
+        // before the products only cover the operands they use.
         int off = off0;
         int s = 0;
-        for (; s + 1 < nsteps; s += 2) {
-            // scheduling barriers keep each prefetch ahead of the products
-            // that do not need it (left alone, the compiler sinks the loads
-            // below them to share registers, exposing their latency)
-            off = advance(off);  // step s + 1
+        for (; s + PD <= nsteps; s += PD) {
 #pragma unroll
-            for (int i = 0; i < MB; ++i) a1[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a0, b0);
-            __builtin_amdgcn_sched_barrier(0);
-            const size_t w2 = (size_t)min(s + 2, last) * wstep;
+            for (int t = 0; t < PD; ++t) {
+                // scheduling barriers keep each prefetch ahead of the products
+                // that do not need it (left alone, the compiler sinks the
+                // loads below them to share registers, exposing their latency)
+                off = advance(off);  // step s + t + 1
+                const int offa = s + t + 1 < nsteps ? off : off0;
 #pragma unroll
-            for (int j = 0; j < NB; ++j) b0[j] = wpk[w2 + j * 64];
-            off = advance(off);  // step s + 2
-            const int offa = s + 2 < nsteps ? off : off0;
+                for (int i = 0; i < MB; ++i)
+                    av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
+                __builtin_amdgcn_sched_barrier(0);
+                mma(av[t & 1], b[t]);
+                __builtin_amdgcn_sched_barrier(0);
+                const size_t wn2 = (size_t)min(s + t + PD, last) * wstep;
 #pragma unroll
-            for (int i = 0; i < MB; ++i) a0[i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
-            __builtin_amdgcn_sched_barrier(0);
-            mma(a1, b1);
-            __builtin_amdgcn_sched_barrier(0);
-            const size_t w3 = (size_t)min(s + 3, last) * wstep;
-#pragma unroll
-            for (int j = 0; j < NB; ++j) b1[j] = wpk[w3 + j * 64];
+                for (int j = 0; j < NB; ++j) b[t][j] = wpk[wn2 + j * 64];
+            }
         }
-        if (s < nsteps) mma(a0, b0);
+        // the last nsteps % PD steps (their weights are already loaded)
+#pragma unroll
+        for (int t = 0; t + 1 < PD; ++t) {
+            if (s + t < nsteps) {
+                off = advance(off);
+                const int offa = s + t + 1 < nsteps ? off : off0;
+#pragma unroll
+                for (int i = 0; i < MB; ++i)
+                    av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
+                mma(av[t & 1], b[t]);
+            }
+        }
     } else {
         const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
         u4 bcur[NB], bnxt[NB];
@@ -489,7 +539,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
 
     if (!a.direct_store) {
-        // Wide pixels: the runs go to an LDS [pixel][channel] tile (one 8- or
+        // Restaged: the runs go to an LDS [pixel][channel] tile (one 8- or
         // 16-byte write each), then all threads copy the tile out in 16-byte
         // pieces; the pixels of a band row are contiguous in memory, so a tile
         // row leaves as one contiguous run.
@@ -507,15 +557,15 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
                     for (int p = 0; p < NB / 2; ++p) {
                         // channels 8g .. 8g + 3 from block 2p, 8g + 4 .. 8g + 7 from 2p + 1
-                        uint16_t h[8];
+                        float h[8];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            h[e] = f2bf(act(acc[i][2 * p][e] + bv[2 * p][e]));
-                            h[4 + e] = f2bf(act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]));
+                            h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
+                            h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
                         }
                         u4 pk;
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)h[2 * e] | ((uint32_t)h[2 * e + 1] << 16);
+                        for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(h[2 * e], h[2 * e + 1]);
                         *reinterpret_cast<u4 *>(row + (wn * NB + 2 * p) * 16 + 8 * g) = pk;
                     }
                 } else {
@@ -524,10 +574,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                         TC *dst = row + (wn * NB + j) * 16 + 4 * g;
                         if constexpr (BF) {
                             uint2 pk;
-                            pk.x = (uint32_t)f2bf(act(acc[i][j][0] + bv[j][0])) |
-                                   ((uint32_t)f2bf(act(acc[i][j][1] + bv[j][1])) << 16);
-                            pk.y = (uint32_t)f2bf(act(acc[i][j][2] + bv[j][2])) |
-                                   ((uint32_t)f2bf(act(acc[i][j][3] + bv[j][3])) << 16);
+                            pk.x = pack_bf16(act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]));
+                            pk.y = pack_bf16(act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3]));
                             *reinterpret_cast<uint2 *>(dst) = pk;
                         } else {
                             *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]),
@@ -539,59 +587,66 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
         __syncthreads();
         TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
+        const int orow = a.out_w * a.cout;
         const int nch = min(NW, a.cout - nbase);
         const int npx = lend - l0;
         if ((a.cout % TPAD) == 0 && (nch % TPAD) == 0) {
             const int nv = nch / TPAD;
+            const Div dnv(nv);
             for (int idx = threadIdx.x; idx < npx * nv; idx += 256) {
-                const int m = idx / nv, v = idx - (idx / nv) * nv;
-                const int l = l0 + m;
-                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
-                *reinterpret_cast<u4 *>(outp + ((size_t)y * a.out_w + x) * a.cout + v * TPAD) =
-                    *reinterpret_cast<const u4 *>(tile + m * TS + v * TPAD);
+                int m, v, y, x;
+                dnv.qr(idx, m, v);
+                dtw.qr(l0 + m, y, x);
+                x += c0;
+                *reinterpret_cast<u4 *>(outp + (y * orow + __mul24(x, a.cout) + v * TPAD)) =
+                    *reinterpret_cast<const u4 *>(tile + __mul24(m, TS) + v * TPAD);
             }
         } else {
+            const Div dnc(nch);
             for (int idx = threadIdx.x; idx < npx * nch; idx += 256) {
-                const int m = idx / nch, c = idx - (idx / nch) * nch;
-                const int l = l0 + m;
-                const int y = l / twb, x = c0 + (l - (l / twb) * twb);
-                outp[((size_t)y * a.out_w + x) * a.cout + c] = tile[m * TS + c];
+                int m, c, y, x;
+                dnc.qr(idx, m, c);
+                dtw.qr(l0 + m, y, x);
+                x += c0;
+                outp[y * orow + __mul24(x, a.cout) + c] = tile[__mul24(m, TS) + c];
             }
         }
         return;
     }
 
-    // Narrow pixels: every store instruction of a wave covers whole pixels
-    // (16 consecutive pixels of a band row), so the runs go straight out.
+    // Direct: every lane writes its runs straight from registers.
     if (wk != 0) return;
     TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
+    const int orow = a.out_w * a.cout;
     const bool full = (a.cout % RUN) == 0;
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int l = l0 + (wm * MB + i) * 16 + lm;
         if (l >= lend) continue;
-        const int y = l / twb, x = c0 + (l - (l / twb) * twb);
-        TC *px = outp + ((size_t)y * a.out_w + x) * a.cout;
+        int y, x;
+        dtw.qr(l, y, x);
+        x += c0;
+        TC *px = outp + (y * orow + __mul24(x, a.cout));
         if constexpr (PAIRED) {
 #pragma unroll
             for (int p = 0; p < NB / 2; ++p) {
                 const int ch = (nb0 + 2 * p) * 16 + 8 * g;
                 if (ch >= a.cout) continue;
-                uint16_t h[8];
+                float h[8];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    h[e] = f2bf(act(acc[i][2 * p][e] + bv[2 * p][e]));
-                    h[4 + e] = f2bf(act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]));
+                    h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
+                    h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
                 }
-                if (full) {
-                    u4 pk;
+                u4 pk;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) pk[e] = (uint32_t)h[2 * e] | ((uint32_t)h[2 * e + 1] << 16);
+                for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(h[2 * e], h[2 * e + 1]);
+                if (full) {
                     *reinterpret_cast<u4 *>(px + ch) = pk;
                 } else {
 #pragma unroll
                     for (int e = 0; e < 8; ++e)
-                        if (ch + e < a.cout) px[ch + e] = h[e];
+                        if (ch + e < a.cout) px[ch + e] = (uint16_t)(pk[e / 2] >> (16 * (e % 2)));
                 }
             }
         } else {
@@ -603,18 +658,15 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j][e]);
                 if constexpr (BF) {
-                    uint16_t h[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) h[e] = f2bf(v[e]);
+                    uint2 pk;
+                    pk.x = pack_bf16(v[0], v[1]);
+                    pk.y = pack_bf16(v[2], v[3]);
                     if (full) {
-                        uint2 pk;
-                        pk.x = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
-                        pk.y = (uint32_t)h[2] | ((uint32_t)h[3] << 16);
                         *reinterpret_cast<uint2 *>(px + ch) = pk;
                     } else {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            if (ch + e < a.cout) px[ch + e] = h[e];
+                            if (ch + e < a.cout) px[ch + e] = (uint16_t)((e < 2 ? pk.x : pk.y) >> (16 * (e % 2)));
                     }
                 } else {
                     if (full) {

@@ -23,6 +23,7 @@ constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of poo
 constexpr int kMaxHeadClasses = 16;
 constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
 constexpr size_t kMaxLdsBytes = 160 * 1024;  // LDS of one CDNA4 compute unit
+constexpr int kMaxChannels = 16384;           // per layer (kernels divide by channel counts below 2^16)
 constexpr int kMaxFusedClasses = 4;   // classes of a last layer fused into a conv epilogue
 
 enum ActKind { ACT_NONE = 0, ACT_TANH = 1, ACT_SOFTMAX = 2 };
@@ -54,9 +55,8 @@ struct ConvArgs {
     int mt;               // output pixels per tile (16 * MB * 4 / (WN * WK))
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
-    int direct_store;     // 1: lanes store their channel runs straight to memory
-                          // (a pixel's channels fit in 64 bytes); 0: restaged
-                          // through LDS and written as whole rows
+    int direct_store;     // 1: lanes store their channel runs straight to memory;
+                          // 0: restaged through LDS and written as whole rows
     AxisTable ext;        // true sizes of the input fragments
     // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
     // activation, and the reassembly are applied in the epilogue, which then
