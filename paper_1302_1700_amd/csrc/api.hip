@@ -812,6 +812,10 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         const int grp = l.nb * l.wn;
         l.nbt = (nbt0 + grp - 1) / grp * grp;
         l.ksteps = l.vec ? l.k * l.k * (l.cin / KSTEP) : (l.k * l.k * l.cin + KSTEP - 1) / KSTEP;
+        if (l.ksteps < l.wk) {  // every K-splitting wave needs at least one step
+            delete net;
+            return fail(FS_ERR_UNSUPPORTED, "layer %d: %d K steps cannot be split over %d waves", i, l.ksteps, l.wk);
+        }
         std::vector<uint8_t> pw;
         pack_conv_weights(l, s.weight, dtype, pw);
         l.w_off = push(pw.data(), pw.size());

@@ -142,6 +142,16 @@ def test_rejects_bad_nets():
     assert _status([wl.conv(2, 1, 2, "none"), wl.fc(1, 2, 2)]) == fsb.FS_OK
 
 
+def test_split_k_needs_a_step_per_wave(monkeypatch):
+    # a 1x1 16 -> 16 layer has one K step; forcing two K-splitting waves on
+    # it (tuning override) is refused instead of leaving a wave without work
+    layers = [wl.conv(1, 16, 16), wl.fc(1, 16, 2, "softmax")]
+    monkeypatch.setenv("FRAGSCAN_TILE", "0:0,0,0,0,2")
+    assert _status(layers, c0=16) == fsb.FS_ERR_UNSUPPORTED
+    monkeypatch.delenv("FRAGSCAN_TILE")
+    assert _status(layers, c0=16) == fsb.FS_OK
+
+
 def test_image_smaller_than_patch_rejected():
     net = _plan_net(wl.WORKLOADS[1].layers)
     with pytest.raises(fsb.FsError) as e:
