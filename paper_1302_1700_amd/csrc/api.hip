@@ -338,6 +338,103 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile fits in LDS", L.layer);
 }
 
+// Children of a k x k pool (Eqs. 5-7): per axis, parent index i and offset
+// o give child i*k + o of size floor((s - o) / k).
+Geo pool_geo(const Geo &g, int k)
+{
+    Geo o;
+    o.Q = g.Q * k;
+    o.ey.assign(o.Q, 0);
+    o.ex.assign(o.Q, 0);
+    for (int i = 0; i < g.Q; ++i)
+        for (int off = 0; off < k; ++off) {
+            o.ey[i * k + off] = std::max(g.ey[i] - off, 0) / k;
+            o.ex[i * k + off] = std::max(g.ex[i] - off, 0) / k;
+        }
+    o.C = g.C;
+    o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
+    o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
+    o.is_image = false;
+    return o;
+}
+
+// Tiles of a convolution with the following k x k pool fused in (kernel:
+// conv_impl.h, pool_k > 0).  Bands of ~16 columns of the stride-1 max filter;
+// a tile holds pool_rt filter rows, i.e. (pool_rt + kp - 1) x (band + kp - 1)
+// convolution outputs, which must fit the register tile (mt pixels).
+fs_status plan_conv_pool_tiles(const fs_net *net, const NetLayer &l, const Geo &in, int kp, Launch &L)
+{
+    const int k = l.k;
+    const int es = elem_of(net->dtype);
+    const int KSTEP = kstep_of(net->dtype);
+    const int pad = 16 / es;
+    const int cs = l.vec ? l.cin + pad : l.cin;
+    const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
+    const int hM_max = in.hmax - k + 1 - kp + 1, wM_max = in.wmax - k + 1 - kp + 1;
+    const int wm = 4 / (l.wn * l.wk);
+    int mb_force = 0, band_force = 0;
+    tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
+    const int mbs[4] = {4, 8, 2, 1};
+    for (int mi = 0; mi < 4; ++mi) {
+        const int mb = mb_force ? mb_force : mbs[mi];
+        if (!conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
+            if (mb_force) break;
+            continue;
+        }
+        const int mt = 16 * mb * wm;
+        const int wmax = std::max(wM_max, 1), hmax = std::max(hM_max, 1);
+        int nbands = wmax <= 32 ? 1 : (wmax + 15) / 16;
+        if (band_force) nbands = (wmax + band_force - 1) / band_force;
+        for (; nbands <= wmax; ++nbands) {
+            const int band_w = (wmax + nbands - 1) / nbands;
+            const int ew = band_w + kp - 1;
+            const int rt = std::min(mt / ew - (kp - 1), hmax);
+            if (rt < 1) continue;  // narrower bands
+            const size_t win = offtab + (size_t)(rt + kp - 1 + k - 1) * (ew + k - 1) * cs * es;
+            const size_t tile = (size_t)mt * (l.wn * l.nb * 16 + pad) * es;
+            const size_t part = (size_t)(l.wk - 1) * (4 / l.wk) * mb * l.nb * 4 * 64 * 4;
+            const size_t need = std::max(std::max(win, tile), part);
+            if (win > 96 * 1024 || need > kMaxLdsBytes) {
+                if (band_w <= 8) break;
+                continue;
+            }
+            if ((long long)in.hmax * ew >= (1 << 20)) continue;
+            L.mb = mb;
+            L.conv.band_w = band_w;
+            L.conv.nbands = nbands;
+            L.conv.mt = mt;
+            L.conv.pool_rt = rt;
+            L.conv.tiles_per_band = (hmax + rt - 1) / rt;
+            L.conv.lds_cs = cs;
+            L.conv.direct_store = 1;
+            L.conv.lds_bytes = (int)need;
+            return FS_OK;
+        }
+        if (mb_force) break;
+    }
+    return fail(FS_ERR_UNSUPPORTED, "layer %d: no fused convolution + pool tile", L.layer);
+}
+
+// Whether the pool after conv layer li goes into the convolution's epilogue.
+// Per output pixel, fusing recomputes a halo share `ov` of the products
+// (2 c_in k^2 c_out ov FLOPs; ov ~ 0.35 for 2 x 2 pools with 16-column
+// bands, 0.5 for larger pools) and saves the pool's read and write of the
+// pixel (2 c_out elem bytes).  At peak rates that pays when
+// c_in k^2 ov < elem * (peak FLOP/s / HBM bytes/s): every layer of the five
+// workloads except N4's 48 -> 48 convolutions, whose fused form measured
+// 10-35% slower.  FRAGSCAN_POOL_FUSE=1 / 0 forces it on / off.
+bool want_pool_fusion(const fs_net *net, int li)
+{
+    const int nl = (int)net->L.size();
+    if (li + 1 >= nl) return false;
+    const NetLayer &l = net->L[li], &p = net->L[li + 1];
+    if (l.kind == FS_MAXPOOL || p.kind != FS_MAXPOOL || l.nbt != l.nb * l.wn) return false;
+    if (const char *e = getenv("FRAGSCAN_POOL_FUSE"); e && e[0]) return e[0] == '1';
+    const double ov = p.k == 2 ? 0.35 : 0.5;
+    const double ridge = net->dtype == DT_BF16 ? 2516.6e12 / 8e12 : 157.3e12 / 8e12;  // FLOP per byte
+    return (double)l.cin * l.k * l.k * ov < elem_of(net->dtype) * ridge;
+}
+
 fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
 {
     if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
@@ -384,17 +481,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
         Geo o;
         if (l.kind == 1) {  // pool
             const int k = l.k;
-            o.Q = g.Q * k;
-            o.ey.assign(o.Q, 0);
-            o.ex.assign(o.Q, 0);
-            for (int i = 0; i < g.Q; ++i)
-                for (int off = 0; off < k; ++off) {
-                    o.ey[i * k + off] = std::max(g.ey[i] - off, 0) / k;
-                    o.ex[i * k + off] = std::max(g.ex[i] - off, 0) / k;
-                }
-            o.C = g.C;
-            o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
-            o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
+            o = pool_geo(g, k);
             if (g.Q * k > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
             L.type = 1;
             PoolArgs &a = L.pool;
@@ -455,11 +542,13 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             // it for every layer it supports, =0 for none.
             const char *dv = getenv("FRAGSCAN_DIRECT");
             const bool want_direct = dv ? dv[0] == '1' : l.cout <= 16;
-            if (l.has_w32 && !fused_here && want_direct) {
+            const bool pool_fuse = !fused_here && want_pool_fusion(net, li);
+            if (l.has_w32 && !fused_here && !pool_fuse && want_direct) {
                 L.direct = true;
                 L.conv.lds_bytes = 0;
             } else {
-                fs_status st = plan_conv_tiles(net, l, g, L);
+                fs_status st = pool_fuse ? plan_conv_pool_tiles(net, l, g, net->L[li + 1].k, L)
+                                         : plan_conv_tiles(net, l, g, L);
                 if (st != FS_OK) return st;
             }
             L.gx = L.direct ? B * F * ((a.out_h * a.out_w + 255) / 256) : B * F * a.nbands * a.tiles_per_band;
@@ -472,6 +561,20 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                       (double)l.cin * k * k * l.cout * es;
             L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, k)
                               : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
+            if (pool_fuse) {
+                const int kp = net->L[li + 1].k;
+                if (g.Q * kp > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
+                const Geo o2 = pool_geo(o, kp);
+                a.pool_k = kp;
+                a.pool_oh = std::max(o2.hmax, 1);
+                a.pool_ow = std::max(o2.wmax, 1);
+                L.n_layers = 2;
+                L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) +
+                          (double)B * true_pixels(o2) * l.cout * es + (double)l.cin * k * k * l.cout * es;
+                L.name += "+pool";
+                o = o2;
+                ++li;  // the pool is done
+            }
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
                 a.head_ncls = net->ncls;

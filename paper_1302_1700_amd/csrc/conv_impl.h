@@ -58,6 +58,16 @@ typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 typedef float f2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
 
+// Two bfloat16 values -> two int16 keys with the same order (negative values
+// get their 15 magnitude bits flipped), so a packed integer max picks the
+// larger value of each half; the map is its own inverse.
+typedef short s2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_key(uint32_t x) { return x ^ (__umul24((x >> 15) & 0x00010001u, 0x7fffu)); }
+__device__ __forceinline__ uint32_t max_i16x2(uint32_t a, uint32_t b)
+{
+    return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s2v, a), __builtin_bit_cast(s2v, b)));
+}
+
 // float -> bfloat16, round to nearest even (one v_cvt_pk_bf16_f32 per pair)
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi)
@@ -245,13 +255,35 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const int hin = a.ext.y[fy], win = a.ext.x[fx];
     const int hout = hin - a.k + 1, wout = win - a.k + 1;
     if (hout <= 0 || wout <= 0) return;
+    // The tile's convolution outputs are numbered l in [l0, lend), pixel l at
+    // row l / twb, column c0 + l % twb of the fragment's output.
     const int c0 = band * a.band_w;
-    const int twb = min(a.band_w, wout - c0);
-    if (twb <= 0) return;
-    const int npix = hout * twb;
-    const int l0 = t * a.mt;
-    if (l0 >= npix) return;
-    const int lend = min(l0 + a.mt, npix);
+    int twb, l0, lend;
+    int y0 = 0, rtM = 0, twM = 0;  // fused pool: max-filter rows [y0, y0 + rtM), columns [c0, c0 + twM)
+    if (a.pool_k) {
+        // Section 2.2.2: child (o_x, o_y) of a k x k pool holds the stride-1
+        // k x k max filter M of its parent at (o_y + k*ybar, o_x + k*xbar),
+        // so every filter position y < hout - k + 1 (and likewise x) feeds
+        // exactly one child.  The tile computes the convolution outputs its
+        // filter positions need: k - 1 more rows and columns.
+        const int hM = hout - a.pool_k + 1, wM = wout - a.pool_k + 1;
+        if (hM <= 0 || wM <= 0) return;
+        twM = min(a.band_w, wM - c0);
+        if (twM <= 0) return;
+        y0 = t * a.pool_rt;
+        if (y0 >= hM) return;
+        rtM = min(a.pool_rt, hM - y0);
+        twb = twM + a.pool_k - 1;
+        l0 = y0 * twb;
+        lend = l0 + (rtM + a.pool_k - 1) * twb;
+    } else {
+        twb = min(a.band_w, wout - c0);
+        if (twb <= 0) return;
+        const int npix = hout * twb;
+        l0 = t * a.mt;
+        if (l0 >= npix) return;
+        lend = min(l0 + a.mt, npix);
+    }
     const int yfirst = l0 / twb;
     const int ylast = (lend - 1) / twb;
     const int R = ylast - yfirst + a.k;  // window rows
@@ -538,53 +570,140 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
     for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
 
-    if (!a.direct_store) {
-        // Restaged: the runs go to an LDS [pixel][channel] tile (one 8- or
-        // 16-byte write each), then all threads copy the tile out in 16-byte
-        // pieces; the pixels of a band row are contiguous in memory, so a tile
-        // row leaves as one contiguous run.
-        constexpr int NW = WN * NB * 16;            // channels this workgroup owns
-        constexpr int TPAD = 16 / (int)sizeof(TC);  // 16 bytes of row padding
-        constexpr int TS = NW + TPAD;
-        const int nbase = blockIdx.y * NW;
-        TC *tile = reinterpret_cast<TC *>(smem);
-        __syncthreads();  // every wave is done with the window / partial sums
-        if (wk == 0) {
+    // LDS [pixel][channel] tile of act(acc + bias) (one 8- or 16-byte write per
+    // run), for the restaged stores and the fused pool
+    constexpr int NW = WN * NB * 16;            // channels this workgroup owns
+    constexpr int TPAD = 16 / (int)sizeof(TC);  // 16 bytes of row padding
+    constexpr int TS = NW + TPAD;
+    // keys: bf16 runs are written as order keys (bf16x2_key), for the pool
+    auto stage_tile = [&](TC *tile, bool keys) {
+        if (wk != 0) return;
 #pragma unroll
-            for (int i = 0; i < MB; ++i) {
-                TC *row = tile + ((wm * MB + i) * 16 + lm) * TS;
-                if constexpr (PAIRED) {
+        for (int i = 0; i < MB; ++i) {
+            TC *row = tile + ((wm * MB + i) * 16 + lm) * TS;
+            if constexpr (PAIRED) {
 #pragma unroll
-                    for (int p = 0; p < NB / 2; ++p) {
-                        // channels 8g .. 8g + 3 from block 2p, 8g + 4 .. 8g + 7 from 2p + 1
-                        float h[8];
+                for (int p = 0; p < NB / 2; ++p) {
+                    // channels 8g .. 8g + 3 from block 2p, 8g + 4 .. 8g + 7 from 2p + 1
+                    float h[8];
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
-                            h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
-                        }
-                        u4 pk;
-#pragma unroll
-                        for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(h[2 * e], h[2 * e + 1]);
-                        *reinterpret_cast<u4 *>(row + (wn * NB + 2 * p) * 16 + 8 * g) = pk;
+                    for (int e = 0; e < 4; ++e) {
+                        h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
+                        h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
                     }
-                } else {
+                    u4 pk;
 #pragma unroll
-                    for (int j = 0; j < NB; ++j) {
-                        TC *dst = row + (wn * NB + j) * 16 + 4 * g;
-                        if constexpr (BF) {
-                            uint2 pk;
-                            pk.x = pack_bf16(act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]));
-                            pk.y = pack_bf16(act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3]));
-                            *reinterpret_cast<uint2 *>(dst) = pk;
-                        } else {
-                            *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]),
-                                                              act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3])};
+                    for (int e = 0; e < 4; ++e) {
+                        pk[e] = pack_bf16(h[2 * e], h[2 * e + 1]);
+                        if (keys) pk[e] = bf16x2_key(pk[e]);
+                    }
+                    *reinterpret_cast<u4 *>(row + (wn * NB + 2 * p) * 16 + 8 * g) = pk;
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < NB; ++j) {
+                    TC *dst = row + (wn * NB + j) * 16 + 4 * g;
+                    if constexpr (BF) {
+                        uint2 pk;
+                        pk.x = pack_bf16(act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]));
+                        pk.y = pack_bf16(act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3]));
+                        if (keys) {
+                            pk.x = bf16x2_key(pk.x);
+                            pk.y = bf16x2_key(pk.y);
                         }
+                        *reinterpret_cast<uint2 *>(dst) = pk;
+                    } else {
+                        *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]),
+                                                          act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3])};
                     }
                 }
             }
         }
+    };
+
+    if (a.pool_k) {
+        // Fused k x k pool (the workgroup owns every channel): the filter
+        // value at fragment position (y, x) = (y0 + r, c0 + c) is the
+        // maximum over the tile's k x k outputs from (r, c), and goes to
+        // child (o_y, o_x) = (y mod k, x mod k) at (y div k, x div k); the
+        // child of (fy, fx) is fragment (fy*k + o_y, fx*k + o_x) of the next
+        // layer (Qc = Q*k per axis).  Same values as a separate pool kernel
+        // reading this layer's stored (rounded) outputs.
+        TC *tile = reinterpret_cast<TC *>(smem);
+        __syncthreads();  // every wave is done with the window / partial sums
+        stage_tile(tile, true);
+        __syncthreads();
+        const int kp = a.pool_k, ew = twb;
+        const int Qc = a.Q * kp;
+        const size_t child_px = (size_t)a.pool_oh * a.pool_ow;
+        const size_t cbase = (size_t)(q / a.F) * a.F * kp * kp;  // first child of image b
+        const Div dkp(kp), dtm(twM);
+        auto child_ptr = [&](int r, int c) {
+            int ybar, oy, xbar, ox;
+            dkp.qr(y0 + r, ybar, oy);
+            dkp.qr(c0 + c, xbar, ox);
+            const size_t qc = cbase + (size_t)(fy * kp + oy) * Qc + (fx * kp + ox);
+            return reinterpret_cast<TC *>(a.out) + (qc * child_px + (size_t)ybar * a.pool_ow + xbar) * a.cout;
+        };
+        if ((a.cout % TPAD) == 0) {
+            const int nv = a.cout / TPAD;
+            const Div dnv(nv);
+            const int total = rtM * twM * nv;
+            for (int idx = threadIdx.x; idx < total; idx += 256) {
+                int p, v, r, c;
+                dnv.qr(idx, p, v);
+                dtm.qr(p, r, c);
+                const TC *src = tile + __mul24(__mul24(r, ew) + c, TS) + v * TPAD;
+                u4 m = *reinterpret_cast<const u4 *>(src);
+                for (int i = 0; i < kp; ++i)
+                    for (int j = 0; j < kp; ++j) {
+                        const u4 x = *reinterpret_cast<const u4 *>(src + __mul24(__mul24(i, ew) + j, TS));
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            if constexpr (BF)
+                                m[e] = max_i16x2(m[e], x[e]);
+                            else
+                                m[e] = __float_as_uint(fmaxf(__uint_as_float(m[e]), __uint_as_float(x[e])));
+                        }
+                    }
+                if constexpr (BF) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) m[e] = bf16x2_key(m[e]);
+                }
+                *reinterpret_cast<u4 *>(child_ptr(r, c) + v * TPAD) = m;
+            }
+        } else {
+            const Div dco(a.cout);
+            const int total = rtM * twM * a.cout;
+            for (int idx = threadIdx.x; idx < total; idx += 256) {
+                int p, ch, r, c;
+                dco.qr(idx, p, ch);
+                dtm.qr(p, r, c);
+                const TC *src = tile + __mul24(__mul24(r, ew) + c, TS) + ch;
+                TC m = src[0];
+                for (int i = 0; i < kp; ++i)
+                    for (int j = 0; j < kp; ++j) {
+                        const TC x = src[__mul24(__mul24(i, ew) + j, TS)];
+                        if constexpr (BF)
+                            m = (TC)max_i16x2(m, x);  // keys in the low half
+                        else
+                            m = fmaxf(m, x);
+                    }
+                if constexpr (BF) m = (TC)bf16x2_key(m);
+                child_ptr(r, c)[ch] = m;
+            }
+        }
+        return;
+    }
+
+    if (!a.direct_store) {
+        // Restaged: all threads copy the tile out in 16-byte pieces; the
+        // pixels of a band row are contiguous in memory, so a tile row leaves
+        // as one contiguous run.
+        const int nbase = blockIdx.y * NW;
+        TC *tile = reinterpret_cast<TC *>(smem);
+        __syncthreads();  // every wave is done with the window / partial sums
+        stage_tile(tile, false);
         __syncthreads();
         TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
         const int orow = a.out_w * a.cout;

@@ -57,6 +57,12 @@ struct ConvArgs {
     int lds_bytes;        // dynamic LDS bytes of one workgroup
     int direct_store;     // 1: lanes store their channel runs straight to memory;
                           // 0: restaged through LDS and written as whole rows
+    // Fused max-pool (pool_k > 0): the launch also applies the k x k pool that
+    // follows the convolution and writes its children straight to `out`
+    // ([nfrag * k^2][pool_oh][pool_ow][cout]); bands then run over the
+    // stride-1 max filter's columns, and a tile is pool_rt filter rows plus
+    // the k - 1 rows and columns of convolution outputs they also need.
+    int pool_k, pool_rt, pool_oh, pool_ow;
     AxisTable ext;        // true sizes of the input fragments
     // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
     // activation, and the reassembly are applied in the epilogue, which then

@@ -315,6 +315,42 @@ def test_split_k_tiles(fsb, monkeypatch, tile):
     assert np.abs(got - ref).max() <= TOL["f32"]
 
 
+@pytest.mark.parametrize("fuse", ["0", "1"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_pool_fusion_modes(fsb, monkeypatch, fuse, dt):
+    """Convolutions with the following max-pool fused into their epilogue (or
+    not): 2x2 and 3x3 pools, channel counts on and off the 16-byte grid
+    (vector and per-channel maxima), the gather and the vector path, ragged
+    fragments, B = 2."""
+    layers = [wl.conv(2, 3, 32), wl.pool(3, 32), wl.conv(2, 32, 18), wl.pool(2, 18),
+              wl.conv(2, 18, 64), wl.pool(2, 64), wl.fc(2, 64, 24), wl.fc(1, 24, 3, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 21, 0.2)
+    img = wl.make_image(22, 2, w0 + 37, w0 + 44, 3)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", fuse)
+    net = fsb.Net(layers, params, 3, 0, dt)
+    names = [L["name"] for L in net.launches(2, w0 + 37, w0 + 44)]
+    net.close()
+    assert sum(n.endswith("+pool") for n in names) == (3 if fuse == "1" else 0), names
+    got = _scan(fsb, layers, params, img, 3, dtype=dt)
+    assert np.abs(got - ref).max() <= TOL[dt]
+
+
+def test_pool_fusion_split_k(fsb, monkeypatch):
+    """Split-K (two waves per pixel block) feeding the fused pool."""
+    layers = [wl.conv(2, 1, 48), wl.pool(2, 48), wl.conv(3, 48, 48), wl.pool(2, 48),
+              wl.fc(2, 48, 20), wl.fc(1, 20, 2, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 23, 0.1)
+    img = wl.make_image(24, 1, w0 + 53, w0 + 40, 1)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "1")
+    monkeypatch.setenv("FRAGSCAN_TILE", "2:4,3,1,0,2")
+    got = _scan(fsb, layers, params, img, 1)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+
+
 @pytest.mark.parametrize("store", ["direct", "lds"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_store_modes(fsb, monkeypatch, store, dt):
