@@ -79,6 +79,7 @@ struct fs_net {
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
     size_t head_wp_off = 0;   // head weights in the previous layer's (block, row) order
+    int ncu = 0;              // compute units of the device (0: plan-only net)
     int head_cin = 0;
     void *d_mem = nullptr;
     size_t mem_bytes = 0;
@@ -554,6 +555,14 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.gx = L.direct ? B * F * ((a.out_h * a.out_w + 255) / 256) : B * F * a.nbands * a.tiles_per_band;
             L.gy = L.direct ? 1 : l.nbt / (l.nb * l.wn);
             if (!L.direct) L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
+            // The FC layer with the fused head, when its register tile fits
+            // only two workgroups per CU, ran 2-7% faster one per CU on grids
+            // of at most 12 workgroups per CU (N4 on 512x512 and 2x512x512
+            // images; 3-5% slower on larger grids; other layers, whose tiles
+            // fit three, 12-18% slower): pad its LDS to admit one.
+            if (fused_here && !L.direct && net->ncu > 0 && (long long)L.gx * L.gy <= 12LL * net->ncu &&
+                conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, a.lds_bytes) == 2)
+                a.lds_bytes = std::max(a.lds_bytes, (int)(kMaxLdsBytes / 2 + 1024));
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
@@ -966,6 +975,11 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
     if (e != hipSuccess) {
         delete net;
         return hip_fail(e, "hipGetDevice");
+    }
+    {
+        int n = 0;
+        if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, net->device) == hipSuccess && n > 0)
+            net->ncu = n;
     }
     net->mem_bytes = blob.size();
     e = hipMalloc(&net->d_mem, blob.size());

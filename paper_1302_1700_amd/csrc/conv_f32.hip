@@ -2,12 +2,41 @@
 // convolution launcher.
 #include "conv_impl.h"
 
+#include <array>
 #include <cstdio>
+#include <map>
+#include <mutex>
 
 namespace fs {
 
 hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int wn, int wk, bool vec, int gx,
                             int gy, hipStream_t s);
+int conv_blocks_per_cu_bf16(bool in_f32, int mb, int nb, int wn, int wk, bool vec, int lds);
+
+int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, int lds)
+{
+    // memoised per device and kernel shape (plans are rebuilt on every scan)
+    static std::mutex mu;
+    static std::map<std::array<int, 10>, int> memo;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return 0;
+    const std::array<int, 10> key{dev, dtype, in_f32, mb, nb, wn, wk, vec, lds, 0};
+    {
+        std::lock_guard<std::mutex> g(mu);
+        auto it = memo.find(key);
+        if (it != memo.end()) return it->second;
+    }
+    int n;
+    if (dtype == DT_BF16)
+        n = conv_blocks_per_cu_bf16(in_f32, mb, nb, wn, wk, vec, lds);
+    else
+        n = vec ? conv::tile_blocks_per_cu<false, false, true>(mb, nb, wn, wk, lds)
+                : conv::tile_blocks_per_cu<false, false, false>(mb, nb, wn, wk, lds);
+    std::lock_guard<std::mutex> g(mu);
+    memo[key] = n;
+    return n;
+}
+
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec)
 {
 #define FS_CONV_HAS(M, N, W, K) \

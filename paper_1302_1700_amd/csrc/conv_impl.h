@@ -46,6 +46,7 @@
 
 #include "fs_internal.h"
 
+#include <algorithm>
 #include <type_traits>
 
 namespace fs {
@@ -830,6 +831,34 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
 #define FS_CONV_TILES_GATHER(X)                                                                 \
     X(1, 1, 1, 1) X(1, 2, 1, 1) X(1, 3, 1, 1) X(1, 4, 1, 1) X(2, 1, 1, 1) X(2, 2, 1, 1)          \
     X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 1) X(4, 4, 1, 1)
+
+// Workgroups of one tile shape that fit on a CU with `lds` dynamic LDS bytes
+// (0 if unknown): a 256-thread workgroup puts one wave on each of the 4
+// SIMDs, each SIMD holds 512 VGPRs per lane (allocated in granules of 8),
+// and the CU has kMaxLdsBytes of LDS.
+template <bool BF, bool IN_F32, bool VEC>
+int tile_blocks_per_cu(int mb, int nb, int wn, int wk, int lds)
+{
+#define FS_CONV_OCC(M, N, W, K)                                                                          \
+    if (mb == M && nb == N && wn == W && wk == K) {                                                      \
+        hipFuncAttributes fa{};                                                                          \
+        if (hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(conv_frag_mfma<M, N, W, K, BF, IN_F32, VEC>)) != hipSuccess) { \
+            (void)hipGetLastError();                                                                     \
+            return 0;                                                                                    \
+        }                                                                                                \
+        const int regs = (fa.numRegs + 7) / 8 * 8;                                                       \
+        int n = regs > 0 ? 512 / regs : 8;                                                               \
+        if (lds > 0) n = std::min(n, (int)(kMaxLdsBytes / (size_t)lds));                                 \
+        return std::min(n, 8);                                                                           \
+    }
+    if constexpr (VEC) {
+        FS_CONV_TILES_VEC(FS_CONV_OCC)
+    } else {
+        FS_CONV_TILES_GATHER(FS_CONV_OCC)
+    }
+#undef FS_CONV_OCC
+    return 0;
+}
 
 template <bool BF, bool IN_F32, bool VEC>
 hipError_t dispatch_tile(const ConvArgs &a, int mb, int nb, int wn, int wk, int gx, int gy, hipStream_t s)

@@ -111,6 +111,9 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);
+// Workgroups of that convolution kernel resident per CU with `lds` bytes of
+// dynamic LDS, on the current device (0 if the query fails).
+int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, int lds);
 // Direct (vector-ALU) convolution for tiny K = c_in * k * k (<= 64) and
 // c_out <= 48; wpk = weights as [rows][KP] float32 with rows = c_out rounded
 // up to 8 (zero rows past c_out), K index (dy * k + dx) * c_in + ci, zero
