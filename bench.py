@@ -1,6 +1,7 @@
 """Benchmark of the fragment-based image scan on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload ID] [--no-cpu]
+                    [--border valid|reflect|symmetric]
 
 A step is one full scan (every layer, the head and the reassembly) of the
 workload's synthetic image batch, already resident in device memory.  Prints
@@ -14,7 +15,9 @@ one JSON line:
   cpu_baseline the per-patch CPU oracle on a bounded sample of windows, on
                this host's cores
 Default workload: net N4 (the paper's Table 1 net) on a 512 x 512 greyscale
-image, 418 x 418 windows.
+image, 418 x 418 windows.  --border reflect / symmetric scans with mirrored
+edges instead (Section 3.2's setup: one output per pixel, 512 x 512); the
+per-launch figures then come from the scan of the extended image.
 """
 import argparse
 import json
@@ -98,6 +101,8 @@ def main():
     ap.add_argument("--profile-reps", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline legs")
     ap.add_argument("--cpu-fragment", action="store_true", help="also time the CPU fragment method")
+    ap.add_argument("--border", default="valid", choices=["valid", "reflect", "symmetric"],
+                    help="mirrored image edges (one output per pixel)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported" % args.gpus,
@@ -114,28 +119,39 @@ def main():
     torch.cuda.set_device(0)
     net = fragscan.Net(w.layers, params, w.channels, 0, w.dtype)
     x = torch.from_numpy(img).cuda()
-    out = torch.empty((w.batch, w.out_h, w.out_w, w.n_classes), dtype=torch.float32, device="cuda")
-    ws = net.workspace(w.batch, w.height, w.width, x.device)
-    plan = net.plan(w.batch, w.height, w.width)
-    launches = net.launches(w.batch, w.height, w.width)
+    border = args.border
+    oh, ow = (w.out_h, w.out_w) if border == "valid" else (w.height, w.width)
+    out = torch.empty((w.batch, oh, ow, w.n_classes), dtype=torch.float32, device="cuda")
+    ws = net.workspace(w.batch, w.height, w.width, x.device, border)
+    plan = net.plan(w.batch, w.height, w.width, border)
+    # the launches of the (extended) image's scan
+    eh, ew = (w.height, w.width) if border == "valid" else (w.height + w.patch - 1, w.width + w.patch - 1)
+    launches = net.launches(w.batch, eh, ew)
 
     for _ in range(args.warmup):
-        net.scan(x, out=out, workspace=ws)
+        net.scan(x, out=out, workspace=ws, border=border)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
     for _ in range(args.steps):
-        net.scan(x, out=out, workspace=ws)
+        net.scan(x, out=out, workspace=ws, border=border)
     t1.record(stream)
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / args.steps
-    pixels = w.batch * w.out_h * w.out_w
+    pixels = w.batch * oh * ow
 
     # per-launch mean durations: HIP events around --profile-reps back-to-back
-    # runs of each launch on the scan's stream
-    per = net.profile(x, reps=args.profile_reps, out=out)
+    # runs of each launch on the scan's stream (mirrored borders: the same
+    # launches on an image of the extended size; timing does not depend on
+    # the pixel values)
+    if border == "valid":
+        per = net.profile(x, reps=args.profile_reps, out=out)
+    else:
+        xe = torch.zeros((w.batch, eh, ew, w.channels), dtype=torch.float32, device="cuda")
+        xe[:, :w.height, :w.width] = x
+        per = net.profile(xe, reps=args.profile_reps)
     peak_mm = PEAK["bf16_tflops"] if w.dtype == "bf16" else PEAK["f32_tflops"]
     rows = []
     for L, t in zip(launches, per):
@@ -177,7 +193,8 @@ def main():
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "image": [w.batch, w.height, w.width, w.channels],
-                   "patch": w.patch, "outputs": [w.batch, w.out_h, w.out_w], "fragments": net.info["n_fragments"]},
+                   "patch": w.patch, "outputs": [w.batch, oh, ow], "fragments": net.info["n_fragments"],
+                   "border": border},
         "tflops": plan["flops"] / (ms * 1e-3) / 1e12,
         "pct_mfma_peak": 100.0 * plan["flops"] / (ms * 1e-3) / 1e12 / peak_mm,
         "conv_tflops_in_conv_kernels": conv_flops / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0,

@@ -176,6 +176,39 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W,
 fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
                   float *d_out, void *d_workspace, size_t workspace_bytes, void *stream);
 
+/* Border handling (Section 3.2: the image's edges are mirrored so that the
+ * net can be applied at every position).  FS_BORDER_VALID is the plain scan
+ * above.  The mirrored modes extend the image by p0 = floor((w_0 - 1) / 2)
+ * pixels before the first row / column and w_0 - 1 - p0 after the last, so
+ * that output (y, x) is the window whose central pixel (for even w_0: the
+ * pixel p0 below and right of its top-left) is image pixel (y, x), and the
+ * output map is H x W.  Index i outside [0, n) maps to
+ *   FS_BORDER_REFLECT:   period 2(n - 1), mirrored about the edge pixels
+ *                        (..., 2, 1, | 0, 1, 2, ...), n = 1: pixel 0;
+ *   FS_BORDER_SYMMETRIC: period 2n, edge pixels repeated
+ *                        (..., 1, 0, | 0, 1, ...),
+ * repeatedly for borders wider than the image.  The paper does not say
+ * which of the two it used. */
+typedef enum {
+    FS_BORDER_VALID = 0,
+    FS_BORDER_REFLECT = 1,
+    FS_BORDER_SYMMETRIC = 2
+} fs_border;
+
+/* fs_scan_plan for a border mode: out_h = H and out_w = W for the mirrored
+ * modes; workspace_bytes includes the extended image.  FS_ERR_INVALID_ARG
+ * for an unknown mode. */
+fs_status fs_scan_plan_border(const fs_net *net, int32_t B, int32_t H, int32_t W, int32_t border,
+                              fs_plan_info *out);
+
+/* fs_scan for a border mode: d_out is [B][out_h][out_w][n_classes] as
+ * fs_scan_plan_border gives it (H x W for the mirrored modes, any H, W >= 1);
+ * the extended image is built in d_workspace, which must hold
+ * fs_scan_plan_border's workspace_bytes.  Otherwise as fs_scan. */
+fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
+                         int32_t border, float *d_out, void *d_workspace, size_t workspace_bytes,
+                         void *stream);
+
 /* fs_scan with every launch repeated `reps` times back to back between two
  * HIP events on `stream` (a repetition recomputes the same values, so d_out
  * ends as after fs_scan); synchronises the stream and writes, per launch,

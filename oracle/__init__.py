@@ -14,7 +14,10 @@ Contents
   frag_cpu        the fragment method itself on the CPU, double precision
                   (Section 2.2), a second derivation checked against
                   patch_forward and the CPU "image-based" baseline
+  border          mirrored image borders (Section 3.2) and the per-patch
+                  forward on the extended image
 """
 from .patch import patch_forward, ORACLE_LIB  # noqa: F401
 from . import index  # noqa: F401
 from . import frag_cpu  # noqa: F401
+from . import border  # noqa: F401

@@ -685,6 +685,32 @@ fs_status check_device(const fs_net *net)
     return FS_OK;
 }
 
+// Plan of a scan with a border mode: the mirrored modes scan the extended
+// image (H + w_0 - 1) x (W + w_0 - 1), built in the workspace after the
+// scan's own buffers (from byte pad_off).
+fs_status border_plan(const fs_net *net, int B, int H, int W, int border, Plan &P, int &He, int &We,
+                      size_t &pad_off, size_t &ws_total)
+{
+    if (border != BORDER_VALID && border != BORDER_REFLECT && border != BORDER_SYMMETRIC)
+        return fail(FS_ERR_INVALID_ARG, "unknown border mode %d", border);
+    He = H;
+    We = W;
+    if (border != BORDER_VALID) {
+        if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
+        He = H + net->patch - 1;
+        We = W + net->patch - 1;
+    }
+    fs_status st = make_plan(net, B, He, We, P);
+    if (st != FS_OK) return st;
+    pad_off = P.ws_bytes;
+    ws_total = P.ws_bytes;
+    if (border != BORDER_VALID) {
+        pad_off = align_up(P.ws_bytes, 256);
+        ws_total = pad_off + (size_t)B * He * We * net->C * sizeof(float);
+    }
+    return FS_OK;
+}
+
 fs_status validate_scan(const fs_net *net, const float *d_image, int B, int H, int W, float *d_out,
                         void *d_ws, size_t ws_bytes, Plan &P)
 {
@@ -1043,6 +1069,60 @@ fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_pl
     out->workspace_bytes = P.ws_bytes;
     out->flops = P.flops;
     out->min_bytes = P.bytes;
+    return FS_OK;
+}
+
+fs_status fs_scan_plan_border(const fs_net *net, int32_t B, int32_t H, int32_t W, int32_t border,
+                              fs_plan_info *out)
+{
+    if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
+    Plan P;
+    int He, We;
+    size_t pad_off, ws_total;
+    fs_status st = border_plan(net, B, H, W, border, P, He, We, pad_off, ws_total);
+    if (st != FS_OK) return st;
+    out->batch = B;
+    out->out_h = P.ny;
+    out->out_w = P.nx;
+    out->n_launches = (int)P.launches.size() + (border != BORDER_VALID);
+    out->workspace_bytes = ws_total;
+    out->flops = P.flops;
+    out->min_bytes = P.bytes + (border != BORDER_VALID ? 2.0 * B * He * We * net->C * sizeof(float) : 0.0);
+    return FS_OK;
+}
+
+fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, int32_t border,
+                         float *d_out, void *d_workspace, size_t workspace_bytes, void *stream)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
+    if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
+        return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
+    Plan P;
+    int He, We;
+    size_t pad_off, ws_total;
+    fs_status st = border_plan(net, B, H, W, border, P, He, We, pad_off, ws_total);
+    if (st != FS_OK) return st;
+    if (workspace_bytes < ws_total)
+        return fail(FS_ERR_WORKSPACE, "workspace of %zu bytes, the scan needs %zu", workspace_bytes, ws_total);
+    if (ws_total && !d_workspace) return fail(FS_ERR_INVALID_ARG, "workspace pointer is NULL");
+    if ((uintptr_t)d_workspace & 255) return fail(FS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    st = check_device(net);
+    if (st != FS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const float *img = d_image;
+    if (border != BORDER_VALID) {
+        float *pad = reinterpret_cast<float *>(static_cast<char *>(d_workspace) + pad_off);
+        const int p0 = (net->patch - 1) / 2;
+        hipError_t e = launch_mirror_pad(d_image, pad, B, H, W, net->C, p0, He, We, border, s);
+        if (e != hipSuccess) return fail(FS_ERR_HIP, "mirror pad: %s", hipGetErrorString(e));
+        img = pad;
+    }
+    for (int i = 0; i < (int)P.launches.size(); ++i) {
+        hipError_t e = enqueue(net, P, img, d_out, d_workspace, s, i);
+        if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
+                                         hipGetErrorString(e));
+    }
     return FS_OK;
 }
 

@@ -108,6 +108,11 @@ struct HeadArgs {
 hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
+// Mirrored borders: out[B][He][We][C] from in[B][H][W][C], extended index
+// (y, x) reading image pixel (mirror(y - p0, H), mirror(x - p0, W)).
+enum BorderMode { BORDER_VALID = 0, BORDER_REFLECT = 1, BORDER_SYMMETRIC = 2 };
+hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0, int He, int We,
+                             int mode, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);

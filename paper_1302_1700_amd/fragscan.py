@@ -18,6 +18,7 @@ FS_OK, FS_ERR_INVALID_ARG, FS_ERR_SHAPE, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE, F
 KIND = {"conv": 0, "pool": 1, "fc": 2}
 ACT = {"none": 0, "tanh": 1, "softmax": 2}
 DTYPE = {"f32": 0, "bf16": 1}
+BORDER = {"valid": 0, "reflect": 1, "symmetric": 2}
 
 
 class FsError(RuntimeError):
@@ -52,7 +53,7 @@ class fs_launch_info(ctypes.Structure):
 
 EXPORTS = ["fs_net_create", "fs_net_create_plan_only", "fs_net_destroy", "fs_net_query", "fs_scan_plan", "fs_scan_launches",
            "fs_scan", "fs_scan_profile", "fs_fragment_table", "fs_reassembly_index",
-           "fs_status_str", "fs_last_error"]
+           "fs_status_str", "fs_last_error", "fs_scan_plan_border", "fs_scan_border"]
 
 _lib = None
 
@@ -73,6 +74,8 @@ def load():
         "fs_net_destroy": [VP],
         "fs_net_query": [VP, P(fs_net_info)],
         "fs_scan_plan": [VP, I32, I32, I32, P(fs_plan_info)],
+        "fs_scan_plan_border": [VP, I32, I32, I32, I32, P(fs_plan_info)],
+        "fs_scan_border": [VP, VP, I32, I32, I32, I32, VP, VP, SZ, VP],
         "fs_scan_launches": [VP, I32, I32, I32, P(fs_launch_info), I32],
         "fs_scan": [VP, VP, I32, I32, I32, VP, VP, SZ, VP],
         "fs_scan_profile": [VP, VP, I32, I32, I32, VP, VP, SZ, VP, I32, P(ctypes.c_float), I32],
@@ -154,9 +157,12 @@ class Net:
             pass
 
     # -- planning --------------------------------------------------------------
-    def plan(self, B, H, W):
+    def plan(self, B, H, W, border="valid"):
         p = fs_plan_info()
-        _check(load().fs_scan_plan(self._h, B, H, W, ctypes.byref(p)))
+        if border == "valid":
+            _check(load().fs_scan_plan(self._h, B, H, W, ctypes.byref(p)))
+        else:
+            _check(load().fs_scan_plan_border(self._h, B, H, W, BORDER[border], ctypes.byref(p)))
         return {n: getattr(p, n) for n, _ in fs_plan_info._fields_}
 
     def launches(self, B, H, W):
@@ -190,9 +196,9 @@ class Net:
         return buf.reshape(H - self.patch + 1, W - self.patch + 1, 3)
 
     # -- scanning --------------------------------------------------------------
-    def workspace(self, B, H, W, device=None):
+    def workspace(self, B, H, W, device=None, border="valid"):
         import torch
-        nbytes = self.plan(B, H, W)["workspace_bytes"]
+        nbytes = self.plan(B, H, W, border)["workspace_bytes"]
         key = (nbytes, str(device))
         ws = self._ws.get(key)
         if ws is None:
@@ -201,19 +207,28 @@ class Net:
             self._ws[key] = ws
         return ws
 
-    def scan(self, image, out=None, workspace=None, stream=None):
-        """image: CUDA float32 tensor [B, H, W, C] (contiguous) -> [B, H-w0+1, W-w0+1, n]."""
+    def scan(self, image, out=None, workspace=None, stream=None, border="valid"):
+        """image: CUDA float32 tensor [B, H, W, C] (contiguous) -> [B, H-w0+1, W-w0+1, n]
+        (border "valid"), or [B, H, W, n] with the image's edges mirrored
+        ("reflect": about the edge pixels, "symmetric": edge pixels repeated)."""
         import torch
         if not image.is_cuda or image.dtype != torch.float32 or not image.is_contiguous():
             raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
+        if border not in BORDER:
+            raise ValueError("border must be one of %s" % sorted(BORDER))
         B, H, W, C = image.shape
+        oh, ow = (H - self.patch + 1, W - self.patch + 1) if border == "valid" else (H, W)
         if out is None:
-            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes),
-                              dtype=torch.float32, device=image.device)
-        ws = workspace if workspace is not None else self.workspace(B, H, W, image.device)
-        _check(load().fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
-                              ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                              ws.numel(), _stream_handle(stream)))
+            out = torch.empty((B, oh, ow, self.n_classes), dtype=torch.float32, device=image.device)
+        ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, border)
+        if border == "valid":
+            _check(load().fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                  ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                  ws.numel(), _stream_handle(stream)))
+        else:
+            _check(load().fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
+                                         ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                         ws.numel(), _stream_handle(stream)))
         return out
 
     def profile(self, image, reps=10, out=None, stream=None):

@@ -152,6 +152,30 @@ def test_split_k_needs_a_step_per_wave(monkeypatch):
     assert _status(layers, c0=16) == fsb.FS_OK
 
 
+def test_border_plans():
+    """Mirrored borders (Section 3.2): H x W outputs for any H, W >= 1, the
+    scan of the extended image plus room for it in the workspace."""
+    w = wl.WORKLOADS[2]
+    net = _plan_net(w.layers)
+    for mode in ("reflect", "symmetric"):
+        for H, W in ((512, 512), (40, 33), (1, 1)):
+            p = net.plan(1, H, W, mode)
+            assert (p["out_h"], p["out_w"]) == (H, W)
+            inner = net.plan(1, H + w.patch - 1, W + w.patch - 1)
+            assert p["workspace_bytes"] >= inner["workspace_bytes"] + (H + w.patch - 1) * (W + w.patch - 1) * 4
+            assert p["n_launches"] == inner["n_launches"] + 1
+    assert net.plan(2, 512, 512, "valid") == net.plan(2, 512, 512)
+    net.close()
+
+
+def test_border_mode_rejected_when_unknown():
+    net = _plan_net(wl.WORKLOADS[1].layers)
+    p = fsb.fs_plan_info()
+    st = fsb.load().fs_scan_plan_border(net._h, 1, 64, 64, 7, fsb.ctypes.byref(p))
+    assert st == fsb.FS_ERR_INVALID_ARG
+    net.close()
+
+
 def test_image_smaller_than_patch_rejected():
     net = _plan_net(wl.WORKLOADS[1].layers)
     with pytest.raises(fsb.FsError) as e:

@@ -315,6 +315,72 @@ def test_split_k_tiles(fsb, monkeypatch, tile):
     assert np.abs(got - ref).max() <= TOL["f32"]
 
 
+def _scan_border(fsb, layers, params, img, c0, mode, dtype="f32"):
+    net = fsb.Net(layers, params, c0, 0, dtype)
+    x = torch.from_numpy(np.ascontiguousarray(img, np.float32)).cuda()
+    out = net.scan(x, border=mode)
+    torch.cuda.synchronize()
+    res = out.cpu().numpy().astype(np.float64)
+    net.close()
+    return res
+
+
+@pytest.mark.parametrize("mode", ["reflect", "symmetric"])
+def test_mirrored_borders_full(fsb, mode):
+    """Section 3.2's mirrored edges: H x W outputs, each the window centred on
+    its pixel; workload 1's net (even w_0 = 14: 6 rows / columns before, 7
+    after), B = 2, full map against the per-patch oracle on the extended
+    image."""
+    w = wl.WORKLOADS[1]
+    params, _ = wl.workload_inputs(1)
+    img = wl.make_image(41, 2, 40, 37, 1)
+    ref = oracle.border.scan_mirrored(w.layers, params, img, w.patch, mode)
+    got = _scan_border(fsb, w.layers, params, img, 1, mode)
+    assert got.shape == ref.shape == (2, 40, 37, 2)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+
+
+@pytest.mark.parametrize("mode", ["reflect", "symmetric"])
+def test_mirrored_image_smaller_than_border(fsb, mode):
+    """A 3 x 2 image under a 14 x 14 window: the border is mirrored
+    repeatedly; single-pixel rows use the one pixel."""
+    w = wl.WORKLOADS[1]
+    params, _ = wl.workload_inputs(1)
+    for H, W in ((3, 2), (1, 5)):
+        img = wl.make_image(42, 1, H, W, 1)
+        ref = oracle.border.scan_mirrored(w.layers, params, img, w.patch, mode)
+        got = _scan_border(fsb, w.layers, params, img, 1, mode)
+        assert np.abs(got - ref).max() <= TOL["f32"], (H, W)
+
+
+def test_mirrored_n4_sampled(fsb):
+    """Net N4 (odd w_0 = 95, 47 pixels each side) on a 60 x 70 image, smaller
+    than the window: sampled windows, corners included."""
+    w = wl.WORKLOADS[2]
+    params, _ = wl.workload_inputs(2)
+    img = wl.make_image(43, 1, 60, 70, 1)
+    got = _scan_border(fsb, w.layers, params, img, 1, "reflect")
+    rng = np.random.default_rng(44)
+    pts = {(0, 0, 0), (0, 59, 69), (0, 0, 69), (0, 59, 0)}
+    for _ in range(60):
+        pts.add((0, int(rng.integers(0, 60)), int(rng.integers(0, 70))))
+    pts = np.array(sorted(pts), np.int32)
+    ref = oracle.border.scan_mirrored(w.layers, params, img, w.patch, "reflect", pts)
+    assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref).max() <= TOL["f32"]
+
+
+def test_mirrored_bf16(fsb):
+    w = wl.WORKLOADS[5]
+    params, _ = wl.workload_inputs(5, height=61, width=61)
+    img = wl.make_image(45, 1, 50, 47, 3)
+    got = _scan_border(fsb, w.layers, params, img, 3, "symmetric", "bf16")
+    rng = np.random.default_rng(46)
+    pts = np.array(sorted({(0, int(rng.integers(0, 50)), int(rng.integers(0, 47))) for _ in range(60)}
+                          | {(0, 0, 0), (0, 49, 46)}), np.int32)
+    ref = oracle.border.scan_mirrored(w.layers, params, img, w.patch, "symmetric", pts)
+    assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref).max() <= TOL["bf16"]
+
+
 @pytest.mark.parametrize("fuse", ["0", "1"])
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 def test_pool_fusion_modes(fsb, monkeypatch, fuse, dt):
