@@ -216,6 +216,7 @@ struct Launch {
     int mb = 0, nb = 0, wn = 1, wk = 1;
     bool vec = false, has_fc = false;
     bool direct = false;      // vector-ALU convolution for tiny K
+    int frag_tiles = 0, frag_lds = 0;  // per-fragment tiling when run tiles are planned
     int gx = 1, gy = 1;
     int frags = 0;
     long long out_pixels = 0;
@@ -250,7 +251,54 @@ long long true_pixels(const Geo &g)
     return sy * sx;  // separable: sum over (fy, fx) of ey[fy] * ex[fx]
 }
 
-// Tile choice for a conv launch (see conv_kernel.hip for the scheme).
+// Run tiles for a one-band layer: mt consecutive output pixels of the
+// image's fragment sequence per tile instead of per fragment, whose tiles
+// are counted for the largest fragment and leave the smaller ones' last
+// tiles part empty (N4's 3x3 layer on a 448 x 448 image: 22-23 outputs per
+// axis, 5 tiles of 128 per fragment where 4 hold the 22 x 22 ones).  A tile
+// then spans at most two fragments, which needs every fragment to hold at
+// least mt outputs; its window stacks the rows of both.  Planned when the
+// LDS still fits and FRAGSCAN_RUN is not 0; make_plan then keeps them where
+// they save a round of workgroups.
+void plan_run_tiles(const NetLayer &l, const Geo &in, int mt, int cs, int es, int offtab, size_t other,
+                    Launch &L)
+{
+    if (const char *e = getenv("FRAGSCAN_RUN"); e && e[0] == '0') return;
+    const int k = l.k;
+    if (in.Q > kMaxAxis) return;
+    long long sy = 0, sx = 0;
+    int hmin = 1 << 30, wmin = 1 << 30, wmax = 0;
+    ConvArgs &a = L.conv;
+    a.run_ypre[0] = a.run_xpre[0] = 0;
+    for (int i = 0; i < in.Q; ++i) {
+        const int ho = in.ey[i] - k + 1, wo = in.ex[i] - k + 1;
+        hmin = std::min(hmin, ho);
+        wmin = std::min(wmin, wo);
+        wmax = std::max(wmax, wo);
+        sy += std::max(ho, 0);
+        sx += std::max(wo, 0);
+        if (sy >= 65536 || sx >= 65536) return;  // uint16 prefix sums
+        a.run_ypre[i + 1] = (uint16_t)sy;
+        a.run_xpre[i + 1] = (uint16_t)sx;
+    }
+    if (hmin <= 0 || wmin <= 0 || (long long)hmin * wmin < mt || sy * sx >= (1LL << 31)) return;
+    // window rows of a tile: n0 pixels of one fragment from any column span
+    // at most (n0 + w - 2) / w + 1 output rows, the n1 = mt - n0 of the next
+    // (from its column 0) (n1 - 1) / w + 1, each plus k - 1
+    const int rows = (mt + wmin - 1) / wmin + 2 * k;
+    const size_t lds = offtab + (size_t)rows * (wmax + k - 1) * cs * es;
+    const size_t need = std::max(std::max(lds, other), (size_t)a.lds_bytes);
+    if (need > kMaxLdsBytes) return;
+    L.frag_tiles = a.tiles_per_band;
+    L.frag_lds = a.lds_bytes;
+    a.run = 1;
+    a.run_pix = (int)(sy * sx);
+    a.run_wsum = (int)sx;
+    a.tiles_per_band = (int)((sy * sx + mt - 1) / mt);
+    a.lds_bytes = (int)need;
+}
+
+// Tile choice for a conv launch (the tiling itself is described in conv_impl.h).
 fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, Launch &L)
 {
     const int k = l.k;
@@ -332,6 +380,8 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                 continue;
             }
             L.conv.lds_bytes = (int)need;
+            L.conv.run = 0;
+            if (nbands == 1 && direct) plan_run_tiles(l, in, mt, cs, es, offtab, std::max(part, red), L);
             return FS_OK;
         }
         if (mb_force) break;
@@ -552,17 +602,50 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                                          : plan_conv_tiles(net, l, g, L);
                 if (st != FS_OK) return st;
             }
-            L.gx = L.direct ? B * F * ((a.out_h * a.out_w + 255) / 256) : B * F * a.nbands * a.tiles_per_band;
             L.gy = L.direct ? 1 : l.nbt / (l.nb * l.wn);
-            if (!L.direct) L.gx = (L.gx + 7) / 8 * 8;  // XCD-contiguous tile order needs a multiple of 8
-            // The FC layer with the fused head, when its register tile fits
-            // only two workgroups per CU, ran 2-7% faster one per CU on grids
-            // of at most 12 workgroups per CU (N4 on 512x512 and 2x512x512
-            // images; 3-5% slower on larger grids; other layers, whose tiles
-            // fit three, 12-18% slower): pad its LDS to admit one.
-            if (fused_here && !L.direct && net->ncu > 0 && (long long)L.gx * L.gy <= 12LL * net->ncu &&
-                conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, a.lds_bytes) == 2)
-                a.lds_bytes = std::max(a.lds_bytes, (int)(kMaxLdsBytes / 2 + 1024));
+            if (L.direct) {
+                L.gx = B * F * ((a.out_h * a.out_w + 255) / 256);
+            } else {
+                // grid (a multiple of 8 for the XCD-contiguous tile order)
+                // and dynamic LDS of either tiling; returns the rounds of
+                // workgroups the device needs for it
+                auto finish = [&](int tiles, int &lds, int &gx) {
+                    gx = (tiles + 7) / 8 * 8;
+                    // The FC layer with the fused head, when its register
+                    // tile fits only two workgroups per CU, ran 2-7% faster
+                    // one per CU on grids of at most 12 workgroups per CU
+                    // (N4 on 512x512 and 2x512x512 images; 3-5% slower on
+                    // larger grids; other layers, whose tiles fit three,
+                    // 12-18% slower): pad its LDS to admit one.
+                    if (fused_here && net->ncu > 0 && (long long)gx * L.gy <= 12LL * net->ncu &&
+                        conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, lds) == 2)
+                        lds = std::max(lds, (int)(kMaxLdsBytes / 2 + 1024));
+                    // plan-only nets: 256 CUs, one workgroup each
+                    const int bpc = net->ncu > 0 ? conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn,
+                                                                      L.wk, L.vec, lds) : 1;
+                    const long long slots = (long long)(net->ncu > 0 ? net->ncu : 256) * std::max(bpc, 1);
+                    return ((long long)gx * L.gy + slots - 1) / slots;
+                };
+                int lds = a.lds_bytes, gx = 0;
+                const long long rounds = finish((a.run ? B : B * F) * a.nbands * a.tiles_per_band, lds, gx);
+                if (a.run) {
+                    // Run tiles only where they save a round of workgroups:
+                    // with equal rounds their two-fragment windows cost
+                    // 2% (N4's 3x3 layer on 512 x 512: 1375 run tiles
+                    // against 1536, 6 rounds each); FRAGSCAN_RUN=1 keeps them.
+                    int lds_f = L.frag_lds, gx_f = 0;
+                    const long long rounds_f = finish(B * F * L.frag_tiles, lds_f, gx_f);
+                    const char *e = getenv("FRAGSCAN_RUN");
+                    if (rounds >= rounds_f && !(e && e[0] == '1')) {
+                        a.run = 0;
+                        a.tiles_per_band = L.frag_tiles;
+                        lds = lds_f;
+                        gx = gx_f;
+                    }
+                }
+                a.lds_bytes = lds;
+                L.gx = gx;
+            }
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
             L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
@@ -609,6 +692,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                           (double)l.cin * k * k * l.cout * es;
                 L.name += "+head";
             }
+            if (!L.direct && a.run) L.name += "+run";
         }
         o.is_image = false;
         // kernels address within one fragment (or image) with 32-bit offsets

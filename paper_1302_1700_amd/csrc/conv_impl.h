@@ -179,18 +179,16 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
     }
 }
 
-template <int WN>
-__device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int fy, int fx, int l0, int lend,
-                                                  int twb, int c0, const float *red)
+// locate(m, fy, fx, y, x): fragment (fy, fx) of image b and output (y, x)
+// in it of the tile's pixel m < npix.
+template <int WN, class Locate>
+__device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int npix, Locate locate,
+                                                  const float *red)
 {
     constexpr int NC = kMaxFusedClasses;
     const int ncls = a.head_ncls;
     const int mt = a.mt;
-    const int b = q / a.F;
-    const Div dtw(twb);
-    for (int m = threadIdx.x; m < mt; m += blockDim.x) {
-        const int l = l0 + m;
-        if (l >= lend) break;
+    for (int m = threadIdx.x; m < npix; m += blockDim.x) {
         float z[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -218,9 +216,8 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int q, int 
 #pragma unroll
             for (int c = 0; c < NC; ++c) z[c] = tanhf(z[c]);
         }
-        int y, x;
-        dtw.qr(l, y, x);
-        x += c0;
+        int fy, fx, y, x;
+        locate(m, fy, fx, y, x);
         const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
         float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * ncls;
 #pragma unroll
@@ -245,50 +242,103 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     // 8; the padding tiles exit).
     const int per_xcd = gridDim.x / 8;
     int bid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    if (bid >= a.nfrag * a.nbands * a.tiles_per_band) return;
+    const int nunit = a.run ? a.nfrag / a.F : a.nfrag;  // images (run tiles) or fragments
+    if (bid >= nunit * a.nbands * a.tiles_per_band) return;
     const int t = bid % a.tiles_per_band;
     bid /= a.tiles_per_band;
     const int band = bid % a.nbands;
-    const int q = bid / a.nbands;
 
-    const int rem = q % a.F;
-    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
-    const int hin = a.ext.y[fy], win = a.ext.x[fx];
-    const int hout = hin - a.k + 1, wout = win - a.k + 1;
-    if (hout <= 0 || wout <= 0) return;
-    // The tile's convolution outputs are numbered l in [l0, lend), pixel l at
-    // row l / twb, column c0 + l % twb of the fragment's output.
-    const int c0 = band * a.band_w;
-    int twb, l0, lend;
+    // The tile's convolution outputs: segment 0 numbers them l in [l0, lend),
+    // pixel l at row l / twb, column c0 + l % twb of fragment q's output; a
+    // run tile that reaches the end of its fragment continues with the first
+    // n1 pixels of the next fragment q1 (segment 1, width twb1).
+    int q, fy, fx, l0, lend, twb;
+    int q1 = 0, fy1 = 0, fx1 = 0, n1 = 0, twb1 = 1;
+    int c0 = 0;
     int y0 = 0, rtM = 0, twM = 0;  // fused pool: max-filter rows [y0, y0 + rtM), columns [c0, c0 + twM)
-    if (a.pool_k) {
-        // Section 2.2.2: child (o_x, o_y) of a k x k pool holds the stride-1
-        // k x k max filter M of its parent at (o_y + k*ybar, o_x + k*xbar),
-        // so every filter position y < hout - k + 1 (and likewise x) feeds
-        // exactly one child.  The tile computes the convolution outputs its
-        // filter positions need: k - 1 more rows and columns.
-        const int hM = hout - a.pool_k + 1, wM = wout - a.pool_k + 1;
-        if (hM <= 0 || wM <= 0) return;
-        twM = min(a.band_w, wM - c0);
-        if (twM <= 0) return;
-        y0 = t * a.pool_rt;
-        if (y0 >= hM) return;
-        rtM = min(a.pool_rt, hM - y0);
-        twb = twM + a.pool_k - 1;
-        l0 = y0 * twb;
-        lend = l0 + (rtM + a.pool_k - 1) * twb;
+    int hin, win;
+    if (a.run) {
+        const int b = bid / a.nbands;
+        const int p0 = t * a.mt;
+        if (p0 >= a.run_pix) return;
+        const int np = min(a.mt, a.run_pix - p0);
+        // row of fragments: the last fy with ypre[fy] * wsum <= p0
+        const int v = p0 / a.run_wsum;
+        int lo = 0, hi = a.Q - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int)a.run_ypre[mid] <= v) lo = mid; else hi = mid - 1;
+        }
+        fy = lo;
+        const int ho = a.run_ypre[fy + 1] - a.run_ypre[fy];
+        const int r0 = p0 - (int)a.run_ypre[fy] * a.run_wsum;
+        const int u = r0 / ho;
+        lo = 0;
+        hi = a.Q - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if ((int)a.run_xpre[mid] <= u) lo = mid; else hi = mid - 1;
+        }
+        fx = lo;
+        twb = a.run_xpre[fx + 1] - a.run_xpre[fx];
+        l0 = r0 - ho * (int)a.run_xpre[fx];
+        lend = min(ho * twb, l0 + np);
+        n1 = np - (lend - l0);
+        q = b * a.F + fy * a.Q + fx;
+        if (n1 > 0) {  // every fragment holds at least mt pixels: one more segment at most
+            fy1 = fy;
+            fx1 = fx + 1;
+            if (fx1 == a.Q) {
+                fx1 = 0;
+                ++fy1;
+            }
+            q1 = b * a.F + fy1 * a.Q + fx1;
+            twb1 = a.run_xpre[fx1 + 1] - a.run_xpre[fx1];
+        }
+        hin = a.ext.y[fy];
+        win = a.ext.x[fx];
     } else {
-        twb = min(a.band_w, wout - c0);
-        if (twb <= 0) return;
-        const int npix = hout * twb;
-        l0 = t * a.mt;
-        if (l0 >= npix) return;
-        lend = min(l0 + a.mt, npix);
+        q = bid / a.nbands;
+        const int rem = q % a.F;
+        fy = rem / a.Q;
+        fx = rem - (rem / a.Q) * a.Q;
+        hin = a.ext.y[fy];
+        win = a.ext.x[fx];
+        const int hout = hin - a.k + 1, wout = win - a.k + 1;
+        if (hout <= 0 || wout <= 0) return;
+        c0 = band * a.band_w;
+        if (a.pool_k) {
+            // Section 2.2.2: child (o_x, o_y) of a k x k pool holds the stride-1
+            // k x k max filter M of its parent at (o_y + k*ybar, o_x + k*xbar),
+            // so every filter position y < hout - k + 1 (and likewise x) feeds
+            // exactly one child.  The tile computes the convolution outputs its
+            // filter positions need: k - 1 more rows and columns.
+            const int hM = hout - a.pool_k + 1, wM = wout - a.pool_k + 1;
+            if (hM <= 0 || wM <= 0) return;
+            twM = min(a.band_w, wM - c0);
+            if (twM <= 0) return;
+            y0 = t * a.pool_rt;
+            if (y0 >= hM) return;
+            rtM = min(a.pool_rt, hM - y0);
+            twb = twM + a.pool_k - 1;
+            l0 = y0 * twb;
+            lend = l0 + (rtM + a.pool_k - 1) * twb;
+        } else {
+            twb = min(a.band_w, wout - c0);
+            if (twb <= 0) return;
+            const int npix = hout * twb;
+            l0 = t * a.mt;
+            if (l0 >= npix) return;
+            lend = min(l0 + a.mt, npix);
+        }
     }
+    const int n0 = lend - l0;
     const int yfirst = l0 / twb;
     const int ylast = (lend - 1) / twb;
-    const int R = ylast - yfirst + a.k;  // window rows
-    const int Cc = twb + a.k - 1;        // window columns
+    const int R = ylast - yfirst + a.k;                      // window rows of segment 0
+    const int R1 = n1 > 0 ? (n1 - 1) / twb1 + a.k : 0;       // then those of segment 1
+    const int Cc = max(twb, n1 > 0 ? twb1 : 0) + a.k - 1;    // window columns
+    const int hin1 = n1 > 0 ? a.ext.y[fy1] : 0, win1 = n1 > 0 ? a.ext.x[fx1] : 0;
     const int CS = a.lds_cs;
     const int kk_total = a.ksteps * KSTEP;
 
@@ -296,11 +346,16 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     TC *win_lds = reinterpret_cast<TC *>(smem + (VEC ? 0 : ((kk_total * 4 + 15) & ~15)));
 
     // ---- stage the input window ----------------------------------------------
-    const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * a.in_h * a.in_w * a.in_c;
+    // window rows [0, R) come from fragment q (rows yfirst ..), rows
+    // [R, R + R1) from fragment q1 (rows 0 ..); columns c0 .. of both
+    const size_t fsz = (size_t)a.in_h * a.in_w * a.in_c;
+    const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * fsz;
+    const TI *inp1 = reinterpret_cast<const TI *>(a.in) + (size_t)q1 * fsz;
+    const int RT = R + R1;
     if constexpr (VEC && !IN_F32) {
         // batches of 8 loads in flight per thread before their LDS stores
         const int nvec = a.cin / LPE;
-        const int total = R * Cc * nvec;
+        const int total = RT * Cc * nvec;
         const Div dnv(nvec), dcc(Cc);
         const int rowp = a.in_w * a.in_c;  // elements per input row (fragments stay below 2^31)
         constexpr int UN = 8;
@@ -313,10 +368,12 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 int p, v, r, c;
                 dnv.qr(idx, p, v);
                 dcc.qr(p, r, c);
-                const int gy = yfirst + r, gx = c0 + c;
+                const bool s1 = r >= R;
+                const int gy = s1 ? r - R : yfirst + r, gx = c0 + c;
                 val[u] = u4{0u, 0u, 0u, 0u};
-                if (idx < total && gy < hin && gx < win)
-                    val[u] = *reinterpret_cast<const u4 *>(inp + (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
+                if (idx < total && gy < (s1 ? hin1 : hin) && gx < (s1 ? win1 : win))
+                    val[u] = *reinterpret_cast<const u4 *>((s1 ? inp1 : inp) +
+                                                           (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
                 dsto[u] = idx < total ? __mul24(__mul24(r, Cc) + c, CS) + v * LPE : -1;
             }
 #pragma unroll
@@ -324,17 +381,18 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 if (dsto[u] >= 0) *reinterpret_cast<u4 *>(win_lds + dsto[u]) = val[u];
         }
     } else {
-        const int total = R * Cc * a.cin;
+        const int total = RT * Cc * a.cin;
         const Div dci(a.cin), dcc(Cc);
         const int rowp = a.in_w * a.in_c;
         for (int idx = threadIdx.x; idx < total; idx += 256) {
             int p, ci, r, c;
             dci.qr(idx, p, ci);
             dcc.qr(p, r, c);
-            const int gy = yfirst + r, gx = c0 + c;
+            const bool s1 = r >= R;
+            const int gy = s1 ? r - R : yfirst + r, gx = c0 + c;
             TC val = 0;
-            if (gy < hin && gx < win) {
-                TI x = inp[gy * rowp + __mul24(gx, a.in_c) + ci];
+            if (gy < (s1 ? hin1 : hin) && gx < (s1 ? win1 : win)) {
+                TI x = (s1 ? inp1 : inp)[gy * rowp + __mul24(gx, a.in_c) + ci];
                 if constexpr (BF && IN_F32)
                     val = f2bf(x);
                 else
@@ -370,15 +428,25 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const int lm = lane & 15, g = lane >> 4;
     const int nb0 = blockIdx.y * (WN * NB) + wn * NB;
 
-    const Div dtw(twb);
+    // tile pixel m < npix: segment seg, output row y and column c0 + x of
+    // fragment q (seg 0) or q1 (seg 1; c0 = 0 there)
+    const int npix = n0 + n1;
+    const Div dtw(twb), dtw1(twb1);
+    auto locate = [&](int m, int &seg, int &y, int &x) {
+        seg = m >= n0;
+        if (seg)
+            dtw1.qr(m - n0, y, x);
+        else
+            dtw.qr(l0 + m, y, x);
+    };
     int abase[MB];
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
-        const int l = l0 + (wm * MB + i) * 16 + lm;
-        if (l < lend) {
-            int y, x;
-            dtw.qr(l, y, x);
-            y -= yfirst;
+        const int m = (wm * MB + i) * 16 + lm;
+        if (m < npix) {
+            int seg, y, x;
+            locate(m, seg, y, x);
+            y += seg ? R : -yfirst;
             abase[i] = (y * Cc + x) * CS + g * LPE;
         } else {
             abase[i] = g * LPE;  // any in-window address; the result is not stored
@@ -555,7 +623,16 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         __syncthreads();  // the LDS window / partial sums (which red reuses) are no longer read
         if (wk == 0) fused_head_partials<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, red);
         __syncthreads();
-        fused_head_finish<WN>(a, q, fy, fx, l0, lend, twb, c0, red);
+        fused_head_finish<WN>(
+            a, q / a.F, npix,
+            [&](int m, int &hy, int &hx, int &y, int &x) {
+                int seg;
+                locate(m, seg, y, x);
+                x += c0;
+                hy = seg ? fy1 : fy;
+                hx = seg ? fx1 : fx;
+            },
+            red);
         return;
     }
     // Lane (lm, g) holds, for pixel lm of each m-block, rows 4g .. 4g + 3 of
@@ -706,29 +783,30 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         __syncthreads();  // every wave is done with the window / partial sums
         stage_tile(tile, false);
         __syncthreads();
-        TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout + nbase;
+        const size_t osz = (size_t)a.out_h * a.out_w * a.cout;
+        TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * osz + nbase;
+        TC *outp1 = reinterpret_cast<TC *>(a.out) + (size_t)q1 * osz + nbase;
         const int orow = a.out_w * a.cout;
         const int nch = min(NW, a.cout - nbase);
-        const int npx = lend - l0;
         if ((a.cout % TPAD) == 0 && (nch % TPAD) == 0) {
             const int nv = nch / TPAD;
             const Div dnv(nv);
-            for (int idx = threadIdx.x; idx < npx * nv; idx += 256) {
-                int m, v, y, x;
+            for (int idx = threadIdx.x; idx < npix * nv; idx += 256) {
+                int m, v, seg, y, x;
                 dnv.qr(idx, m, v);
-                dtw.qr(l0 + m, y, x);
+                locate(m, seg, y, x);
                 x += c0;
-                *reinterpret_cast<u4 *>(outp + (y * orow + __mul24(x, a.cout) + v * TPAD)) =
+                *reinterpret_cast<u4 *>((seg ? outp1 : outp) + (y * orow + __mul24(x, a.cout) + v * TPAD)) =
                     *reinterpret_cast<const u4 *>(tile + __mul24(m, TS) + v * TPAD);
             }
         } else {
             const Div dnc(nch);
-            for (int idx = threadIdx.x; idx < npx * nch; idx += 256) {
-                int m, c, y, x;
+            for (int idx = threadIdx.x; idx < npix * nch; idx += 256) {
+                int m, c, seg, y, x;
                 dnc.qr(idx, m, c);
-                dtw.qr(l0 + m, y, x);
+                locate(m, seg, y, x);
                 x += c0;
-                outp[y * orow + __mul24(x, a.cout) + c] = tile[__mul24(m, TS) + c];
+                (seg ? outp1 : outp)[y * orow + __mul24(x, a.cout) + c] = tile[__mul24(m, TS) + c];
             }
         }
         return;
@@ -736,17 +814,19 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 
     // Direct: every lane writes its runs straight from registers.
     if (wk != 0) return;
-    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * a.out_h * a.out_w * a.cout;
+    const size_t osz = (size_t)a.out_h * a.out_w * a.cout;
+    TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * osz;
+    TC *outp1 = reinterpret_cast<TC *>(a.out) + (size_t)q1 * osz;
     const int orow = a.out_w * a.cout;
     const bool full = (a.cout % RUN) == 0;
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
-        const int l = l0 + (wm * MB + i) * 16 + lm;
-        if (l >= lend) continue;
-        int y, x;
-        dtw.qr(l, y, x);
+        const int m = (wm * MB + i) * 16 + lm;
+        if (m >= npix) continue;
+        int seg, y, x;
+        locate(m, seg, y, x);
         x += c0;
-        TC *px = outp + (y * orow + __mul24(x, a.cout));
+        TC *px = (seg ? outp1 : outp) + (y * orow + __mul24(x, a.cout));
         if constexpr (PAIRED) {
 #pragma unroll
             for (int p = 0; p < NB / 2; ++p) {

@@ -63,6 +63,16 @@ struct ConvArgs {
     // stride-1 max filter's columns, and a tile is pool_rt filter rows plus
     // the k - 1 rows and columns of convolution outputs they also need.
     int pool_k, pool_rt, pool_oh, pool_ow;
+    // Run tiles (run > 0; layers whose fragments each fit one band and hold
+    // at least mt output pixels): per image the fragments' output pixels are
+    // numbered in fragment order, fragment (fy, fx) holding
+    // [ypre[fy] * wsum + ho[fy] * xpre[fx], ... + ho[fy] * wo[fx]) with ho, wo
+    // its output sizes and ypre / xpre their per-axis prefix sums (wsum =
+    // xpre[Q]); a tile is mt consecutive pixels of that sequence, so it may
+    // end in one fragment and continue in the next.  tiles_per_band is then
+    // tiles per image.
+    int run, run_pix, run_wsum;
+    uint16_t run_ypre[kMaxAxis + 1], run_xpre[kMaxAxis + 1];
     AxisTable ext;        // true sizes of the input fragments
     // Fused last layer (head_ncls > 0): the 1x1 layer cout -> head_ncls, its
     // activation, and the reassembly are applied in the epilogue, which then

@@ -168,6 +168,48 @@ def test_border_plans():
     net.close()
 
 
+RUN_NET = [wl.conv(3, 3, 32), wl.conv(2, 32, 64), wl.pool(2, 64), wl.conv(2, 64, 40),
+           wl.conv(1, 40, 18), wl.pool(2, 18), wl.fc(2, 18, 24), wl.fc(1, 24, 3, "softmax")]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_run_tile_plans(monkeypatch, dt):
+    """One-band layers whose fragments all hold a tile's worth of outputs
+    can take run tiles (named +run): the split-K vector layer at the smaller
+    image, the gather layer with the fused head at the larger one (pools not
+    fused); FRAGSCAN_RUN=1 keeps them wherever they fit, =0 turns them off,
+    and a run launch needs no more workgroups than per-fragment tiles."""
+    w0 = ix.patch_size(RUN_NET)
+    cases = (((w0 + 41, w0 + 29), "", {3}), ((w0 + 90, w0 + 77), "0", {6}))
+    for (H, W), fuse, want in cases:
+        monkeypatch.setenv("FRAGSCAN_POOL_FUSE", fuse)
+        monkeypatch.setenv("FRAGSCAN_RUN", "1")
+        net = _plan_net(RUN_NET, c0=3, dtype=dt)
+        on = net.launches(2, H, W)
+        monkeypatch.setenv("FRAGSCAN_RUN", "0")
+        off = net.launches(2, H, W)
+        net.close()
+        assert {L["layer"] for L in on if L["name"].endswith("+run")} == want
+        assert not any("+run" in L["name"] for L in off)
+        for a, b in zip(on, off):
+            assert a["out_pixels"] == b["out_pixels"] and a["flops"] == b["flops"]
+            if a["layer"] in want:
+                assert a["grid"] <= b["grid"]
+
+
+def test_run_tiles_where_they_save_a_round(monkeypatch):
+    """By default run tiles are kept only where they need fewer rounds of
+    workgroups (plan-only nets count 256 CUs, one workgroup each): N4's 3x3
+    layer with the fused head on 448 x 448 (1280 per-fragment tiles, 980 run
+    tiles) but not on 512 x 512 (1536 against 1375: six rounds either way)."""
+    monkeypatch.delenv("FRAGSCAN_RUN", raising=False)
+    net = _plan_net(wl.WORKLOADS[2].layers)
+    fc = {H: [L for L in net.launches(1, H, H) if L["layer"] == 8][0] for H in (448, 512)}
+    net.close()
+    assert fc[448]["name"].endswith("+head+run") and fc[448]["grid"] == 984
+    assert fc[512]["name"].endswith("+head") and fc[512]["grid"] == 1536
+
+
 def test_border_mode_rejected_when_unknown():
     net = _plan_net(wl.WORKLOADS[1].layers)
     p = fsb.fs_plan_info()

@@ -435,6 +435,29 @@ def test_store_modes(fsb, monkeypatch, store, dt):
     assert np.abs(got - ref).max() <= TOL[dt]
 
 
+@pytest.mark.parametrize("big", [False, True])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_run_tiles(fsb, monkeypatch, dt, big):
+    """Run tiles (a tile continues into the next fragment) give the same
+    values as one tile sequence per fragment, bit for bit: the split-K vector
+    layer on the smaller image, the gather layer with the fused head on the
+    larger (pools not fused there); two images of ragged fragments."""
+    layers = [wl.conv(3, 3, 32), wl.conv(2, 32, 64), wl.pool(2, 64), wl.conv(2, 64, 40),
+              wl.conv(1, 40, 18), wl.pool(2, 18), wl.fc(2, 18, 24), wl.fc(1, 24, 3, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 21, 0.2)
+    H, W = (w0 + 90, w0 + 77) if big else (w0 + 41, w0 + 29)
+    img = wl.make_image(22, 2, H, W, 3)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "0" if big else "")
+    monkeypatch.setenv("FRAGSCAN_RUN", "1")
+    run = _scan(fsb, layers, params, img, 3, dtype=dt)
+    monkeypatch.setenv("FRAGSCAN_RUN", "0")
+    per_frag = _scan(fsb, layers, params, img, 3, dtype=dt)
+    assert np.array_equal(run, per_frag)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    assert np.abs(run - ref).max() <= TOL[dt]
+
+
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
 def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     """Small-K layers take either the per-pixel vector-ALU kernel or the
