@@ -264,6 +264,7 @@ void plan_run_tiles(const NetLayer &l, const Geo &in, int mt, int cs, int es, in
                     Launch &L)
 {
     if (const char *e = getenv("FRAGSCAN_RUN"); e && e[0] == '0') return;
+    if (!conv_tile_supported(L.mb, l.nb, l.wn, l.wk, l.vec, true)) return;
     const int k = l.k;
     if (in.Q > kMaxAxis) return;
     long long sy = 0, sx = 0;
@@ -609,7 +610,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                 // grid (a multiple of 8 for the XCD-contiguous tile order)
                 // and dynamic LDS of either tiling; returns the rounds of
                 // workgroups the device needs for it
-                auto finish = [&](int tiles, int &lds, int &gx) {
+                auto finish = [&](bool run, int tiles, int &lds, int &gx) {
                     gx = (tiles + 7) / 8 * 8;
                     // The FC layer with the fused head, when its register
                     // tile fits only two workgroups per CU, ran 2-7% faster
@@ -618,23 +619,23 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                     // larger grids; other layers, whose tiles fit three,
                     // 12-18% slower): pad its LDS to admit one.
                     if (fused_here && net->ncu > 0 && (long long)gx * L.gy <= 12LL * net->ncu &&
-                        conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, lds) == 2)
+                        conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, run, lds) == 2)
                         lds = std::max(lds, (int)(kMaxLdsBytes / 2 + 1024));
                     // plan-only nets: 256 CUs, one workgroup each
                     const int bpc = net->ncu > 0 ? conv_blocks_per_cu(net->dtype, g.is_image, L.mb, L.nb, L.wn,
-                                                                      L.wk, L.vec, lds) : 1;
+                                                                      L.wk, L.vec, run, lds) : 1;
                     const long long slots = (long long)(net->ncu > 0 ? net->ncu : 256) * std::max(bpc, 1);
                     return ((long long)gx * L.gy + slots - 1) / slots;
                 };
                 int lds = a.lds_bytes, gx = 0;
-                const long long rounds = finish((a.run ? B : B * F) * a.nbands * a.tiles_per_band, lds, gx);
+                const long long rounds = finish(a.run, (a.run ? B : B * F) * a.nbands * a.tiles_per_band, lds, gx);
                 if (a.run) {
                     // Run tiles only where they save a round of workgroups:
                     // with equal rounds their two-fragment windows cost
                     // 2% (N4's 3x3 layer on 512 x 512: 1375 run tiles
                     // against 1536, 6 rounds each); FRAGSCAN_RUN=1 keeps them.
                     int lds_f = L.frag_lds, gx_f = 0;
-                    const long long rounds_f = finish(B * F * L.frag_tiles, lds_f, gx_f);
+                    const long long rounds_f = finish(false, B * F * L.frag_tiles, lds_f, gx_f);
                     const char *e = getenv("FRAGSCAN_RUN");
                     if (rounds >= rounds_f && !(e && e[0] == '1')) {
                         a.run = 0;
@@ -652,7 +653,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
                       (double)l.cin * k * k * l.cout * es;
             L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, k)
-                              : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec);
+                              : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, a.run);
             if (pool_fuse) {
                 const int kp = net->L[li + 1].k;
                 if (g.Q * kp > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);

@@ -14,11 +14,11 @@ hipError_t launch_conv_bf16(const ConvArgs &a, bool in_f32, int mb, int nb, int 
                : conv::dispatch_tile<true, false, false>(a, mb, nb, wn, wk, gx, gy, s);
 }
 
-int conv_blocks_per_cu_bf16(bool in_f32, int mb, int nb, int wn, int wk, bool vec, int lds)
+int conv_blocks_per_cu_bf16(bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run, int lds)
 {
-    if (in_f32) return vec ? 0 : conv::tile_blocks_per_cu<true, true, false>(mb, nb, wn, wk, lds);
-    return vec ? conv::tile_blocks_per_cu<true, false, true>(mb, nb, wn, wk, lds)
-               : conv::tile_blocks_per_cu<true, false, false>(mb, nb, wn, wk, lds);
+    if (in_f32) return vec ? 0 : conv::tile_blocks_per_cu<true, true, false>(mb, nb, wn, wk, run, lds);
+    return vec ? conv::tile_blocks_per_cu<true, false, true>(mb, nb, wn, wk, run, lds)
+               : conv::tile_blocks_per_cu<true, false, false>(mb, nb, wn, wk, run, lds);
 }
 
 }  // namespace fs

@@ -226,7 +226,9 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
     }
 }
 
-template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC>
+// RUN: run tiles (ConvArgs::run = 1, no fused pool); the other instances
+// take one band of one fragment per tile sequence.
+template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC, bool RUN>
 __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 {
     using TC = typename Elem<BF>::T;                                // LDS / operand element
@@ -242,7 +244,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     // 8; the padding tiles exit).
     const int per_xcd = gridDim.x / 8;
     int bid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
-    const int nunit = a.run ? a.nfrag / a.F : a.nfrag;  // images (run tiles) or fragments
+    const int nunit = RUN ? a.nfrag / a.F : a.nfrag;  // images (run tiles) or fragments
     if (bid >= nunit * a.nbands * a.tiles_per_band) return;
     const int t = bid % a.tiles_per_band;
     bid /= a.tiles_per_band;
@@ -257,7 +259,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     int c0 = 0;
     int y0 = 0, rtM = 0, twM = 0;  // fused pool: max-filter rows [y0, y0 + rtM), columns [c0, c0 + twM)
     int hin, win;
-    if (a.run) {
+    if constexpr (RUN) {
         const int b = bid / a.nbands;
         const int p0 = t * a.mt;
         if (p0 >= a.run_pix) return;
@@ -351,56 +353,58 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const size_t fsz = (size_t)a.in_h * a.in_w * a.in_c;
     const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * fsz;
     const TI *inp1 = reinterpret_cast<const TI *>(a.in) + (size_t)q1 * fsz;
-    const int RT = R + R1;
-    if constexpr (VEC && !IN_F32) {
-        // batches of 8 loads in flight per thread before their LDS stores
-        const int nvec = a.cin / LPE;
-        const int total = RT * Cc * nvec;
-        const Div dnv(nvec), dcc(Cc);
+    // nrows window rows from row row0 on: rows gy0 .. of fragment src, whose
+    // true size is hh x ww (outside it, zeros)
+    auto stage = [&](const TI *src, int gy0, int hh, int ww, int row0, int nrows) {
         const int rowp = a.in_w * a.in_c;  // elements per input row (fragments stay below 2^31)
-        constexpr int UN = 8;
-        for (int base = threadIdx.x; base < total; base += 256 * UN) {
-            u4 val[UN];
-            int dsto[UN];
+        if constexpr (VEC && !IN_F32) {
+            // batches of 8 loads in flight per thread before their LDS stores
+            const int nvec = a.cin / LPE;
+            const int total = nrows * Cc * nvec;
+            const Div dnv(nvec), dcc(Cc);
+            constexpr int UN = 8;
+            for (int base = threadIdx.x; base < total; base += 256 * UN) {
+                u4 val[UN];
+                int dsto[UN];
 #pragma unroll
-            for (int u = 0; u < UN; ++u) {
-                const int idx = base + u * 256;
-                int p, v, r, c;
-                dnv.qr(idx, p, v);
+                for (int u = 0; u < UN; ++u) {
+                    const int idx = base + u * 256;
+                    int p, v, r, c;
+                    dnv.qr(idx, p, v);
+                    dcc.qr(p, r, c);
+                    const int gy = gy0 + r, gx = c0 + c;
+                    val[u] = u4{0u, 0u, 0u, 0u};
+                    if (idx < total && gy < hh && gx < ww)
+                        val[u] = *reinterpret_cast<const u4 *>(src + (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
+                    dsto[u] = idx < total ? __mul24(__mul24(row0 + r, Cc) + c, CS) + v * LPE : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < UN; ++u)
+                    if (dsto[u] >= 0) *reinterpret_cast<u4 *>(win_lds + dsto[u]) = val[u];
+            }
+        } else {
+            const int total = nrows * Cc * a.cin;
+            const Div dci(a.cin), dcc(Cc);
+            for (int idx = threadIdx.x; idx < total; idx += 256) {
+                int p, ci, r, c;
+                dci.qr(idx, p, ci);
                 dcc.qr(p, r, c);
-                const bool s1 = r >= R;
-                const int gy = s1 ? r - R : yfirst + r, gx = c0 + c;
-                val[u] = u4{0u, 0u, 0u, 0u};
-                if (idx < total && gy < (s1 ? hin1 : hin) && gx < (s1 ? win1 : win))
-                    val[u] = *reinterpret_cast<const u4 *>((s1 ? inp1 : inp) +
-                                                           (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
-                dsto[u] = idx < total ? __mul24(__mul24(r, Cc) + c, CS) + v * LPE : -1;
+                const int gy = gy0 + r, gx = c0 + c;
+                TC val = 0;
+                if (gy < hh && gx < ww) {
+                    TI x = src[gy * rowp + __mul24(gx, a.in_c) + ci];
+                    if constexpr (BF && IN_F32)
+                        val = f2bf(x);
+                    else
+                        val = x;
+                }
+                win_lds[__mul24(__mul24(row0 + r, Cc) + c, CS) + ci] = val;
             }
-#pragma unroll
-            for (int u = 0; u < UN; ++u)
-                if (dsto[u] >= 0) *reinterpret_cast<u4 *>(win_lds + dsto[u]) = val[u];
         }
-    } else {
-        const int total = RT * Cc * a.cin;
-        const Div dci(a.cin), dcc(Cc);
-        const int rowp = a.in_w * a.in_c;
-        for (int idx = threadIdx.x; idx < total; idx += 256) {
-            int p, ci, r, c;
-            dci.qr(idx, p, ci);
-            dcc.qr(p, r, c);
-            const bool s1 = r >= R;
-            const int gy = s1 ? r - R : yfirst + r, gx = c0 + c;
-            TC val = 0;
-            if (gy < (s1 ? hin1 : hin) && gx < (s1 ? win1 : win)) {
-                TI x = (s1 ? inp1 : inp)[gy * rowp + __mul24(gx, a.in_c) + ci];
-                if constexpr (BF && IN_F32)
-                    val = f2bf(x);
-                else
-                    val = x;
-            }
-            win_lds[__mul24(__mul24(r, Cc) + c, CS) + ci] = val;
-        }
-    }
+    };
+    stage(inp, yfirst, hin, win, 0, R);
+    if constexpr (RUN)
+        if (R1 > 0) stage(inp1, 0, hin1, win1, R, R1);
     if constexpr (!VEC) {
         const Div dci(a.cin), dk(a.k);
         for (int kk = threadIdx.x; kk < kk_total; kk += 256) {
@@ -433,7 +437,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const int npix = n0 + n1;
     const Div dtw(twb), dtw1(twb1);
     auto locate = [&](int m, int &seg, int &y, int &x) {
-        seg = m >= n0;
+        seg = RUN && m >= n0;
         if (seg)
             dtw1.qr(m - n0, y, x);
         else
@@ -443,13 +447,23 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int m = (wm * MB + i) * 16 + lm;
-        if (m < npix) {
-            int seg, y, x;
-            locate(m, seg, y, x);
-            y += seg ? R : -yfirst;
-            abase[i] = (y * Cc + x) * CS + g * LPE;
+        if (m < n0) {
+            int y, x;
+            dtw.qr(l0 + m, y, x);
+            abase[i] = ((y - yfirst) * Cc + x) * CS + g * LPE;
         } else {
             abase[i] = g * LPE;  // any in-window address; the result is not stored
+        }
+    }
+    if (RUN && n1 > 0) {
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            const int m = (wm * MB + i) * 16 + lm;
+            if (m >= n0 && m < npix) {
+                int y, x;
+                dtw1.qr(m - n0, y, x);
+                abase[i] = ((y + R) * Cc + x) * CS + g * LPE;
+            }
         }
     }
 
@@ -643,7 +657,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const bool act_tanh = a.act == ACT_TANH;
     auto act = [&](float v) { return act_tanh ? tanh_fast(v) : v; };
     constexpr bool PAIRED = BF && (NB % 2) == 0;
-    constexpr int RUN = PAIRED ? 8 : 4;  // consecutive channels per lane and block (pair)
+    constexpr int CRUN = PAIRED ? 8 : 4;  // consecutive channels per lane and block (pair)
     f4 bv[NB];
 #pragma unroll
     for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
@@ -699,7 +713,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
     };
 
-    if (a.pool_k) {
+    if (!RUN && a.pool_k) {
         // Fused k x k pool (the workgroup owns every channel): the filter
         // value at fragment position (y, x) = (y0 + r, c0 + c) is the
         // maximum over the tile's k x k outputs from (r, c), and goes to
@@ -818,7 +832,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     TC *outp = reinterpret_cast<TC *>(a.out) + (size_t)q * osz;
     TC *outp1 = reinterpret_cast<TC *>(a.out) + (size_t)q1 * osz;
     const int orow = a.out_w * a.cout;
-    const bool full = (a.cout % RUN) == 0;
+    const bool full = (a.cout % CRUN) == 0;
 #pragma unroll
     for (int i = 0; i < MB; ++i) {
         const int m = (wm * MB + i) * 16 + lm;
@@ -882,10 +896,10 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     }
 }
 
-template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC>
+template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC, bool RUN>
 hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
 {
-    auto kern = conv_frag_mfma<MB, NB, WN, WK, BF, IN_F32, VEC>;
+    auto kern = conv_frag_mfma<MB, NB, WN, WK, BF, IN_F32, VEC, RUN>;
     if (a.lds_bytes > 65536) {
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
@@ -911,46 +925,74 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
 #define FS_CONV_TILES_GATHER(X)                                                                 \
     X(1, 1, 1, 1) X(1, 2, 1, 1) X(1, 3, 1, 1) X(1, 4, 1, 1) X(2, 1, 1, 1) X(2, 2, 1, 1)          \
     X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 1) X(4, 4, 1, 1)
+// ... and with run tiles (a subset: those one-band layers take)
+#define FS_CONV_TILES_RUN_VEC(X)                                                                \
+    X(2, 2, 1, 1) X(2, 4, 1, 1) X(2, 7, 1, 1) X(2, 13, 1, 1) X(4, 2, 1, 1) X(4, 3, 1, 2)         \
+    X(4, 4, 1, 1) X(4, 7, 2, 1)
+#define FS_CONV_TILES_RUN_GATHER(X) \
+    X(2, 1, 1, 1) X(2, 2, 1, 1) X(2, 3, 1, 1) X(2, 4, 1, 1) X(4, 1, 1, 1) X(4, 2, 1, 1)
 
 // Workgroups of one tile shape that fit on a CU with `lds` dynamic LDS bytes
-// (0 if unknown): a 256-thread workgroup puts one wave on each of the 4
-// SIMDs, each SIMD holds 512 VGPRs per lane (allocated in granules of 8),
-// and the CU has kMaxLdsBytes of LDS.
+// (0 if unknown or the shape has no instance): a 256-thread workgroup
+// puts one wave on each of the 4 SIMDs, each SIMD holds 512 VGPRs per lane
+// (allocated in granules of 8), and the CU has kMaxLdsBytes of LDS.
 template <bool BF, bool IN_F32, bool VEC>
-int tile_blocks_per_cu(int mb, int nb, int wn, int wk, int lds)
+int tile_blocks_per_cu(int mb, int nb, int wn, int wk, bool run, int lds)
 {
-#define FS_CONV_OCC(M, N, W, K)                                                                          \
-    if (mb == M && nb == N && wn == W && wk == K) {                                                      \
-        hipFuncAttributes fa{};                                                                          \
-        if (hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(conv_frag_mfma<M, N, W, K, BF, IN_F32, VEC>)) != hipSuccess) { \
-            (void)hipGetLastError();                                                                     \
-            return 0;                                                                                    \
-        }                                                                                                \
-        const int regs = (fa.numRegs + 7) / 8 * 8;                                                       \
-        int n = regs > 0 ? 512 / regs : 8;                                                               \
-        if (lds > 0) n = std::min(n, (int)(kMaxLdsBytes / (size_t)lds));                                 \
-        return std::min(n, 8);                                                                           \
-    }
-    if constexpr (VEC) {
-        FS_CONV_TILES_VEC(FS_CONV_OCC)
+    const void *kern = nullptr;
+#define FS_CONV_OCC(M, N, W, K) \
+    if (mb == M && nb == N && wn == W && wk == K) kern = reinterpret_cast<const void *>(conv_frag_mfma<M, N, W, K, BF, IN_F32, VEC, false>);
+#define FS_CONV_OCC_RUN(M, N, W, K) \
+    if (mb == M && nb == N && wn == W && wk == K) kern = reinterpret_cast<const void *>(conv_frag_mfma<M, N, W, K, BF, IN_F32, VEC, true>);
+    if (run) {
+        if constexpr (VEC) {
+            FS_CONV_TILES_RUN_VEC(FS_CONV_OCC_RUN)
+        } else {
+            FS_CONV_TILES_RUN_GATHER(FS_CONV_OCC_RUN)
+        }
     } else {
-        FS_CONV_TILES_GATHER(FS_CONV_OCC)
+        if constexpr (VEC) {
+            FS_CONV_TILES_VEC(FS_CONV_OCC)
+        } else {
+            FS_CONV_TILES_GATHER(FS_CONV_OCC)
+        }
     }
 #undef FS_CONV_OCC
-    return 0;
+#undef FS_CONV_OCC_RUN
+    if (!kern) return 0;
+    hipFuncAttributes fa{};
+    if (hipFuncGetAttributes(&fa, kern) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    const int regs = (fa.numRegs + 7) / 8 * 8;
+    int n = regs > 0 ? 512 / regs : 8;
+    if (lds > 0) n = std::min(n, (int)(kMaxLdsBytes / (size_t)lds));
+    return std::min(n, 8);
 }
 
 template <bool BF, bool IN_F32, bool VEC>
 hipError_t dispatch_tile(const ConvArgs &a, int mb, int nb, int wn, int wk, int gx, int gy, hipStream_t s)
 {
 #define FS_CONV_CASE(M, N, W, K) \
-    if (mb == M && nb == N && wn == W && wk == K) return launch_one<M, N, W, K, BF, IN_F32, VEC>(a, gx, gy, s);
-    if constexpr (VEC) {
-        FS_CONV_TILES_VEC(FS_CONV_CASE)
+    if (mb == M && nb == N && wn == W && wk == K) return launch_one<M, N, W, K, BF, IN_F32, VEC, false>(a, gx, gy, s);
+#define FS_CONV_CASE_RUN(M, N, W, K) \
+    if (mb == M && nb == N && wn == W && wk == K) return launch_one<M, N, W, K, BF, IN_F32, VEC, true>(a, gx, gy, s);
+    if (a.run) {
+        if constexpr (VEC) {
+            FS_CONV_TILES_RUN_VEC(FS_CONV_CASE_RUN)
+        } else {
+            FS_CONV_TILES_RUN_GATHER(FS_CONV_CASE_RUN)
+        }
     } else {
-        FS_CONV_TILES_GATHER(FS_CONV_CASE)
+        if constexpr (VEC) {
+            FS_CONV_TILES_VEC(FS_CONV_CASE)
+        } else {
+            FS_CONV_TILES_GATHER(FS_CONV_CASE)
+        }
     }
 #undef FS_CONV_CASE
+#undef FS_CONV_CASE_RUN
     return hipErrorInvalidValue;
 }
 

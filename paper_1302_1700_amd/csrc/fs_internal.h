@@ -114,7 +114,7 @@ struct HeadArgs {
 // operand type; `in_f32` says the input is float32 even in a bf16 net (the
 // image).  Convolution register tiles: mb pixel blocks x nb channel blocks per
 // wave, wn waves across the output channels, wk waves splitting the K steps,
-// 4 / (wn * wk) across the pixels.
+// 4 / (wn * wk) across the pixels.  a.run picks the run-tile instance.
 hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec,
                        int grid_x, int grid_y, hipStream_t s);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
@@ -125,10 +125,11 @@ hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, i
                              int mode, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
-bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec);
+// Whether a tile shape has an instance (run: one with run tiles).
+bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec, bool run = false);
 // Workgroups of that convolution kernel resident per CU with `lds` bytes of
 // dynamic LDS, on the current device (0 if the query fails).
-int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, int lds);
+int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run, int lds);
 // Direct (vector-ALU) convolution for tiny K = c_in * k * k (<= 64) and
 // c_out <= 48; wpk = weights as [rows][KP] float32 with rows = c_out rounded
 // up to 8 (zero rows past c_out), K index (dy * k + dx) * c_in + ci, zero
@@ -140,7 +141,7 @@ hipError_t launch_conv_direct(const ConvArgs &a, const float *wpk, int dtype, bo
 std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int k);
 
 // Kernel names as the profiler reports them (for measurement reports).
-std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec);
+std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run);
 const char *pool_kernel_name(int dtype, bool in_f32);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
