@@ -79,6 +79,8 @@ struct fs_net {
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
     size_t head_wp_off = 0;   // head weights in the previous layer's (block, row) order
+    size_t head_wbf_off = 0;  // ... as bf16 row operands (ConvArgs::head_wbf), bf16 nets with paired blocks
+    bool has_head_wbf = false;
     int ncu = 0;              // compute units of the device (0: plan-only net)
     int head_cin = 0;
     void *d_mem = nullptr;
@@ -670,6 +672,8 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             }
             if (fuse && li == body - 1) {
                 const NetLayer &hl = net->L[nl - 1];
+                if (net->dtype == DT_BF16 && L.nb % 2 == 0 && !net->has_head_wbf)
+                    return fail(FS_ERR_UNSUPPORTED, "layer %d: no bf16 head operands for the fused head", li);
                 a.head_ncls = net->ncls;
                 a.head_act = hl.act;
                 a.ny = P.ny;
@@ -831,6 +835,7 @@ hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_ou
         L.conv.bias = reinterpret_cast<const float *>(mem + l.b_off);
         if (L.conv.head_ncls > 0) {
             L.conv.head_w = reinterpret_cast<const float *>(mem + net->head_wp_off);
+            L.conv.head_wbf = net->has_head_wbf ? mem + net->head_wbf_off : nullptr;
             L.conv.head_b = reinterpret_cast<const float *>(mem + net->head_b_off);
             L.conv.head_out = d_out;
             L.conv.out = nullptr;
@@ -1012,6 +1017,18 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
                         if (ci < l.cin) wp[(size_t)c * pl.nbt * 16 + r] = w[(size_t)c * l.cin + ci];
                     }
                 net->head_wp_off = push(wp.data(), wp.size() * 4);
+                if (dtype == DT_BF16 && pl.nb % 2 == 0) {
+                    std::vector<uint16_t> wb((size_t)pl.nbt / 2 * 64 * 8, 0);
+                    for (int P = 0; P < pl.nbt / 2; ++P)
+                        for (int lane = 0; lane < 64; ++lane)
+                            for (int e = 0; e < 8; ++e) {
+                                const int c = lane % 16, ci = 32 * P + 8 * (lane / 16) + e;
+                                if (c < l.cout && ci < l.cin)
+                                    wb[((size_t)P * 64 + lane) * 8 + e] = host_f2bf(w[(size_t)c * l.cin + ci]);
+                            }
+                    net->head_wbf_off = push(wb.data(), wb.size() * 2);
+                    net->has_head_wbf = true;
+                }
             }
             continue;
         }

@@ -125,50 +125,92 @@ struct Elem<true> {
 // registers: every lane multiplies its values (rows 4g .. 4g + 3 of each
 // channel block, for pixel lm of each m-block) by the last layer's weights
 // (stored over the same (block, row) order), the four lanes of a pixel add up
-// with xor shuffles (fused_head_partials); the waves that split the channels
+// with xor shuffles (fused_head_partials; bf16 tiles with paired blocks use a
+// matrix-core product per block pair instead); the waves that split the channels
 // add up through LDS and one thread per pixel applies the last activation
 // (softmax: exp(z - max z) / sum) and writes the pixel's classes to the dense
 // map at the window corner the pixel stands for: final fragment (fy, fx)
 // position (y, x) holds window (base[fy] + S*y, base[fx] + S*x)
 // (fused_head_finish).  A workgroup barrier separates the two.
-template <int MB, int NB, int WN>
+template <int MB, int NB, int WN, bool BF>
 __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm,
                                                     int wn, int lm, int g, float *red)
 {
     constexpr int NC = kMaxFusedClasses;
-    const int ldw = a.nbt * 16;
     float part[MB][NC];
+    if constexpr (BF && NB % 2 == 0) {
+        // bf16 with paired blocks: the activations, rounded to bf16 as the
+        // layer would store them, are the column operand of one 16x16x32
+        // product per block pair against the class weights (rows = classes):
+        // lane (lm, g) supplies pixel lm's channels 8g .. 8g + 7 of the pair
+        // and ends with classes 4g .. 4g + 3 of pixel lm.
+        const u4 *hw = reinterpret_cast<const u4 *>(a.head_wbf) + (size_t)(nb0 / 2) * 64 + g * 16 + lm;
+        f4 hacc[MB];
 #pragma unroll
-    for (int i = 0; i < MB; ++i)
+        for (int i = 0; i < MB; ++i) hacc[i] = f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NC; ++c) part[i][c] = 0.f;
+        for (int p = 0; p < NB / 2; ++p) {
+            const u4 wv = hw[p * 64];
+            const f4 b0 = *reinterpret_cast<const f4 *>(a.bias + (nb0 + 2 * p) * 16 + 4 * g);
+            const f4 b1 = *reinterpret_cast<const f4 *>(a.bias + (nb0 + 2 * p + 1) * 16 + 4 * g);
 #pragma unroll
-    for (int j = 0; j < NB; ++j) {
-        const int r0 = (nb0 + j) * 16 + 4 * g;  // (block, row) index of element 0
-        const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
-        // (rows past head_ncls are zero on the device: unconditional loads)
-        f4 w2[NC];
+            for (int i = 0; i < MB; ++i) {
+                float h[8];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) w2[c] = *reinterpret_cast<const f4 *>(a.head_w + (size_t)c * ldw + r0);
+                for (int e = 0; e < 4; ++e) {
+                    h[e] = acc[i][2 * p][e] + b0[e];
+                    h[4 + e] = acc[i][2 * p + 1][e] + b1[e];
+                }
+                if (a.act == ACT_TANH) {
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) h[e] = tanh_fast(h[e]);
+                }
+                u4 pk;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) pk[e] = pack_bf16(h[2 * e], h[2 * e + 1]);
+                hacc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, wv), __builtin_bit_cast(bf8, pk),
+                                                                  hacc[i], 0, 0, 0);
+            }
+        }
 #pragma unroll
         for (int i = 0; i < MB; ++i)
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float v = acc[i][j][e] + bv[e];
-                if (a.act == ACT_TANH) v = tanh_fast(v);
+            for (int c = 0; c < NC; ++c) part[i][c] = hacc[i][c];
+    } else {
+        const int ldw = a.nbt * 16;
 #pragma unroll
-                for (int c = 0; c < NC; ++c) part[i][c] = fmaf(w2[c][e], v, part[i][c]);
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) part[i][c] = 0.f;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int r0 = (nb0 + j) * 16 + 4 * g;  // (block, row) index of element 0
+            const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
+            // (rows past head_ncls are zero on the device: unconditional loads)
+            f4 w2[NC];
+#pragma unroll
+            for (int c = 0; c < NC; ++c) w2[c] = *reinterpret_cast<const f4 *>(a.head_w + (size_t)c * ldw + r0);
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float v = acc[i][j][e] + bv[e];
+                    if (a.act == ACT_TANH) v = tanh_fast(v);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) part[i][c] = fmaf(w2[c][e], v, part[i][c]);
+                }
+        }
+        // the four lanes of a pixel hold disjoint channels: add them up
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) {
+                float t = part[i][c];
+                t += __shfl_xor(t, 16);
+                t += __shfl_xor(t, 32);
+                part[i][c] = t;
             }
     }
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            float t = part[i][c];
-            t += __shfl_xor(t, 16);
-            t += __shfl_xor(t, 32);
-            part[i][c] = t;
-        }
     if (g == 0) {
 #pragma unroll
         for (int i = 0; i < MB; ++i) {
@@ -635,7 +677,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     if (a.head_ncls > 0) {
         float *red = reinterpret_cast<float *>(smem);
         __syncthreads();  // the LDS window / partial sums (which red reuses) are no longer read
-        if (wk == 0) fused_head_partials<MB, NB, WN>(a, acc, nb0, wm, wn, lm, g, red);
+        if (wk == 0) fused_head_partials<MB, NB, WN, BF>(a, acc, nb0, wm, wn, lm, g, red);
         __syncthreads();
         fused_head_finish<WN>(
             a, q / a.F, npix,

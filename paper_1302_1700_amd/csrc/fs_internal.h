@@ -79,6 +79,11 @@ struct ConvArgs {
     // writes the dense output map instead of `out`'s fragment batch.
     int head_ncls, head_act;
     const float *head_w;  // [max(head_ncls, kMaxFusedClasses)][nbt * 16], columns in (block, row) order, zero rows past head_ncls
+    // bf16 nets whose tile pairs channel blocks: the same weights as the row
+    // operand of a 16x16x32 bf16 product, [nbt / 2][64 lanes][8 bf16], lane l
+    // holding class l % 16 (zero past head_ncls) at channels
+    // 32 * pair + 8 * (l / 16) .. + 7 (zero past the channels)
+    const void *head_wbf;
     const float *head_b;  // [head_ncls]
     float *head_out;      // [B][ny][nx][head_ncls]
     int ny, nx, S;
