@@ -780,32 +780,81 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             return reinterpret_cast<TC *>(a.out) + (qc * child_px + (size_t)ybar * a.pool_ow + xbar) * a.cout;
         };
         if ((a.cout % TPAD) == 0) {
+            // A thread owns one 16-byte channel chunk v of one filter column
+            // c and walks a run of consecutive filter rows, so its LDS source
+            // and child addresses only advance: a row down in the tile, and
+            // the next child row (o_y + 1, or o_y = 0 and ybar + 1).  With
+            // fewer (column, chunk) pairs than threads the rows are shared
+            // out as well.
             const int nv = a.cout / TPAD;
-            const Div dnv(nv);
-            const int total = rtM * twM * nv;
-            for (int idx = threadIdx.x; idx < total; idx += 256) {
-                int p, v, r, c;
-                dnv.qr(idx, p, v);
-                dtm.qr(p, r, c);
-                const TC *src = tile + __mul24(__mul24(r, ew) + c, TS) + v * TPAD;
-                u4 m = *reinterpret_cast<const u4 *>(src);
-                for (int i = 0; i < kp; ++i)
-                    for (int j = 0; j < kp; ++j) {
-                        const u4 x = *reinterpret_cast<const u4 *>(src + __mul24(__mul24(i, ew) + j, TS));
+            const int items = twM * nv;
+            const int nrg = max(1, 256 / items);   // row runs per (column, chunk)
+            const int rpt = (rtM + nrg - 1) / nrg;  // rows per run
+            const Div dit(items), dnv(nv);
+            const long long d_oy = (long long)Qc * child_px * a.cout;  // next o_y: the child Qc fragments on
+            const long long d_yb = (long long)a.pool_ow * a.cout;      // next ybar
+            auto walk = [&](auto kc) {
+                constexpr int KC = decltype(kc)::value;  // pool size if known here, else 0
+                const int K = KC ? KC : kp;
+                for (int w = threadIdx.x; w < items * nrg; w += 256) {
+                    int rg, it, c, v;
+                    dit.qr(w, rg, it);
+                    dnv.qr(it, c, v);
+                    const int r0 = rg * rpt, r1 = min(r0 + rpt, rtM);
+                    if (r0 >= r1) continue;
+                    int ybar, oy;
+                    dkp.qr(y0 + r0, ybar, oy);
+                    TC *dst = child_ptr(r0, c) + v * TPAD;
+                    const TC *src = tile + __mul24(__mul24(r0, ew) + c, TS) + v * TPAD;
+                    for (int r = r0; r < r1; ++r) {
+                        u4 m = *reinterpret_cast<const u4 *>(src);
+                        auto tap = [&](int ii, int jj) {
+                            const u4 x = *reinterpret_cast<const u4 *>(src + __mul24(__mul24(ii, ew) + jj, TS));
 #pragma unroll
-                        for (int e = 0; e < 4; ++e) {
-                            if constexpr (BF)
-                                m[e] = max_i16x2(m[e], x[e]);
-                            else
-                                m[e] = __float_as_uint(fmaxf(__uint_as_float(m[e]), __uint_as_float(x[e])));
+                            for (int e = 0; e < 4; ++e) {
+                                if constexpr (BF)
+                                    m[e] = max_i16x2(m[e], x[e]);
+                                else
+                                    m[e] = __float_as_uint(fmaxf(__uint_as_float(m[e]), __uint_as_float(x[e])));
+                            }
+                        };
+                        if constexpr (KC == 2) {
+                            tap(0, 1);
+                            tap(1, 0);
+                            tap(1, 1);
+                        } else if constexpr (KC > 0) {
+                            // one row of taps in flight (fewer registers for
+                            // the kernel as a whole)
+#pragma unroll 1
+                            for (int i = 0; i < KC; ++i)
+#pragma unroll
+                                for (int j = 0; j < KC; ++j)
+                                    if (i + j > 0) tap(i, j);
+                        } else {
+                            for (int i = 0; i < K; ++i)
+                                for (int j = 0; j < K; ++j) tap(i, j);
+                        }
+                        if constexpr (BF) {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) m[e] = bf16x2_key(m[e]);
+                        }
+                        *reinterpret_cast<u4 *>(dst) = m;
+                        src += ew * TS;
+                        if (++oy == K) {
+                            oy = 0;
+                            dst += d_yb - (K - 1) * d_oy;
+                        } else {
+                            dst += d_oy;
                         }
                     }
-                if constexpr (BF) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) m[e] = bf16x2_key(m[e]);
                 }
-                *reinterpret_cast<u4 *>(child_ptr(r, c) + v * TPAD) = m;
-            }
+            };
+            if (kp == 2)
+                walk(std::integral_constant<int, 2>());
+            else if (kp == 3)
+                walk(std::integral_constant<int, 3>());
+            else
+                walk(std::integral_constant<int, 0>());
         } else {
             const Div dco(a.cout);
             const int total = rtM * twM * a.cout;
