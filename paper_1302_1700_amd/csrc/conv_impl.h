@@ -132,6 +132,14 @@ struct Elem<true> {
 // map at the window corner the pixel stands for: final fragment (fy, fx)
 // position (y, x) holds window (base[fy] + S*y, base[fx] + S*x)
 // (fused_head_finish).  A workgroup barrier separates the two.
+// Whether the fused head keeps only z1 - z0 (two classes and softmax, per-lane
+// products): fused_head_partials and fused_head_finish agree on it.
+template <bool BF, int NB>
+__device__ __forceinline__ bool head_two_class(const ConvArgs &a)
+{
+    return !(BF && NB % 2 == 0) && a.head_ncls == 2 && a.head_act == ACT_SOFTMAX;
+}
+
 template <int MB, int NB, int WN, bool BF>
 __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 (&acc)[MB][NB], int nb0, int wm,
                                                     int wn, int lm, int g, float *red)
@@ -176,6 +184,36 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
         for (int i = 0; i < MB; ++i)
 #pragma unroll
             for (int c = 0; c < NC; ++c) part[i][c] = hacc[i][c];
+    } else if (head_two_class<BF, NB>(a)) {
+        // two classes with softmax: only z1 - z0 is needed, one product per
+        // value with the weight differences
+        const int ldw = a.nbt * 16;
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) part[i][c] = 0.f;
+#pragma unroll
+        for (int j = 0; j < NB; ++j) {
+            const int r0 = (nb0 + j) * 16 + 4 * g;
+            const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
+            const f4 w0 = *reinterpret_cast<const f4 *>(a.head_w + r0);
+            const f4 w1 = *reinterpret_cast<const f4 *>(a.head_w + (size_t)ldw + r0);
+#pragma unroll
+            for (int i = 0; i < MB; ++i)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float v = acc[i][j][e] + bv[e];
+                    if (a.act == ACT_TANH) v = tanh_fast(v);
+                    part[i][0] = fmaf(w1[e] - w0[e], v, part[i][0]);
+                }
+        }
+#pragma unroll
+        for (int i = 0; i < MB; ++i) {
+            float t = part[i][0];
+            t += __shfl_xor(t, 16);
+            t += __shfl_xor(t, 32);
+            part[i][0] = t;
+        }
     } else {
         const int ldw = a.nbt * 16;
 #pragma unroll
@@ -225,13 +263,27 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
 // in it of the tile's pixel m < npix.
 template <int WN, class Locate>
 __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int npix, Locate locate,
-                                                  const float *red)
+                                                  const float *red, bool two_class)
 {
     constexpr int NC = kMaxFusedClasses;
     const int ncls = a.head_ncls;
     const int mt = a.mt;
     for (int m = threadIdx.x; m < npix; m += blockDim.x) {
         float z[NC];
+        if (two_class) {
+            // softmax of two: p1 = 1 / (1 + exp(z0 - z1)), p0 = 1 / (1 + exp(z1 - z0))
+            float d = a.head_b[1] - a.head_b[0];
+#pragma unroll
+            for (int w = 0; w < WN; ++w) d += red[((size_t)w * mt + m) * NC];
+            z[0] = 1.0f / (1.0f + expf(d));
+            z[1] = 1.0f / (1.0f + expf(-d));
+            int fy, fx, y, x;
+            locate(m, fy, fx, y, x);
+            const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
+            float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * 2;
+            *reinterpret_cast<float2 *>(dst) = float2{z[0], z[1]};
+            continue;
+        }
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             float t = c < ncls ? a.head_b[c] : 0.f;
@@ -688,7 +740,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 hy = seg ? fy1 : fy;
                 hx = seg ? fx1 : fx;
             },
-            red);
+            red, head_two_class<BF, NB>(a));
         return;
     }
     // Lane (lm, g) holds, for pixel lm of each m-block, rows 4g .. 4g + 3 of
