@@ -127,6 +127,9 @@ typedef struct {
     int32_t grid;         /* workgroups launched */
     int32_t block;        /* threads per workgroup */
     char name[64];
+    int32_t lds_bytes;    /* dynamic LDS per workgroup */
+    int32_t per_cu;       /* workgroups resident per CU (registers and LDS;
+                             0 when unknown, e.g. plan-only nets) */
 } fs_launch_info;
 
 /* Create a net.  The stack must be: conv / max-pool layers in any order, then

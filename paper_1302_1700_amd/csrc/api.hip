@@ -315,11 +315,15 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     if (l.vec && (pad * es) % 16) pad = 16 / es;
     const int cs = l.vec ? l.cin + pad : l.cin;
     const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
-    // distinct output widths present
-    std::vector<int> wouts;
+    // distinct output widths present; every fragment's output height and width
+    std::vector<int> wouts, houts, wouts_all;
     for (int v : in.ex)
         if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
             wouts.push_back(v - k + 1);
+    for (int v : in.ey)
+        if (v - k + 1 > 0) houts.push_back(v - k + 1);
+    for (int v : in.ex)
+        if (v - k + 1 > 0) wouts_all.push_back(v - k + 1);
     const int wm = 4 / (l.wn * l.wk);
     int mb_force = 0, band_force = 0, lds_min = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force, nullptr, &lds_min);
@@ -349,25 +353,12 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                     const int twb = std::min(band_w, wo - b * band_w);
                     if (twb > 0) tmin = std::min(tmin, twb);
                 }
-            int rmax = (mt - 1 + tmin - 1) / tmin + k;
-            rmax = std::min(rmax, in.hmax);
-            const size_t lds = offtab + (size_t)rmax * (band_w + k - 1) * cs * es;
             // the kernel's index arithmetic (Div in conv_impl.h) takes pixel
             // numbers within a band below 2^20
             if ((long long)hout_max * band_w >= (1 << 20)) continue;
-            if (lds > 96 * 1024) {
-                if (band_w <= 8) break;
-                continue;
-            }
             const size_t red = (size_t)l.wn * mt * kMaxFusedClasses * 4;  // fused-head reduction
             // split-K partial sums of the waves with wk > 0
             const size_t part = (size_t)(l.wk - 1) * (4 / l.wk) * mb * l.nb * 4 * 64 * 4;
-            L.mb = mb;
-            L.conv.band_w = band_w;
-            L.conv.nbands = nbands;
-            L.conv.mt = mt;
-            L.conv.tiles_per_band = (hout_max * band_w + mt - 1) / mt;
-            L.conv.lds_cs = cs;
             // Stores: straight from the registers (16-byte runs of 4 f32 or
             // 8 bf16 channels per lane; measured no slower than restaging on
             // every conv layer of the five workloads, faster on the bf16 and
@@ -376,12 +367,63 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             int direct = 1;
             if (const char *e = getenv("FRAGSCAN_STORE"); e && e[0]) direct = e[0] == 'd';
             const size_t otile = direct ? 0 : (size_t)mt * (l.wn * l.nb * 16 + 16 / es) * es;
-            L.conv.direct_store = direct;
-            const size_t need = std::max(std::max(std::max(lds, part), std::max(red, otile)), (size_t)lds_min);
+            const size_t other = std::max(std::max(part, red), std::max(otile, (size_t)lds_min));
+            // Pixel tiles: mt consecutive pixels of a band, whose window in
+            // the narrowest band spans the most rows, and that sizes the LDS
+            // of every workgroup.  Row tiles (several bands): rows_t = mt /
+            // band_w whole band rows, the same window rows in every band.
+            const int rmax_p = std::min((mt - 1 + tmin - 1) / tmin + k, in.hmax);
+            const size_t lds_p = offtab + (size_t)rmax_p * (band_w + k - 1) * cs * es;
+            const int rows_t = (nbands > 1 && mt >= band_w) ? mt / band_w : 0;
+            const size_t lds_r = rows_t ? offtab + (size_t)std::min(rows_t + k - 1, in.hmax) * (band_w + k - 1) * cs * es
+                                        : lds_p;
+            if (std::min(lds_p, lds_r) > 96 * 1024) {
+                if (band_w <= 8) break;
+                continue;
+            }
+            const size_t need_p = std::max(lds_p, other), need_r = std::max(lds_r, other);
+            // Which one: the tiles that hold pixels, weighted by how much a
+            // lone workgroup per CU (nothing to overlap its staging and
+            // epilogue with) or two cost against three or more; measured on
+            // N4's 48 -> 48 layers: 1 -> 2 per CU 15% faster (5x5 on 606^2
+            // images), 2 -> 3 at most 4% and outweighed by the row tiles'
+            // extra part-empty tiles.  FRAGSCAN_ROWTILES=1/0 forces either.
+            bool use_rows = false;
+            if (rows_t && need_r <= kMaxLdsBytes) {
+                auto per_cu = [&](size_t need) {
+                    if (net->ncu > 0)
+                        return conv_blocks_per_cu(net->dtype, in.is_image, mb, l.nb, l.wn, l.wk, l.vec, false,
+                                                  (int)need);
+                    return (int)std::min<size_t>(8, kMaxLdsBytes / need);
+                };
+                auto weight = [](int n) { return n <= 1 ? 1.30 : n == 2 ? 1.02 : 1.0; };
+                long long tiles_p = 0, tiles_r = 0;
+                for (int ho : houts)
+                    for (int wo : wouts_all)
+                        for (int b = 0; b < nbands; ++b) {
+                            const int twb = std::min(band_w, wo - b * band_w);
+                            if (twb <= 0) break;
+                            tiles_p += ((long long)ho * twb + mt - 1) / mt;
+                            tiles_r += (ho + rows_t - 1) / rows_t;
+                        }
+                const double cost_p = need_p <= kMaxLdsBytes ? tiles_p * weight(per_cu(need_p)) : 1e300;
+                const double cost_r = tiles_r * weight(per_cu(need_r));
+                use_rows = cost_r < cost_p;
+                if (const char *e = getenv("FRAGSCAN_ROWTILES"); e && e[0]) use_rows = e[0] == '1';
+            }
+            const size_t need = use_rows ? need_r : need_p;
             if (need > kMaxLdsBytes) {
                 if (mb_force) break;
                 continue;
             }
+            L.mb = mb;
+            L.conv.band_w = band_w;
+            L.conv.nbands = nbands;
+            L.conv.mt = mt;
+            L.conv.tile_rows = use_rows ? rows_t : 0;
+            L.conv.tiles_per_band = use_rows ? (hout_max + rows_t - 1) / rows_t : (hout_max * band_w + mt - 1) / mt;
+            L.conv.lds_cs = cs;
+            L.conv.direct_store = direct;
             L.conv.lds_bytes = (int)need;
             L.conv.run = 0;
             if (nbands == 1 && direct) plan_run_tiles(l, in, mt, cs, es, offtab, std::max(part, red), L);
@@ -1250,6 +1292,12 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, f
         o.grid = L.gx * L.gy;
         o.block = 256;
         std::snprintf(o.name, sizeof o.name, "%s", L.name.c_str());
+        if (L.type == 0 && !L.direct) {
+            o.lds_bytes = L.conv.lds_bytes;
+            if (net->ncu > 0)
+                o.per_cu = conv_blocks_per_cu(net->dtype, L.in_f32, L.mb, L.nb, L.wn, L.wk, L.vec, L.conv.run,
+                                              L.conv.lds_bytes);
+        }
     }
     return FS_OK;
 }

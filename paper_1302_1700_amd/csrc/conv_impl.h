@@ -423,9 +423,10 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             twb = min(a.band_w, wout - c0);
             if (twb <= 0) return;
             const int npix = hout * twb;
-            l0 = t * a.mt;
+            const int tpx = a.tile_rows ? a.tile_rows * twb : a.mt;  // pixels per tile
+            l0 = t * tpx;
             if (l0 >= npix) return;
-            lend = min(l0 + a.mt, npix);
+            lend = min(l0 + tpx, npix);
         }
     }
     const int n0 = lend - l0;

@@ -53,6 +53,7 @@ struct ConvArgs {
     int nbands;           // bands per fragment
     int tiles_per_band;   // tiles per band (enough for the tallest fragment)
     int mt;               // output pixels per tile (16 * MB * 4 / (WN * WK))
+    int tile_rows;        // > 0: a tile is tile_rows whole rows of its band (tile_rows * band_w <= mt)
     int lds_cs;           // channel stride of a pixel in LDS (elements)
     int lds_bytes;        // dynamic LDS bytes of one workgroup
     int direct_store;     // 1: lanes store their channel runs straight to memory;
