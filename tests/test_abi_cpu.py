@@ -210,6 +210,29 @@ def test_run_tiles_where_they_save_a_round(monkeypatch):
     assert fc[512]["name"].endswith("+head") and fc[512]["grid"] == 1536
 
 
+def test_row_tiles_where_one_workgroup_per_cu(monkeypatch):
+    """N4's 5x5 layer on a 606 x 606 image: 16-column bands leave a 9-column
+    last band, whose 128-pixel tiles span 15 rows; sized for those, the LDS
+    would admit one workgroup per CU, so the planner takes tiles of 8 whole
+    band rows (plan-only nets count LDS only).  FRAGSCAN_ROWTILES=0/1 forces
+    either; at 512 x 512 pixel tiles stay."""
+    monkeypatch.delenv("FRAGSCAN_ROWTILES", raising=False)
+    net = _plan_net(wl.WORKLOADS[2].layers)
+    conv5 = lambda H: [L for L in net.launches(1, H, H) if L["layer"] == 2][0]
+    auto = conv5(606)
+    monkeypatch.setenv("FRAGSCAN_ROWTILES", "0")
+    pix = conv5(606)
+    monkeypatch.setenv("FRAGSCAN_ROWTILES", "1")
+    rows = conv5(606)
+    monkeypatch.delenv("FRAGSCAN_ROWTILES")
+    at512 = conv5(512)
+    net.close()
+    assert pix["lds_bytes"] > 160 * 1024 // 2 >= rows["lds_bytes"]
+    assert auto["lds_bytes"] == rows["lds_bytes"] and auto["grid"] == rows["grid"]
+    assert at512["lds_bytes"] > 160 * 1024 // 3  # pixel tiles, two per CU by LDS
+    assert auto["out_pixels"] == pix["out_pixels"] == rows["out_pixels"]
+
+
 def test_border_mode_rejected_when_unknown():
     net = _plan_net(wl.WORKLOADS[1].layers)
     p = fsb.fs_plan_info()

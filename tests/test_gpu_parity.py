@@ -458,6 +458,27 @@ def test_run_tiles(fsb, monkeypatch, dt, big):
     assert np.abs(run - ref).max() <= TOL[dt]
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_row_tiles(fsb, monkeypatch, dt):
+    """Tiles of whole band rows (a narrower last band gets fewer pixels per
+    tile) give the same values as tiles of mt pixels, bit for bit, on layers
+    with several bands and ragged fragments; pools unfused so the plain conv
+    tiles run everywhere."""
+    layers = [wl.conv(3, 3, 32), wl.conv(2, 32, 48), wl.pool(2, 48), wl.conv(3, 48, 32),
+              wl.pool(2, 32), wl.fc(2, 32, 24), wl.fc(1, 24, 3, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 31, 0.2)
+    img = wl.make_image(32, 2, w0 + 141, w0 + 117, 3)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "0")
+    monkeypatch.setenv("FRAGSCAN_ROWTILES", "1")
+    rows = _scan(fsb, layers, params, img, 3, dtype=dt)
+    monkeypatch.setenv("FRAGSCAN_ROWTILES", "0")
+    pix = _scan(fsb, layers, params, img, 3, dtype=dt)
+    assert np.array_equal(rows, pix)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    assert np.abs(rows - ref).max() <= TOL[dt]
+
+
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
 def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     """Small-K layers take either the per-pixel vector-ALU kernel or the
