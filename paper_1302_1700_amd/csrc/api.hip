@@ -327,13 +327,11 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     const int wm = 4 / (l.wn * l.wk);
     int mb_force = 0, band_force = 0, lds_min = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force, nullptr, &lds_min);
-    // pixel blocks per wave: four when a wave owns at most four channel
-    // blocks (more products per operand load; measured faster on every such
-    // layer) or the K walk is long (N4's 3x3x48 -> 200 layer); else two, so
-    // that three waves per SIMD overlap the epilogues of short-K layers;
-    // then the neighbours
-    const int mb_pref = (l.vec && (l.nb <= 4 || l.ksteps >= 16)) ? 4 : 2;
-    const int mbs[4] = {mb_pref, mb_pref == 4 ? 2 : 4, 1, 8};
+    // pixel blocks per wave: four (more products per operand load; measured
+    // faster on every conv layer of the five workloads, including the short
+    // K walks of workload 3's 2x2x16 -> 100 layer, 742 -> 688 us against two,
+    // and workload 5's gathered 3x3x3 -> 32 first layer), else the neighbours
+    const int mbs[4] = {4, 2, 1, 8};
     for (int mi = 0; mi < 4; ++mi) {
         const int mb = mb_force ? mb_force : mbs[mi];
         if (!conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
