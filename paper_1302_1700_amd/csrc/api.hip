@@ -345,12 +345,6 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
         if (band_force) nbands = (wout_max + band_force - 1) / band_force;
         for (; nbands <= wout_max; ++nbands) {
             const int band_w = (wout_max + nbands - 1) / nbands;
-            int tmin = band_w;
-            for (int wo : wouts)
-                for (int b = 0; b < nbands; ++b) {
-                    const int twb = std::min(band_w, wo - b * band_w);
-                    if (twb > 0) tmin = std::min(tmin, twb);
-                }
             // the kernel's index arithmetic (Div in conv_impl.h) takes pixel
             // numbers within a band below 2^20
             if ((long long)hout_max * band_w >= (1 << 20)) continue;
@@ -370,8 +364,20 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             // the narrowest band spans the most rows, and that sizes the LDS
             // of every workgroup.  Row tiles (several bands): rows_t = mt /
             // band_w whole band rows, the same window rows in every band.
-            const int rmax_p = std::min((mt - 1 + tmin - 1) / tmin + k, in.hmax);
-            const size_t lds_p = offtab + (size_t)rmax_p * (band_w + k - 1) * cs * es;
+            // (the window of a tile in a band of width t spans the rows its
+            // pixels touch plus k - 1, and t + k - 1 columns: the largest over
+            // the bands present and the tile starts i * mt, which repeat
+            // with period t)
+            size_t lds_p = 0;
+            for (int wo : wouts)
+                for (int b = 0; b < nbands; ++b) {
+                    const int t = std::min(band_w, wo - b * band_w);
+                    if (t <= 0) break;
+                    int span = 0;
+                    for (int i = 0; i < t; ++i) span = std::max(span, (int)(((long long)i * mt) % t + mt - 1) / t + 1);
+                    const int rows = std::min(span + k - 1, in.hmax);
+                    lds_p = std::max(lds_p, offtab + (size_t)rows * (t + k - 1) * cs * es);
+                }
             const int rows_t = (nbands > 1 && mt >= band_w) ? mt / band_w : 0;
             const size_t lds_r = rows_t ? offtab + (size_t)std::min(rows_t + k - 1, in.hmax) * (band_w + k - 1) * cs * es
                                         : lds_p;

@@ -211,25 +211,27 @@ def test_run_tiles_where_they_save_a_round(monkeypatch):
 
 
 def test_row_tiles_where_one_workgroup_per_cu(monkeypatch):
-    """N4's 5x5 layer on a 606 x 606 image: 16-column bands leave a 9-column
-    last band, whose 128-pixel tiles span 15 rows; sized for those, the LDS
+    """N4's 5x5 layer on a 494 x 494 image: 16-column bands leave a 2-column
+    last band, whose 128-pixel tiles span 64 rows; sized for those, the LDS
     would admit one workgroup per CU, so the planner takes tiles of 8 whole
     band rows (plan-only nets count LDS only).  FRAGSCAN_ROWTILES=0/1 forces
-    either; at 512 x 512 pixel tiles stay."""
+    either; at 512 x 512 (last band 10 columns) pixel tiles fit three per CU
+    and stay."""
     monkeypatch.delenv("FRAGSCAN_ROWTILES", raising=False)
     net = _plan_net(wl.WORKLOADS[2].layers)
     conv5 = lambda H: [L for L in net.launches(1, H, H) if L["layer"] == 2][0]
-    auto = conv5(606)
+    auto = conv5(494)
     monkeypatch.setenv("FRAGSCAN_ROWTILES", "0")
-    pix = conv5(606)
+    pix = conv5(494)
+    pix512 = conv5(512)
     monkeypatch.setenv("FRAGSCAN_ROWTILES", "1")
-    rows = conv5(606)
+    rows = conv5(494)
     monkeypatch.delenv("FRAGSCAN_ROWTILES")
     at512 = conv5(512)
     net.close()
     assert pix["lds_bytes"] > 160 * 1024 // 2 >= rows["lds_bytes"]
     assert auto["lds_bytes"] == rows["lds_bytes"] and auto["grid"] == rows["grid"]
-    assert at512["lds_bytes"] > 160 * 1024 // 3  # pixel tiles, two per CU by LDS
+    assert at512["lds_bytes"] == pix512["lds_bytes"] <= 160 * 1024 // 3
     assert auto["out_pixels"] == pix["out_pixels"] == rows["out_pixels"]
 
 
