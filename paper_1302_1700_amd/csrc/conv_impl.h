@@ -452,10 +452,58 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     // true size is hh x ww (outside it, zeros)
     auto stage = [&](const TI *src, int gy0, int hh, int ww, int row0, int nrows) {
         const int rowp = a.in_w * a.in_c;  // elements per input row (fragments stay below 2^31)
+        const int npx = nrows * Cc;        // window pixels to stage
+        // Fast form (up to 64 loads per pixel): a thread owns load v of
+        // window pixels p, p + P, p + 2P, ... (P = 256 / loads per pixel);
+        // the pixel's (row, column) and both addresses advance by constants,
+        // with at most one carry into the next row per step.  UN loads are
+        // in flight per thread before their LDS stores.
+        auto walk = [&](int nvec, int width, auto load) {
+            constexpr int UN = 8;
+            const int P = 256 / nvec;
+            int p, v;
+            Div(nvec).qr(threadIdx.x, p, v);
+            if (p >= P) return;  // threads past P * nvec idle
+            int r, c;
+            Div(Cc).qr(p, r, c);
+            const int dr = P / Cc, dc = P - dr * Cc;
+            int soff = (gy0 + r) * rowp + __mul24(c0 + c, a.in_c) + v * width;
+            const int sstep = dr * rowp + dc * a.in_c, swrap = rowp - Cc * a.in_c;
+            int doff = __mul24(__mul24(row0, Cc) + p, CS) + v * width;
+            const int dstep = P * CS;
+            while (p < npx) {
+                decltype(load(0)) val[UN];
+                int dsto[UN];
+#pragma unroll
+                for (int u = 0; u < UN; ++u) {
+                    const bool in = p < npx;
+                    val[u] = {};
+                    if (in && gy0 + r < hh && c0 + c < ww) val[u] = load(soff);
+                    dsto[u] = in ? doff : -1;
+                    p += P;
+                    doff += dstep;
+                    soff += sstep;
+                    r += dr;
+                    c += dc;
+                    if (c >= Cc) {
+                        c -= Cc;
+                        ++r;
+                        soff += swrap;
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < UN; ++u)
+                    if (dsto[u] >= 0) *reinterpret_cast<decltype(load(0)) *>(win_lds + dsto[u]) = val[u];
+            }
+        };
         if constexpr (VEC && !IN_F32) {
-            // batches of 8 loads in flight per thread before their LDS stores
             const int nvec = a.cin / LPE;
-            const int total = nrows * Cc * nvec;
+            if (nvec <= 64) {
+                walk(nvec, LPE, [&](int off) { return *reinterpret_cast<const u4 *>(src + off); });
+                return;
+            }
+            // batches of 8 loads in flight per thread before their LDS stores
+            const int total = npx * nvec;
             const Div dnv(nvec), dcc(Cc);
             constexpr int UN = 8;
             for (int base = threadIdx.x; base < total; base += 256 * UN) {
@@ -478,7 +526,16 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                     if (dsto[u] >= 0) *reinterpret_cast<u4 *>(win_lds + dsto[u]) = val[u];
             }
         } else {
-            const int total = nrows * Cc * a.cin;
+            if (a.cin <= 64) {
+                walk(a.cin, 1, [&](int off) -> TC {
+                    if constexpr (BF && IN_F32)
+                        return f2bf(src[off]);
+                    else
+                        return src[off];
+                });
+                return;
+            }
+            const int total = npx * a.cin;
             const Div dci(a.cin), dcc(Cc);
             for (int idx = threadIdx.x; idx < total; idx += 256) {
                 int p, ci, r, c;
