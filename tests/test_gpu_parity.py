@@ -121,6 +121,22 @@ def test_channel_multiples_vector_path(fsb):
         assert np.abs(got - ref).max() <= TOL[dt], dt
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_wide_channel_staging(fsb, dt):
+    """Window staging for many loads per pixel: 70 channels (gather path,
+    more than 64 elements per pixel) and 272 channels (vector path: 68
+    16-byte loads per pixel in f32, 34 in bf16), with several tiles and
+    ragged fragments."""
+    layers = [wl.conv(2, 3, 70), wl.conv(2, 70, 272), wl.pool(2, 272), wl.conv(2, 272, 32),
+              wl.fc(2, 32, 16), wl.fc(1, 16, 2, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 41, 0.08)
+    img = wl.make_image(42, 1, w0 + 37, w0 + 30, 3)
+    got = _scan(fsb, layers, params, img, 3, dtype=dt)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    assert np.abs(got - ref).max() <= TOL[dt]
+
+
 # ---- workload nets on smaller images: full map -------------------------------
 
 @pytest.mark.parametrize("wid,H,W,B", [(2, 150, 141, 1), (3, 170, 163, 1), (4, 120, 131, 3), (5, 140, 151, 1)])
