@@ -495,6 +495,18 @@ def test_row_tiles(fsb, monkeypatch, dt):
     assert np.abs(rows - ref).max() <= TOL[dt]
 
 
+@pytest.mark.parametrize("wid", [2, 5])
+def test_lds_padding(fsb, monkeypatch, wid):
+    """The per-pixel LDS padding only moves the window in LDS: without it the
+    scan gives the same values bit for bit."""
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid, height=140, width=131)
+    padded = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    monkeypatch.setenv("FRAGSCAN_LDS_PAD", "0")
+    packed = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    assert np.array_equal(padded, packed)
+
+
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
 def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     """Small-K layers take either the per-pixel vector-ALU kernel or the
