@@ -212,6 +212,27 @@ fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int
                          int32_t border, float *d_out, void *d_workspace, size_t workspace_bytes,
                          void *stream);
 
+/* Tiled scan: the same outputs as fs_scan (bit for bit) with a workspace
+ * bounded by the tile instead of the image, for images whose scan would not
+ * fit in device memory.  The H - w_0 + 1 by W - w_0 + 1 output map is cut
+ * into tiles of at most tile_h x tile_w windows; each tile is an ordinary
+ * fragment scan of the image region its windows cover (tile_h + w_0 - 1 rows
+ * of the image, read in place with the image's own pitch; Section 2.2 on that
+ * region), writing straight into its place in d_out, and the tiles run one
+ * after the other on `stream`, reusing d_workspace.  Each tile recomputes
+ * the convolutions of the w_0 - 1 image rows and columns it shares with its
+ * neighbours.  d_image [B][H][W][C] float32 and d_out [B][H - w_0 + 1]
+ * [W - w_0 + 1][n_classes] float32, device, 16-byte aligned; d_workspace
+ * 256-byte aligned, holding fs_scan_plan_tiled's workspace_bytes.  The net's
+ * first layer must be a convolution (FS_ERR_UNSUPPORTED otherwise);
+ * FS_ERR_INVALID_ARG for tile sizes below 1 or more than 2^20 tiles.  Tile
+ * sizes above the map's are clamped to it. */
+fs_status fs_scan_plan_tiled(const fs_net *net, int32_t B, int32_t H, int32_t W, int32_t tile_h,
+                             int32_t tile_w, fs_plan_info *out);
+fs_status fs_scan_tiled(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
+                        int32_t tile_h, int32_t tile_w, float *d_out, void *d_workspace,
+                        size_t workspace_bytes, void *stream);
+
 /* fs_scan with every launch repeated `reps` times back to back between two
  * HIP events on `stream` (a repetition recomputes the same values, so d_out
  * ends as after fs_scan); synchronises the stream and writes, per launch,

@@ -226,8 +226,19 @@ struct Launch {
     std::string name;
 };
 
+// A scan of a sub-image: the image region read has the image's pitch (rows
+// per image img_h, pixels per row img_w) and starts img_off floats in; the
+// outputs go into a map of out_h x out_w windows per image, out_off floats in.
+struct View {
+    int img_h = 0, img_w = 0;
+    size_t img_off = 0;
+    int out_h = 0, out_w = 0;
+    size_t out_off = 0;
+};
+
 struct Plan {
     int B, H, W, ny, nx;
+    View view;                 // img_h == 0: the whole image, outputs dense
     std::vector<Launch> launches;
     size_t buf_bytes = 0;      // each of the two ping-pong buffers
     size_t ws_bytes = 0;
@@ -535,7 +546,7 @@ bool want_pool_fusion(const fs_net *net, int li)
     return (double)l.cin * l.k * l.k * ov < elem_of(net->dtype) * ridge;
 }
 
-fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
+fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View *view = nullptr)
 {
     if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
     if (H < net->patch || W < net->patch)
@@ -546,6 +557,11 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
     P.W = W;
     P.ny = H - net->patch + 1;
     P.nx = W - net->patch + 1;
+    if (view) P.view = *view;
+    // the image's pitch (a view reads a region of a larger image) and the
+    // output map's (a view writes a region of a larger map)
+    const int img_h = view ? view->img_h : H, img_w = view ? view->img_w : W;
+    const int map_h = view ? view->out_h : P.ny, map_w = view ? view->out_w : P.nx;
     const int es = elem_of(net->dtype);
 
     Geo g;
@@ -584,6 +600,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             o = pool_geo(g, k);
             if (g.Q * k > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
             L.type = 1;
+            if (g.is_image && view) return fail(FS_ERR_UNSUPPORTED, "a tiled scan needs a convolution first");
             PoolArgs &a = L.pool;
             a.F = F;
             a.Q = g.Q;
@@ -621,8 +638,8 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
             a.nfrag = B * F;
             a.F = F;
             a.Q = g.Q;
-            a.in_h = g.hmax;
-            a.in_w = g.wmax;
+            a.in_h = g.is_image ? img_h : g.hmax;  // fragment stride and row pitch
+            a.in_w = g.is_image ? img_w : g.wmax;
             a.in_c = g.C;
             a.out_h = std::max(o.hmax, 1);
             a.out_w = std::max(o.wmax, 1);
@@ -722,8 +739,8 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
                     return fail(FS_ERR_UNSUPPORTED, "layer %d: no bf16 head operands for the fused head", li);
                 a.head_ncls = net->ncls;
                 a.head_act = hl.act;
-                a.ny = P.ny;
-                a.nx = P.nx;
+                a.ny = map_h;  // output pitch
+                a.nx = map_w;
                 a.S = net->S;
                 for (int f = 0; f < o.Q; ++f) {  // first output coordinate of axis index f
                     int rest = f, base = 0, S = net->S;
@@ -777,9 +794,12 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P)
         a.Q = g.Q;
         a.in_h = std::max(g.hmax, 1);
         a.in_w = std::max(g.wmax, 1);
+        if (g.is_image && view) return fail(FS_ERR_UNSUPPORTED, "a tiled scan needs a convolution first");
         a.C = g.C;
         a.ny = P.ny;
         a.nx = P.nx;
+        a.out_ny = map_h;
+        a.out_nx = map_w;
         a.ncls = net->ncls;
         a.act = net->L.back().act;
         a.S = net->S;
@@ -862,11 +882,60 @@ fs_status validate_scan(const fs_net *net, const float *d_image, int B, int H, i
     return check_device(net);
 }
 
+// A scan cut into output tiles of at most th x tw windows: the tile with
+// top-left window (y0, x0) reads image rows y0 .. y0 + h + w_0 - 2 (and the
+// same columns) and writes its h x w windows at (y0, x0) of the full map.
+// Tiles of one shape share a plan (at most four shapes: full and last).
+struct Tiled {
+    int ny = 0, nx = 0, th = 0, tw = 0, rows = 0, cols = 0;
+    Plan shape[2][2];  // [last row of tiles][last column of tiles]
+    size_t ws_bytes = 0;
+    int n_launches = 0;
+    double flops = 0, bytes = 0;
+};
+
+fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Tiled &T)
+{
+    if (th < 1 || tw < 1) return fail(FS_ERR_INVALID_ARG, "tile sizes must be >= 1 (got %d x %d)", th, tw);
+    if (B < 1 || H < net->patch || W < net->patch)
+        return fail(FS_ERR_SHAPE, "image %dx%d (batch %d) smaller than the patch size %d", H, W, B, net->patch);
+    T = Tiled();
+    T.ny = H - net->patch + 1;
+    T.nx = W - net->patch + 1;
+    T.th = std::min(th, T.ny);
+    T.tw = std::min(tw, T.nx);
+    T.rows = (T.ny + T.th - 1) / T.th;
+    T.cols = (T.nx + T.tw - 1) / T.tw;
+    if ((long long)T.rows * T.cols > (1 << 20)) return fail(FS_ERR_INVALID_ARG, "more than 2^20 tiles");
+    for (int lr = 0; lr < 2; ++lr)
+        for (int lc = 0; lc < 2; ++lc) {
+            const int h = lr ? T.ny - (T.rows - 1) * T.th : T.th, w = lc ? T.nx - (T.cols - 1) * T.tw : T.tw;
+            View v;
+            v.img_h = H;
+            v.img_w = W;
+            v.out_h = T.ny;
+            v.out_w = T.nx;
+            fs_status st = make_plan(net, B, h + net->patch - 1, w + net->patch - 1, T.shape[lr][lc], &v);
+            if (st != FS_OK) return st;
+            T.ws_bytes = std::max(T.ws_bytes, T.shape[lr][lc].ws_bytes);
+        }
+    for (int r = 0; r < T.rows; ++r)
+        for (int c = 0; c < T.cols; ++c) {
+            const Plan &P = T.shape[r == T.rows - 1][c == T.cols - 1];
+            T.n_launches += (int)P.launches.size();
+            T.flops += P.flops;
+            T.bytes += P.bytes;
+        }
+    return FS_OK;
+}
+
 hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_out, void *d_ws,
                    hipStream_t s, int i)
 {
     Launch &L = P.launches[i];
     char *ws = static_cast<char *>(d_ws);
+    d_image += P.view.img_off;
+    d_out += P.view.out_off;
     auto ptr = [&](int which) -> void * {
         if (which == -1) return const_cast<float *>(d_image);
         if (which == 2) return d_out;
@@ -1201,6 +1270,56 @@ fs_status fs_net_query(const fs_net *net, fs_net_info *out)
     out->stride = net->S;
     out->n_fragments = net->F;
     out->dtype = net->dtype;
+    return FS_OK;
+}
+
+fs_status fs_scan_plan_tiled(const fs_net *net, int32_t B, int32_t H, int32_t W, int32_t tile_h, int32_t tile_w,
+                             fs_plan_info *out)
+{
+    if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
+    Tiled T;
+    fs_status st = tiled_plan(net, B, H, W, tile_h, tile_w, T);
+    if (st != FS_OK) return st;
+    out->batch = B;
+    out->out_h = T.ny;
+    out->out_w = T.nx;
+    out->n_launches = T.n_launches;
+    out->workspace_bytes = T.ws_bytes;
+    out->flops = T.flops;
+    out->min_bytes = T.bytes;
+    return FS_OK;
+}
+
+fs_status fs_scan_tiled(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, int32_t tile_h,
+                        int32_t tile_w, float *d_out, void *d_workspace, size_t workspace_bytes, void *stream)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
+    if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
+        return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
+    Tiled T;
+    fs_status st = tiled_plan(net, B, H, W, tile_h, tile_w, T);
+    if (st != FS_OK) return st;
+    if (workspace_bytes < T.ws_bytes)
+        return fail(FS_ERR_WORKSPACE, "workspace of %zu bytes, the tiled scan needs %zu", workspace_bytes, T.ws_bytes);
+    if (T.ws_bytes && !d_workspace) return fail(FS_ERR_INVALID_ARG, "workspace pointer is NULL");
+    if ((uintptr_t)d_workspace & 255) return fail(FS_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    st = check_device(net);
+    if (st != FS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int r = 0; r < T.rows; ++r)
+        for (int c = 0; c < T.cols; ++c) {
+            Plan &P = T.shape[r == T.rows - 1][c == T.cols - 1];
+            const size_t y0 = (size_t)r * T.th, x0 = (size_t)c * T.tw;
+            P.view.img_off = (y0 * W + x0) * net->C;
+            P.view.out_off = (y0 * T.nx + x0) * net->ncls;
+            for (int i = 0; i < (int)P.launches.size(); ++i) {
+                hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+                if (e != hipSuccess)
+                    return fail(FS_ERR_HIP, "tile (%d, %d) launch %d (%s): %s", r, c, i, P.launches[i].name.c_str(),
+                                hipGetErrorString(e));
+            }
+        }
     return FS_OK;
 }
 

@@ -86,7 +86,7 @@ struct ConvArgs {
     // 32 * pair + 8 * (l / 16) .. + 7 (zero past the channels)
     const void *head_wbf;
     const float *head_b;  // [head_ncls]
-    float *head_out;      // [B][ny][nx][head_ncls]
+    float *head_out;      // [B][ny][nx][head_ncls] (ny, nx: the output map's rows and row pitch)
     int ny, nx, S;
     uint16_t base[kMaxAxis];  // per-axis fragment index -> its first output coordinate
 };
@@ -106,12 +106,13 @@ struct PoolArgs {
 // reassembly of final fragments into the dense output map.
 struct HeadArgs {
     const void *in;      // final fragments [B*F][in_h][in_w][C]
-    float *out;          // [B][ny][nx][ncls]
+    float *out;          // [B][out_ny][out_nx][ncls], windows at [.][0, ny)[0, nx)
     const float *w;      // [ncls][C] (has_fc) or unused
     const float *bias;   // [ncls]
     int B, F, Q;
     int in_h, in_w, C;
-    int ny, nx, ncls, act;
+    int ny, nx, ncls, act;  // windows per image (rows, columns)
+    int out_ny, out_nx;  // the output map's rows and row pitch (>= ny, nx)
     int S;               // product of pool sizes
     uint16_t digit_map[kMaxAxis];  // output coordinate mod S -> per-axis fragment index
 };

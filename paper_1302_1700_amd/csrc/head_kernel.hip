@@ -129,7 +129,7 @@ __global__ __launch_bounds__(256) void head_softmax_reassemble(HeadArgs a)
 #pragma unroll
     for (int c = 0; c < kMaxHeadClasses; ++c)
         if (c == sub) mine = z[c];
-    if (sub < ncls) a.out[gp * ncls + sub] = mine;
+    if (sub < ncls) a.out[(((size_t)b * a.out_ny + Y) * a.out_nx + X) * ncls + sub] = mine;
 }
 
 template <bool BF, bool IN_F32, bool HAS_FC, int V>

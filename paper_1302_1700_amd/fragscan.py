@@ -54,7 +54,8 @@ class fs_launch_info(ctypes.Structure):
 
 EXPORTS = ["fs_net_create", "fs_net_create_plan_only", "fs_net_destroy", "fs_net_query", "fs_scan_plan", "fs_scan_launches",
            "fs_scan", "fs_scan_profile", "fs_fragment_table", "fs_reassembly_index",
-           "fs_status_str", "fs_last_error", "fs_scan_plan_border", "fs_scan_border"]
+           "fs_status_str", "fs_last_error", "fs_scan_plan_border", "fs_scan_border",
+           "fs_scan_plan_tiled", "fs_scan_tiled"]
 
 _lib = None
 
@@ -77,6 +78,8 @@ def load():
         "fs_scan_plan": [VP, I32, I32, I32, P(fs_plan_info)],
         "fs_scan_plan_border": [VP, I32, I32, I32, I32, P(fs_plan_info)],
         "fs_scan_border": [VP, VP, I32, I32, I32, I32, VP, VP, SZ, VP],
+        "fs_scan_plan_tiled": [VP, I32, I32, I32, I32, I32, P(fs_plan_info)],
+        "fs_scan_tiled": [VP, VP, I32, I32, I32, I32, I32, VP, VP, SZ, VP],
         "fs_scan_launches": [VP, I32, I32, I32, P(fs_launch_info), I32],
         "fs_scan": [VP, VP, I32, I32, I32, VP, VP, SZ, VP],
         "fs_scan_profile": [VP, VP, I32, I32, I32, VP, VP, SZ, VP, I32, P(ctypes.c_float), I32],
@@ -197,9 +200,15 @@ class Net:
         return buf.reshape(H - self.patch + 1, W - self.patch + 1, 3)
 
     # -- scanning --------------------------------------------------------------
-    def workspace(self, B, H, W, device=None, border="valid"):
+    def plan_tiled(self, B, H, W, tile):
+        """Plan of scan_tiled with output tiles of tile = (rows, cols) windows."""
+        p = fs_plan_info()
+        _check(load().fs_scan_plan_tiled(self._h, B, H, W, int(tile[0]), int(tile[1]), ctypes.byref(p)))
+        return {n: getattr(p, n) for n, _ in fs_plan_info._fields_}
+
+    def workspace(self, B, H, W, device=None, border="valid", tile=None):
         import torch
-        nbytes = self.plan(B, H, W, border)["workspace_bytes"]
+        nbytes = (self.plan_tiled(B, H, W, tile) if tile else self.plan(B, H, W, border))["workspace_bytes"]
         key = (nbytes, str(device))
         ws = self._ws.get(key)
         if ws is None:
@@ -230,6 +239,23 @@ class Net:
             _check(load().fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
                                          ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
                                          ws.numel(), _stream_handle(stream)))
+        return out
+
+    def scan_tiled(self, image, tile, out=None, workspace=None, stream=None):
+        """As scan (valid windows), computed tile by tile: output tiles of at
+        most tile = (rows, cols) windows, each a fragment scan of the image
+        region it covers, sharing one workspace sized for a tile."""
+        import torch
+        if not image.is_cuda or image.dtype != torch.float32 or not image.is_contiguous():
+            raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
+        B, H, W, C = image.shape
+        if out is None:
+            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes), dtype=torch.float32,
+                              device=image.device)
+        ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, tile=tile)
+        _check(load().fs_scan_tiled(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, int(tile[0]), int(tile[1]),
+                                    ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                    _stream_handle(stream)))
         return out
 
     def profile(self, image, reps=10, out=None, stream=None):

@@ -235,6 +235,38 @@ def test_row_tiles_where_one_workgroup_per_cu(monkeypatch):
     assert auto["out_pixels"] == pix["out_pixels"] == rows["out_pixels"]
 
 
+def test_tiled_plans():
+    """Tiled scan plans: the same output map, a workspace bounded by the
+    tile, one scan's launches per tile, and the halo recomputed (more FLOPs
+    than one scan, the same for a tile covering the map)."""
+    w = wl.WORKLOADS[2]
+    net = _plan_net(w.layers)
+    full = net.plan(2, 700, 650)
+    ny, nx = full["out_h"], full["out_w"]
+    for th, tw in ((128, 96), (1, 1000), (ny, nx), (ny + 5, nx + 9)):
+        t = net.plan_tiled(2, 700, 650, (th, tw))
+        assert (t["out_h"], t["out_w"]) == (ny, nx)
+        rows, cols = -(-ny // min(th, ny)), -(-nx // min(tw, nx))
+        assert t["n_launches"] == rows * cols * full["n_launches"]
+        if rows * cols == 1:
+            assert t["workspace_bytes"] == full["workspace_bytes"] and t["flops"] == full["flops"]
+        else:
+            assert t["workspace_bytes"] < full["workspace_bytes"] and t["flops"] > full["flops"]
+    for bad in ((0, 5), (5, 0)):
+        with pytest.raises(fsb.FsError) as e:
+            net.plan_tiled(1, 200, 200, bad)
+        assert e.value.status == fsb.FS_ERR_INVALID_ARG
+    net.close()
+    # a net that starts with a pool reads the image with the fragment kernels'
+    # own pitch: not tiled
+    layers = [wl.pool(2, 1), wl.conv(3, 1, 4), wl.fc(1, 4, 2, "softmax")]
+    net = _plan_net(layers)
+    with pytest.raises(fsb.FsError) as e:
+        net.plan_tiled(1, 40, 40, (8, 8))
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+    net.close()
+
+
 def test_border_mode_rejected_when_unknown():
     net = _plan_net(wl.WORKLOADS[1].layers)
     p = fsb.fs_plan_info()

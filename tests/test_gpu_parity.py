@@ -507,6 +507,31 @@ def test_lds_padding(fsb, monkeypatch, wid):
     assert np.array_equal(padded, packed)
 
 
+@pytest.mark.parametrize("wid,B,H,W,tiles", [
+    (2, 1, 160, 150, [(17, 23), (5, 64), (1, 1000), (1000, 1000)]),
+    (4, 2, 130, 121, [(9, 11)]),
+    (3, 1, 170, 163, [(31, 7)]),
+    (5, 1, 140, 131, [(20, 33), (7, 80)]),
+    (1, 1, 64, 64, [(1, 1), (50, 2)]),
+])
+def test_tiled_scan(fsb, wid, B, H, W, tiles):
+    """Output tiles scanned one after another, each over the image region
+    its windows cover, give the untiled scan's values bit for bit (ragged
+    last tiles, one-row and one-window tiles, a tile larger than the map)."""
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid, batch=B, height=H, width=W)
+    net = fsb.Net(w.layers, params, w.channels, 0, w.dtype)
+    x = torch.from_numpy(np.ascontiguousarray(img, np.float32)).cuda()
+    ref = net.scan(x).cpu().numpy()
+    for tile in tiles:
+        print("tiled scan", wid, B, H, W, tile, flush=True)
+        out = torch.full_like(torch.from_numpy(ref), float("nan")).cuda()
+        net.scan_tiled(x, tile, out=out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), ref), tile
+    net.close()
+
+
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
 def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     """Small-K layers take either the per-pixel vector-ALU kernel or the
