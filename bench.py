@@ -1,7 +1,7 @@
 """Benchmark of the fragment-based image scan on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload ID] [--no-cpu]
-                    [--border valid|reflect|symmetric]
+                    [--border valid|reflect|symmetric] [--tile R,C]
 
 A step is one full scan (every layer, the head and the reassembly) of the
 workload's synthetic image batch, already resident in device memory.  Prints
@@ -17,7 +17,9 @@ one JSON line:
 Default workload: net N4 (the paper's Table 1 net) on a 512 x 512 greyscale
 image, 418 x 418 windows.  --border reflect / symmetric scans with mirrored
 edges instead (Section 3.2's setup: one output per pixel, 512 x 512); the
-per-launch figures then come from the scan of the extended image.
+per-launch figures then come from the scan of the extended image.  --tile R,C
+scans in output tiles (fs_scan_tiled: a workspace bounded by the tile); the
+per-launch figures stay those of the untiled scan.
 """
 import argparse
 import json
@@ -101,6 +103,8 @@ def main():
     ap.add_argument("--profile-reps", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline legs")
     ap.add_argument("--cpu-fragment", action="store_true", help="also time the CPU fragment method")
+    ap.add_argument("--tile", default=None,
+                    help="R,C: scan in output tiles of at most R x C windows (fs_scan_tiled; valid border)")
     ap.add_argument("--border", default="valid", choices=["valid", "reflect", "symmetric"],
                     help="mirrored image edges (one output per pixel)")
     args = ap.parse_args()
@@ -122,21 +126,31 @@ def main():
     border = args.border
     oh, ow = (w.out_h, w.out_w) if border == "valid" else (w.height, w.width)
     out = torch.empty((w.batch, oh, ow, w.n_classes), dtype=torch.float32, device="cuda")
-    ws = net.workspace(w.batch, w.height, w.width, x.device, border)
+    tile = tuple(int(v) for v in args.tile.split(",")) if args.tile else None
+    if tile and border != "valid":
+        print("bench.py: --tile scans valid windows only", file=sys.stderr)
+        sys.exit(2)
+    ws = net.workspace(w.batch, w.height, w.width, x.device, border, tile=tile)
+
+    def step():
+        if tile:
+            net.scan_tiled(x, tile, out=out, workspace=ws)
+        else:
+            net.scan(x, out=out, workspace=ws, border=border)
     plan = net.plan(w.batch, w.height, w.width, border)
     # the launches of the (extended) image's scan
     eh, ew = (w.height, w.width) if border == "valid" else (w.height + w.patch - 1, w.width + w.patch - 1)
     launches = net.launches(w.batch, eh, ew)
 
     for _ in range(args.warmup):
-        net.scan(x, out=out, workspace=ws, border=border)
+        step()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
     for _ in range(args.steps):
-        net.scan(x, out=out, workspace=ws, border=border)
+        step()
     t1.record(stream)
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / args.steps
@@ -194,7 +208,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "image": [w.batch, w.height, w.width, w.channels],
                    "patch": w.patch, "outputs": [w.batch, oh, ow], "fragments": net.info["n_fragments"],
-                   "border": border},
+                   "border": border, "tile": list(tile) if tile else None,
+                   "workspace_bytes": ws.numel()},
         "tflops": plan["flops"] / (ms * 1e-3) / 1e12,
         "pct_mfma_peak": 100.0 * plan["flops"] / (ms * 1e-3) / 1e12 / peak_mm,
         "conv_tflops_in_conv_kernels": conv_flops / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0,
