@@ -63,7 +63,13 @@ typedef __bf16 bf2v __attribute__((ext_vector_type(2)));
 // get their 15 magnitude bits flipped), so a packed integer max picks the
 // larger value of each half; the map is its own inverse.
 typedef short s2v __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ uint32_t bf16x2_key(uint32_t x) { return x ^ (__umul24((x >> 15) & 0x00010001u, 0x7fffu)); }
+__device__ __forceinline__ uint32_t bf16x2_key(uint32_t x)
+{
+    // per half: all ones for a negative value (arithmetic shift by 15), whose
+    // 15 magnitude bits are then flipped
+    const uint32_t neg = __builtin_bit_cast(uint32_t, __builtin_bit_cast(s2v, x) >> (short)15);
+    return x ^ (neg & 0x7fff7fffu);
+}
 __device__ __forceinline__ uint32_t max_i16x2(uint32_t a, uint32_t b)
 {
     return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s2v, a), __builtin_bit_cast(s2v, b)));
@@ -159,15 +165,13 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
 #pragma unroll
         for (int p = 0; p < NB / 2; ++p) {
             const u4 wv = hw[p * 64];
-            const f4 b0 = *reinterpret_cast<const f4 *>(a.bias + (nb0 + 2 * p) * 16 + 4 * g);
-            const f4 b1 = *reinterpret_cast<const f4 *>(a.bias + (nb0 + 2 * p + 1) * 16 + 4 * g);
 #pragma unroll
             for (int i = 0; i < MB; ++i) {
                 float h[8];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    h[e] = acc[i][2 * p][e] + b0[e];
-                    h[4 + e] = acc[i][2 * p + 1][e] + b1[e];
+                    h[e] = acc[i][2 * p][e];
+                    h[4 + e] = acc[i][2 * p + 1][e];
                 }
                 if (a.act == ACT_TANH) {
 #pragma unroll
@@ -195,14 +199,13 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int r0 = (nb0 + j) * 16 + 4 * g;
-            const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
             const f4 w0 = *reinterpret_cast<const f4 *>(a.head_w + r0);
             const f4 w1 = *reinterpret_cast<const f4 *>(a.head_w + (size_t)ldw + r0);
 #pragma unroll
             for (int i = 0; i < MB; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    float v = acc[i][j][e] + bv[e];
+                    float v = acc[i][j][e];
                     if (a.act == ACT_TANH) v = tanh_fast(v);
                     part[i][0] = fmaf(w1[e] - w0[e], v, part[i][0]);
                 }
@@ -223,7 +226,6 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
 #pragma unroll
         for (int j = 0; j < NB; ++j) {
             const int r0 = (nb0 + j) * 16 + 4 * g;  // (block, row) index of element 0
-            const f4 bv = *reinterpret_cast<const f4 *>(a.bias + r0);
             // (rows past head_ncls are zero on the device: unconditional loads)
             f4 w2[NC];
 #pragma unroll
@@ -232,7 +234,7 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
             for (int i = 0; i < MB; ++i)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    float v = acc[i][j][e] + bv[e];
+                    float v = acc[i][j][e];
                     if (a.act == ACT_TANH) v = tanh_fast(v);
 #pragma unroll
                     for (int c = 0; c < NC; ++c) part[i][c] = fmaf(w2[c][e], v, part[i][c]);
@@ -619,11 +621,17 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
     }
 
+    // The accumulators start from the bias (rows 4g .. 4g + 3 of each block;
+    // the waves with wk > 0 from zero, their sums are added to wk == 0's), so
+    // the epilogue has no bias to add.
     f4 acc[MB][NB];
 #pragma unroll
-    for (int i = 0; i < MB; ++i)
+    for (int j = 0; j < NB; ++j) {
+        f4 b0 = f4{0.f, 0.f, 0.f, 0.f};
+        if (wk == 0) b0 = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
 #pragma unroll
-        for (int j = 0; j < NB; ++j) acc[i][j] = f4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < MB; ++i) acc[i][j] = b0;
+    }
 
     const u4 *wp = reinterpret_cast<const u4 *>(a.w) + (size_t)nb0 * 64 + lane;
     const size_t wstep = (size_t)a.nbt * 64;  // u4 per K step
@@ -810,9 +818,6 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     auto act = [&](float v) { return act_tanh ? tanh_fast(v) : v; };
     constexpr bool PAIRED = BF && (NB % 2) == 0;
     constexpr int CRUN = PAIRED ? 8 : 4;  // consecutive channels per lane and block (pair)
-    f4 bv[NB];
-#pragma unroll
-    for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const f4 *>(a.bias + (nb0 + j) * 16 + 4 * g);
 
     // LDS [pixel][channel] tile of act(acc + bias) (one 8- or 16-byte write per
     // run), for the restaged stores and the fused pool
@@ -832,8 +837,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                     float h[8];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
-                        h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
+                        h[e] = act(acc[i][2 * p][e]);
+                        h[4 + e] = act(acc[i][2 * p + 1][e]);
                     }
                     u4 pk;
 #pragma unroll
@@ -849,16 +854,16 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                     TC *dst = row + (wn * NB + j) * 16 + 4 * g;
                     if constexpr (BF) {
                         uint2 pk;
-                        pk.x = pack_bf16(act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]));
-                        pk.y = pack_bf16(act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3]));
+                        pk.x = pack_bf16(act(acc[i][j][0]), act(acc[i][j][1]));
+                        pk.y = pack_bf16(act(acc[i][j][2]), act(acc[i][j][3]));
                         if (keys) {
                             pk.x = bf16x2_key(pk.x);
                             pk.y = bf16x2_key(pk.y);
                         }
                         *reinterpret_cast<uint2 *>(dst) = pk;
                     } else {
-                        *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0] + bv[j][0]), act(acc[i][j][1] + bv[j][1]),
-                                                          act(acc[i][j][2] + bv[j][2]), act(acc[i][j][3] + bv[j][3])};
+                        *reinterpret_cast<f4 *>(dst) = f4{act(acc[i][j][0]), act(acc[i][j][1]), act(acc[i][j][2]),
+                                                          act(acc[i][j][3])};
                     }
                 }
             }
@@ -1050,8 +1055,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 float h[8];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    h[e] = act(acc[i][2 * p][e] + bv[2 * p][e]);
-                    h[4 + e] = act(acc[i][2 * p + 1][e] + bv[2 * p + 1][e]);
+                    h[e] = act(acc[i][2 * p][e]);
+                    h[4 + e] = act(acc[i][2 * p + 1][e]);
                 }
                 u4 pk;
 #pragma unroll
@@ -1071,7 +1076,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 if (ch >= a.cout) continue;
                 float v[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e] + bv[j][e]);
+                for (int e = 0; e < 4; ++e) v[e] = act(acc[i][j][e]);
                 if constexpr (BF) {
                     uint2 pk;
                     pk.x = pack_bf16(v[0], v[1]);
