@@ -27,11 +27,13 @@ def border_widths(patch):
 
 
 def mirror_pad(image, patch, mode):
-    """[B, H, W, C] image -> [B, H + w_0 - 1, W + w_0 - 1, C] extended image."""
+    """[B, H, W, C] image -> [B, H + h_0 - 1, W + w_0 - 1, C] extended image
+    (patch: w_0, or (h_0, w_0); each axis is extended for its own side)."""
     if mode not in MODES:
         raise ValueError("mode must be one of %s" % (MODES,))
-    lo, hi = border_widths(patch)
-    return np.pad(np.asarray(image, np.float64), ((0, 0), (lo, hi), (lo, hi), (0, 0)), mode=mode)
+    h0, w0 = (patch, patch) if np.isscalar(patch) else patch
+    (ly, hy), (lx, hx) = border_widths(h0), border_widths(w0)
+    return np.pad(np.asarray(image, np.float64), ((0, 0), (ly, hy), (lx, hx), (0, 0)), mode=mode)
 
 
 def scan_mirrored(layers, params, image, patch, mode, patches=None):

@@ -21,7 +21,9 @@ library:
 Every fragment carries where its pixel (0, 0) lands in the output and the step
 between its neighbouring pixels: the input fragment starts at (0, 0) with step
 1; the child at offset o of a fragment with base b and step t gets base
-b + o*t and step t*k, since its window xbar starts at parent pixel o + k*xbar.
+b + o*t and step t*k, since its window xbar starts at parent pixel o + k*xbar
+(per axis: with a k_y x k_x pool, Section 2's rectangular case, the steps of
+the two axes differ).
 A fragment pixel (y, x) at the end is the patch whose top-left corner is
 (base_y + step*y, base_x + step*x): a crop of a fragment's maps is one patch's
 maps (Section 3).
@@ -31,63 +33,66 @@ import numpy as np
 
 def _conv(a, w, b, act):
     """Valid cross-correlation of one fragment a [h, w, ci] with OIHW weights."""
-    co, ci, k, _ = w.shape
+    co, ci, ky, kx = w.shape
     h, wd, _ = a.shape
-    ho, wo = max(h - k + 1, 0), max(wd - k + 1, 0)
+    ho, wo = max(h - ky + 1, 0), max(wd - kx + 1, 0)
     out = np.empty((ho, wo, co), np.float64)
     out[...] = b
     if ho and wo:
-        for dy in range(k):
-            for dx in range(k):
+        for dy in range(ky):
+            for dx in range(kx):
                 out += a[dy:dy + ho, dx:dx + wo, :] @ w[:, :, dy, dx].T
     if act == "tanh":
         np.tanh(out, out=out)
     return out
 
 
-def _pool_children(a, k):
-    """The k^2 children of fragment a [h, w, c] in offset order (o_y, o_x)."""
+def _pool_children(a, ky, kx):
+    """The ky*kx children of fragment a [h, w, c] in offset order (o_y, o_x)."""
     h, wd, c = a.shape
     kids = []
-    for oy in range(k):
-        for ox in range(k):
-            hc, wc = max((h - oy) // k, 0), max((wd - ox) // k, 0)
+    for oy in range(ky):
+        for ox in range(kx):
+            hc, wc = max((h - oy) // ky, 0), max((wd - ox) // kx, 0)
             m = np.full((hc, wc, c), -np.inf)
-            for i in range(k):
-                for j in range(k):
+            for i in range(ky):
+                for j in range(kx):
                     y0, x0 = oy + i, ox + j
-                    m = np.maximum(m, a[y0:y0 + k * hc:k, x0:x0 + k * wc:k, :][:hc, :wc])
+                    m = np.maximum(m, a[y0:y0 + ky * hc:ky, x0:x0 + kx * wc:kx, :][:hc, :wc])
             kids.append(((oy, ox), m))
     return kids
 
 
 def frag_scan(layers, params, image, patch):
-    """Outputs of the net for every patch of every image, [B, H-w0+1, W-w0+1, n]."""
+    """Outputs of the net for every patch of every image, [B, H-h0+1, W-w0+1, n]
+    (patch: w_0, or (h_0, w_0))."""
     img = np.asarray(image, dtype=np.float64)
     B, H, W, C = img.shape
-    ny, nx = H - patch + 1, W - patch + 1
+    h0, w0 = (patch, patch) if np.isscalar(patch) else patch
+    ny, nx = H - h0 + 1, W - w0 + 1
     n_out = layers[-1]["c_out"]
     res = np.full((B, ny, nx, n_out), np.nan)
     for b in range(B):
-        # (base_y, base_x, step, maps)
-        frags = [(0, 0, 1, img[b])]
+        # (base_y, base_x, step_y, step_x, maps)
+        frags = [(0, 0, 1, 1, img[b])]
         for L, p in zip(layers, params):
             if L["kind"] == "pool":
+                ky, kx = L["k"], L.get("kx", L["k"])
                 nxt = []
-                for (by, bx, t, a) in frags:
-                    for (oy, ox), m in _pool_children(a, L["k"]):
-                        nxt.append((by + oy * t, bx + ox * t, t * L["k"], m))
+                for (by, bx, ty, tx, a) in frags:
+                    for (oy, ox), m in _pool_children(a, ky, kx):
+                        nxt.append((by + oy * ty, bx + ox * tx, ty * ky, tx * kx, m))
                 frags = nxt
             else:
                 w = np.asarray(p[0], np.float64)
                 bias = np.asarray(p[1], np.float64)
-                frags = [(by, bx, t, _conv(a, w, bias, L["act"])) for (by, bx, t, a) in frags]
-        for (by, bx, t, a) in frags:
+                frags = [(by, bx, ty, tx, _conv(a, w, bias, L["act"])) for (by, bx, ty, tx, a) in frags]
+        for (by, bx, ty, tx, a) in frags:
             z = a
             if layers[-1]["act"] == "softmax" and z.size:
                 z = z - z.max(axis=-1, keepdims=True)
                 z = np.exp(z)
                 z = z / z.sum(axis=-1, keepdims=True)
             hf, wf = z.shape[:2]
-            res[b, by:by + t * hf:t, bx:bx + t * wf:t, :] = z
+            res[b, by:by + ty * hf:ty, bx:bx + tx * wf:tx, :] = z
     return res

@@ -17,23 +17,36 @@ integer arithmetic written from the paper:
                     parent*k^2 + o_y*k + o_x, the order of the offset list in
                     Section 2.2.2 (o_x varies fastest); div is floor division
                     and a size never goes below 0
+
+Section 2 writes all of it for square maps and kernels and notes that
+rectangular ones follow directly: a layer's "k" is its rows (the y axis) and
+its optional "kx" its columns; every rule above then holds per axis (a
+k_y x k_x pool has k_y * k_x children, numbered parent*k_y*k_x + o_y*k_x +
+o_x).
   fragment_table    per final fragment: offsets, base output pixel, size,
                     all found by tracking every output pixel
   reassembly_index  per output pixel: (f, y_f, x_f), by tracking
   flops_patch / flops_image   the two formulas of Section 3.1 (Table 2)
   algorithmic_flops exact multiply-add count of the scan: 2 * c_in * k^2 *
-                    c_out per output pixel of every fragment, summed
+                    c_out (k_y * k_x for a rectangular kernel) per output
+                    pixel of every fragment, summed
 """
 import numpy as np
 
 
-def patch_sizes(layers, w0):
-    """[w_0, w_1, ..., w_n] for a patch of size w0; raises on a pool that does
-    not divide its map or a kernel larger than its map."""
+def kyx(L):
+    """(rows, columns) of a layer's kernel or pool."""
+    return L["k"], L.get("kx", L["k"])
+
+
+def patch_sizes(layers, w0, axis=0):
+    """[w_0, w_1, ..., w_n] along one axis (0: rows, 1: columns) for a patch
+    of that size; raises on a pool that does not divide its map or a kernel
+    larger than its map."""
     sizes = [w0]
     w = w0
     for L in layers:
-        k = L["k"]
+        k = kyx(L)[axis]
         if L["kind"] == "pool":
             if w % k:
                 raise ValueError("pool %d does not divide map %d" % (k, w))
@@ -46,12 +59,19 @@ def patch_sizes(layers, w0):
     return sizes
 
 
-def patch_size(layers):
-    """w_0 implied by the stack: walk down from a 1 x 1 final map."""
+def patch_size(layers, axis=0):
+    """w_0 implied by the stack along one axis: walk down from a 1 x 1 final
+    map."""
     w = 1
     for L in reversed(layers):
-        w = w * L["k"] if L["kind"] == "pool" else w + L["k"] - 1
+        k = kyx(L)[axis]
+        w = w * k if L["kind"] == "pool" else w + k - 1
     return w
+
+
+def patch_hw(layers):
+    """(h_0, w_0): the window of a stack with rectangular kernels or pools."""
+    return patch_size(layers, 0), patch_size(layers, 1)
 
 
 def track(layers, Y, X):
@@ -64,10 +84,10 @@ def track(layers, Y, X):
     for L in layers:
         if L["kind"] != "pool":
             continue  # a valid convolution keeps the corner where it is
-        k = L["k"]
-        ox, oy = x % k, y % k
-        x, y = x // k, y // k
-        f = f * k * k + oy * k + ox
+        ky, kx = kyx(L)
+        ox, oy = x % kx, y % ky
+        x, y = x // kx, y // ky
+        f = f * ky * kx + oy * kx + ox
         offs.append((ox, oy))
     return f, y, x, offs
 
@@ -78,16 +98,16 @@ def fragment_extents(layers, H, W):
     frags = [(H, W)]
     out = [list(frags)]
     for L in layers:
-        k = L["k"]
+        ky, kx = kyx(L)
         if L["kind"] == "pool":
             nxt = []
             for (sy, sx) in frags:
-                for oy in range(k):
-                    for ox in range(k):
-                        nxt.append((max((sy - oy) // k, 0), max((sx - ox) // k, 0)))
+                for oy in range(ky):
+                    for ox in range(kx):
+                        nxt.append((max((sy - oy) // ky, 0), max((sx - ox) // kx, 0)))
             frags = nxt
         else:
-            frags = [(max(sy - (k - 1), 0), max(sx - (k - 1), 0)) for (sy, sx) in frags]
+            frags = [(max(sy - (ky - 1), 0), max(sx - (kx - 1), 0)) for (sy, sx) in frags]
         out.append(list(frags))
     return out
 
@@ -96,14 +116,14 @@ def n_fragments(layers):
     F = 1
     for L in layers:
         if L["kind"] == "pool":
-            F *= L["k"] ** 2
+            F *= kyx(L)[0] * kyx(L)[1]
     return F
 
 
 def reassembly_index(layers, H, W):
     """[n_y, n_x, 3] int64 array of (f, y_f, x_f) for every output pixel."""
-    w0 = patch_size(layers)
-    ny, nx = H - w0 + 1, W - w0 + 1
+    h0, w0 = patch_hw(layers)
+    ny, nx = H - h0 + 1, W - w0 + 1
     Y, X = np.meshgrid(np.arange(ny), np.arange(nx), indexing="ij")
     f, y, x, _ = track(layers, Y, X)
     return np.stack([f, y, x], axis=-1)
@@ -114,8 +134,8 @@ def fragment_table(layers, H, W):
        {"offsets": [(o_x, o_y) per pool], "base": (Y0, X0), "size": (h, w)}
     found by tracking every output pixel (a fragment with no valid output does
     not appear)."""
-    w0 = patch_size(layers)
-    ny, nx = H - w0 + 1, W - w0 + 1
+    h0, w0 = patch_hw(layers)
+    ny, nx = H - h0 + 1, W - w0 + 1
     Y, X = np.meshgrid(np.arange(ny), np.arange(nx), indexing="ij")
     f, y, x, offs = track(layers, Y, X)
     table = {}
@@ -157,5 +177,5 @@ def algorithmic_flops(layers, B, H, W):
             res.append(0)
             continue
         pix = sum(sy * sx for (sy, sx) in ext[l + 1])
-        res.append(B * pix * 2 * L["c_in"] * L["k"] ** 2 * L["c_out"])
+        res.append(B * pix * 2 * L["c_in"] * kyx(L)[0] * kyx(L)[1] * L["c_out"])
     return res

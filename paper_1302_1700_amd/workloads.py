@@ -25,16 +25,23 @@ from dataclasses import dataclass, field
 import numpy as np
 
 
-def conv(k, c_in, c_out, act="tanh"):
-    return {"kind": "conv", "k": k, "c_in": c_in, "c_out": c_out, "act": act}
+def _layer(kind, k, c_in, c_out, act, kx):
+    L = {"kind": kind, "k": k, "c_in": c_in, "c_out": c_out, "act": act}
+    if kx is not None and kx != k:
+        L["kx"] = kx  # columns of a rectangular kernel / pool (k: its rows)
+    return L
 
 
-def pool(k, c):
-    return {"kind": "pool", "k": k, "c_in": c, "c_out": c, "act": "none"}
+def conv(k, c_in, c_out, act="tanh", kx=None):
+    return _layer("conv", k, c_in, c_out, act, kx)
 
 
-def fc(k, c_in, c_out, act="tanh"):
-    return {"kind": "fc", "k": k, "c_in": c_in, "c_out": c_out, "act": act}
+def pool(k, c, kx=None):
+    return _layer("pool", k, c, c, "none", kx)
+
+
+def fc(k, c_in, c_out, act="tanh", kx=None):
+    return _layer("fc", k, c_in, c_out, act, kx)
 
 
 def n4_layers():
@@ -119,8 +126,8 @@ def make_weights(layers, seed, sigma, zero_bias=False):
         if L["kind"] == "pool":
             params.append(None)
             continue
-        k, ci, co = L["k"], L["c_in"], L["c_out"]
-        w = rng.normal(0.0, sigma, size=(co, ci, k, k)).astype(np.float32)
+        ky, kx, ci, co = L["k"], L.get("kx", L["k"]), L["c_in"], L["c_out"]
+        w = rng.normal(0.0, sigma, size=(co, ci, ky, kx)).astype(np.float32)
         if zero_bias:
             b = np.zeros(co, np.float32)
         else:
@@ -176,3 +183,35 @@ def random_net(rng, max_layers=6, max_c=6, allow_pools=True):
             w = w + L["k"] - 1
     layers[-2]["k"] = w_L
     return layers, w, c_in0
+
+
+def random_rect_net(rng, max_layers=6, max_c=5):
+    """A random stack with rectangular kernels and pools (k: rows, kx:
+    columns, drawn independently).  Returns (layers, (h0, w0), c_in)."""
+    n_cls = int(rng.integers(2, 4))
+    c = int(rng.integers(1, max_c + 1))
+    c_in0 = c
+    layers = []
+    for _ in range(int(rng.integers(1, max_layers))):
+        if rng.random() < 0.45:
+            ky, kx = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+            if ky * kx == 1:
+                kx = 2
+            layers.append(pool(ky, c, kx=kx))
+        else:
+            co = int(rng.integers(1, max_c + 1))
+            layers.append(conv(int(rng.integers(1, 5)), c, co, "tanh" if rng.random() < 0.7 else "none",
+                               kx=int(rng.integers(1, 5))))
+            c = co
+    hidden = int(rng.integers(2, 6))
+    hy, hx = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+    layers.append(fc(hy, c, hidden, "tanh", kx=hx))
+    layers.append(fc(1, hidden, n_cls, "softmax"))
+    h, w = hy, hx
+    for L in reversed(layers[:-2]):
+        ky, kx = L["k"], L.get("kx", L["k"])
+        if L["kind"] == "pool":
+            h, w = h * ky, w * kx
+        else:
+            h, w = h + ky - 1, w + kx - 1
+    return layers, (h, w), c_in0

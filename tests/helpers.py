@@ -4,18 +4,23 @@ import torch
 import torch.nn.functional as F
 
 
+def _k(L):
+    """(rows, columns) of a layer's kernel or pool."""
+    return L["k"], L.get("kx", L["k"])
+
+
 def torch_patch_net(layers, params, crop):
     """The net on one patch with torch CPU library routines, float64.
-    crop: [w0, w0, C] -> returns [n_out]."""
+    crop: [h0, w0, C] -> returns [n_out]."""
     x = torch.from_numpy(np.asarray(crop, np.float64)).permute(2, 0, 1)[None]
     for L, p in zip(layers, params):
         if L["kind"] == "pool":
-            x = F.max_pool2d(x, L["k"])
+            x = F.max_pool2d(x, _k(L))
         else:
             w = torch.from_numpy(np.asarray(p[0], np.float64))
             b = torch.from_numpy(np.asarray(p[1], np.float64))
             if L["kind"] == "fc":
-                assert x.shape[-1] == L["k"] and x.shape[-2] == L["k"]
+                assert (x.shape[-2], x.shape[-1]) == _k(L)
                 x = F.linear(x.reshape(1, -1), w.reshape(w.shape[0], -1), b)[:, :, None, None]
             else:
                 x = F.conv2d(x, w, b)
@@ -30,19 +35,20 @@ def torch_patch_net(layers, params, crop):
 def dilated_scan(layers, params, image):
     """Whole-map formulation with dilated library convolutions: a conv after
     pools of cumulative stride S is a convolution with dilation S, a k-pool is
-    a stride-1 max-pool with dilation S, and then S grows by k.  Output index =
-    patch top-left corner.  [B,H,W,C] -> [B, H-w0+1, W-w0+1, n]."""
+    a stride-1 max-pool with dilation S, and then S grows by k (per axis).
+    Output index = patch top-left corner.  [B,H,W,C] -> [B, H-h0+1, W-w0+1, n]."""
     x = torch.from_numpy(np.asarray(image, np.float64)).permute(0, 3, 1, 2)
-    S = 1
+    Sy = Sx = 1
     for L, p in zip(layers, params):
-        k = L["k"]
+        ky, kx = _k(L)
         if L["kind"] == "pool":
-            x = F.max_pool2d(x, k, stride=1, dilation=S)
-            S *= k
+            x = F.max_pool2d(x, (ky, kx), stride=1, dilation=(Sy, Sx))
+            Sy *= ky
+            Sx *= kx
         else:
             w = torch.from_numpy(np.asarray(p[0], np.float64))
             b = torch.from_numpy(np.asarray(p[1], np.float64))
-            x = F.conv2d(x, w, b, dilation=S)
+            x = F.conv2d(x, w, b, dilation=(Sy, Sx))
             if L["act"] == "tanh":
                 x = torch.tanh(x)
     if layers[-1]["act"] == "softmax":

@@ -20,20 +20,32 @@ from helpers import dilated_scan, torch_patch_net
 SRC = os.path.join(os.path.dirname(oracle.__file__), "patch_oracle.c")
 
 MUTATIONS = {
-    "kernel_flipped": ("* a[((size_t)ci * w + y + dy) * w + x + dx]",
-                       "* a[((size_t)ci * w + y + (k - 1 - dy)) * w + x + (k - 1 - dx)]"),
+    "kernel_flipped": ("* a[((size_t)ci * h + y + dy) * w + x + dx]",
+                       "* a[((size_t)ci * h + y + (ky - 1 - dy)) * w + x + (kx - 1 - dx)]"),
     "bias_dropped": ("double s = L->b ? L->b[co] : 0.0;", "double s = 0.0;"),
-    "crop_transposed": ("a[((size_t)c * w0 + y) * w0 + x] =", "a[((size_t)c * w0 + x) * w0 + y] ="),
-    "pool_window_short": ("for (int i = 0; i < k; ++i)\n                        for (int j = 0; j < k; ++j) {",
-                          "for (int i = 0; i < k - 1; ++i)\n                        for (int j = 0; j < k - 1; ++j) {"),
-    "weight_axes_swapped": ("L->w[(((size_t)co * L->c_in + ci) * k + dy) * k + dx]",
-                            "L->w[(((size_t)ci * L->c_out + co) * k + dy) * k + dx]"),
+    "crop_transposed": ("a[((size_t)c * h0 + y) * w0 + x] =", "a[((size_t)c * h0 + x) * w0 + y] ="),
+    "pool_window_short": ("for (int i = 0; i < ky; ++i)\n                        for (int j = 0; j < kx; ++j) {",
+                          "for (int i = 0; i < ky - 1; ++i)\n                        for (int j = 0; j < kx - 1; ++j) {"),
+    "weight_axes_swapped": ("L->w[(((size_t)co * L->c_in + ci) * ky + dy) * kx + dx]",
+                            "L->w[(((size_t)ci * L->c_out + co) * ky + dy) * kx + dx]"),
+    "kernel_rows_cols_swapped": ("L->w[(((size_t)co * L->c_in + ci) * ky + dy) * kx + dx]",
+                                 "L->w[(((size_t)co * L->c_in + ci) * kx + dx) * ky + dy]"),
+    "pool_rows_cols_swapped": ("double m = a[((size_t)c * h + ky * y) * w + kx * x];",
+                               "double m = a[((size_t)c * h + kx * y) * w + ky * x];"),
     "activation_on_softmax_layer": ("if (L->act == O_ACT_TANH) s = tanh(s);",
                                     "if (L->act != O_ACT_NONE) s = tanh(s);"),
     "softmax_unnormalised": ("for (int i = 0; i < n; ++i) z[i] /= s;", "for (int i = 0; i < n; ++i) z[i] /= 1.0;"),
     "corner_swapped": ("int b = patches[3 * p], Y = patches[3 * p + 1], X = patches[3 * p + 2];",
                        "int b = patches[3 * p], X = patches[3 * p + 1], Y = patches[3 * p + 2];"),
 }
+
+# a net with rectangular kernels and pools (Section 2: the square case
+# generalizes directly); its window is 7 x 11
+RECT_NET = [{"kind": "conv", "k": 2, "kx": 3, "c_in": 2, "c_out": 3, "act": "tanh"},
+            {"kind": "pool", "k": 2, "kx": 3, "c_in": 3, "c_out": 3, "act": "none"},
+            {"kind": "conv", "k": 3, "kx": 2, "c_in": 3, "c_out": 4, "act": "tanh"},
+            {"kind": "pool", "k": 1, "kx": 2, "c_in": 4, "c_out": 4, "act": "none"},
+            {"kind": "fc", "k": 1, "kx": 1, "c_in": 4, "c_out": 3, "act": "softmax"}]
 
 
 def _build_mutant(tmp_path, name):
@@ -49,8 +61,21 @@ def _build_mutant(tmp_path, name):
 
 
 def _pins_fail(lib):
-    """Run a battery of the pins against a (mutated) oracle build; True if any
-    of them fails."""
+    """Run the battery of pins against a (mutated) oracle build in a fresh
+    Python process; True if any of them fails or the build crashes (a mutated
+    index can leave its buffers)."""
+    import sys
+    here = os.path.dirname(os.path.abspath(__file__))
+    code = ("import sys; sys.path[:0] = [%r, %r]; from test_oracle_mutations import _battery; "
+            "sys.exit(1 if _battery(%r) else 0)" % (here, os.path.dirname(here), lib))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, timeout=300)
+    if r.returncode not in (0, 1):
+        return True  # crashed
+    return r.returncode == 1
+
+
+def _battery(lib):
+    """The pins against one oracle build; True if any of them fails."""
     fails = []
     try:
         # single window == torch library net (workload 1, 3 and a random net)
@@ -69,6 +94,13 @@ def _pins_fail(lib):
         img = wl.make_image(3, 1, w0 + 6, w0 + 9, c0)
         got = oracle.patch_forward(layers, params, img, w0, lib_path=lib)
         fails.append(np.abs(got - dilated_scan(layers, params, img)).max() > 1e-12)
+        # rectangular kernels and pools: one window == torch library net, the
+        # whole map == dilated formulation
+        params = wl.make_weights(RECT_NET, 5, 0.6)
+        img = wl.make_image(4, 1, 7 + 5, 11 + 4, 2)
+        got = oracle.patch_forward(RECT_NET, params, img, (7, 11), lib_path=lib)
+        fails.append(np.abs(got[0, 0, 0] - torch_patch_net(RECT_NET, params, img[0, :7, :11])).max() > 1e-12)
+        fails.append(np.abs(got - dilated_scan(RECT_NET, params, img)).max() > 1e-12)
         # hand-evaluated ramp (box sums and a max-pool)
         ramp = (10.0 * np.arange(5)[:, None] + np.arange(5)[None, :]).reshape(1, 5, 5, 1)
         lay = [wl.conv(2, 1, 1, "none"), wl.pool(2, 1), wl.fc(1, 1, 1, "none")]

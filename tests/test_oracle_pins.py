@@ -264,3 +264,55 @@ def test_frag_cpu_workload5_net_sample():
     pts = np.stack([np.zeros(64, int), rng.integers(0, 40, 64), rng.integers(0, 30, 64)], 1)
     ref = oracle.patch_forward(w.layers, params, img, w.patch, pts)
     assert np.abs(got[0, pts[:, 1], pts[:, 2]] - ref).max() <= 1e-12
+
+
+# ---- Rectangular kernels and pools (Section 2: the square case generalizes
+# ---- directly; every rule holds per axis) -----------------------------------
+
+@pytest.mark.parametrize("seed", range(16))
+def test_rect_sizes_counts_and_coverage(seed):
+    rng = np.random.default_rng(1500 + seed)
+    layers, (h0, w0), _ = wl.random_rect_net(rng)
+    assert ix.patch_hw(layers) == (h0, w0)
+    assert ix.patch_sizes(layers, h0, 0)[-1] == 1 == ix.patch_sizes(layers, w0, 1)[-1]
+    prod = 1
+    for L in layers:
+        if L["kind"] == "pool":
+            prod *= L["k"] * L.get("kx", L["k"])
+    H, W = h0 + int(rng.integers(0, 11)), w0 + int(rng.integers(0, 11))
+    ext = ix.fragment_extents(layers, H, W)
+    assert len(ext[-1]) == prod == ix.n_fragments(layers)
+    for frags in ext:
+        ys, xs = [e[0] for e in frags], [e[1] for e in frags]
+        assert max(ys) - min(ys) <= 1 and max(xs) - min(xs) <= 1
+    idx = ix.reassembly_index(layers, H, W).reshape(-1, 3)
+    keys = set(map(tuple, idx.tolist()))
+    assert len(keys) == idx.shape[0] == (H - h0 + 1) * (W - w0 + 1)
+    assert sum(a * b for a, b in ext[-1]) == len(keys)
+    for f, e in ix.fragment_table(layers, H, W).items():
+        assert e["size"] == ext[-1][f]
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_rect_window_equals_library_net(seed):
+    rng = np.random.default_rng(1600 + seed)
+    layers, (h0, w0), c0 = wl.random_rect_net(rng)
+    params = wl.make_weights(layers, seed, 0.5)
+    img = wl.make_image(seed, 1, h0, w0, c0)
+    got = oracle.patch_forward(layers, params, img, (h0, w0))[0, 0, 0]
+    assert np.abs(got - torch_patch_net(layers, params, img[0])).max() <= 1e-12
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_rect_whole_map_and_frag_cpu(seed):
+    """Whole map == the dilated library formulation, and the fragment method
+    on the CPU == the per-window definition, with rectangular layers."""
+    rng = np.random.default_rng(1700 + seed)
+    layers, (h0, w0), c0 = wl.random_rect_net(rng)
+    params = wl.make_weights(layers, seed, 0.5)
+    img = wl.make_image(seed, 2, h0 + int(rng.integers(0, 9)), w0 + int(rng.integers(0, 9)), c0)
+    ref = oracle.patch_forward(layers, params, img, (h0, w0))
+    assert np.abs(ref - dilated_scan(layers, params, img)).max() <= 1e-12
+    got = oracle.frag_cpu.frag_scan(layers, params, img, (h0, w0))
+    assert not np.isnan(got).any()
+    assert np.abs(got - ref).max() <= 1e-12
