@@ -23,6 +23,10 @@
  *   - Fragment ids follow the offset order of Section 2.2.2 (o_x fastest):
  *     the child of fragment f at pooling offset (o_x, o_y) of a k x k pool is
  *     f * k^2 + o_y * k + o_x, starting from fragment 0 (the whole image).
+ *   - Rectangular kernels, pools and windows (Section 2: the square case
+ *     generalises directly): a layer's k_x gives its columns, the window is
+ *     h_0 x w_0, and every rule above holds per axis, rows with h_0 and k,
+ *     columns with w_0 and k_x (a k x k_x pool has k * k_x children).
  *
  * Errors: every call returns an fs_status and never throws or aborts across
  * this boundary; fs_last_error() gives a thread-local message for the last
@@ -75,8 +79,12 @@ typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
 /* One layer.  For FS_MAXPOOL: k = pool size, c_in = c_out = channels, weight
  * and bias NULL, act FS_ACT_NONE.  For FS_CONV / FS_FC: k = kernel size
  * (FS_FC may pass 0 to take the size of the map it receives), weight = host
- * OIHW [c_out][c_in][k][k] float32, bias = host [c_out] float32 or NULL for
- * zeros.  Host arrays are copied by fs_net_create and not kept. */
+ * OIHW [c_out][c_in][k][k_x] float32, bias = host [c_out] float32 or NULL for
+ * zeros.  Host arrays are copied by fs_net_create and not kept.
+ * k_x: the kernel's or pool's columns when they differ from its rows k
+ * (Section 2: the square case generalises directly to rectangles, each rule
+ * holding per axis); 0 means k_x = k.  An FS_FC layer passing k = 0 passes
+ * k_x = 0 too. */
 typedef struct {
     int32_t kind;
     int32_t k;
@@ -85,24 +93,27 @@ typedef struct {
     int32_t act;
     const float *weight;
     const float *bias;
+    int32_t k_x;
 } fs_layer;
 
 typedef struct {
-    int32_t patch;        /* w_0 */
+    int32_t patch;        /* w_0 (rectangular windows: h_0, the rows) */
     int32_t in_channels;  /* C */
     int32_t n_classes;    /* c_out of the last layer */
     int32_t n_layers;
     int32_t n_pools;
     int32_t stride;       /* product of pool sizes: output pixels one final
-                             fragment pixel step covers, per axis */
+                             fragment pixel step covers, per axis (rows) */
     int32_t n_fragments;  /* F_L, the product of the squared pool sizes
-                             (Section 3) */
+                             (Section 3; rectangular pools: of k * k_x) */
     int32_t dtype;        /* fs_dtype */
+    int32_t patch_x;      /* the window's columns (= patch for square nets) */
+    int32_t stride_x;     /* product of the pools' columns k_x */
 } fs_net_info;
 
 typedef struct {
     int32_t batch;
-    int32_t out_h;           /* H - w_0 + 1 */
+    int32_t out_h;           /* H - h_0 + 1 (h_0 = w_0 for square windows) */
     int32_t out_w;           /* W - w_0 + 1 */
     int32_t n_launches;      /* kernel launches fs_scan enqueues */
     size_t workspace_bytes;  /* device workspace fs_scan needs */
@@ -136,7 +147,9 @@ typedef struct {
  * one or more fully connected layers (Section 2); channels must chain; every
  * pool must divide the patch-level map it receives (Section 2.1.2:
  * mod(w_{l-1}, k) = 0); the patch-level map after the last layer must be
- * 1 x 1.  `patch` is w_0 (0: derive it from the stack).  A patch that does
+ * 1 x 1.  `patch` is w_0 (0: derive it from the stack; a rectangular stack,
+ * whose window is h_0 x w_0 with h_0 != w_0, must pass 0 and give its fully
+ * connected sizes).  A patch that does
  * not agree with the stack gives FS_ERR_SHAPE; more than 16384 channels in a
  * layer gives FS_ERR_UNSUPPORTED.  Weights are converted (and
  * for FS_BF16 rounded) and uploaded to the current HIP device, which the net
@@ -247,8 +260,9 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
  * f = 0 .. F_L - 1 a record of 5 + 2 * n_pools int32:
  *   f, h_f, w_f, Y0, X0, then (o_x, o_y) of each pool in layer order,
  * where (h_f, w_f) is the fragment's size after the last layer (Eqs. 3-4 and
- * 6-7, never below 0) and output pixel (Y0 + stride * y, X0 + stride * x)
- * holds the fragment's pixel (y, x).  Host output; writes at most `capacity`
+ * 6-7, never below 0) and output pixel (Y0 + stride * y, X0 + stride_x * x)
+ * holds the fragment's pixel (y, x).  The children of fragment f of a
+ * k x k_x pool are f * k * k_x + o_y * k_x + o_x.  Host output; writes at most `capacity`
  * int32 and stores the number the full table needs in *n_needed (n_needed
  * may be NULL; h_out may be NULL to query the size). */
 fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_out,
@@ -258,7 +272,7 @@ fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_
  * (Y, X), the triple (f, y, x): the final fragment and the position in it
  * that holds the window with top-left corner (Y, X) (Section 3: the union of
  * all fragments covers every window).  Host output, same size protocol as
- * fs_fragment_table (3 * (H - w_0 + 1) * (W - w_0 + 1) int32). */
+ * fs_fragment_table (3 * (H - h_0 + 1) * (W - w_0 + 1) int32). */
 fs_status fs_reassembly_index(const fs_net *net, int32_t H, int32_t W, int32_t *h_out,
                               size_t capacity, size_t *n_needed);
 

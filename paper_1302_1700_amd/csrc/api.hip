@@ -55,7 +55,8 @@ uint16_t host_f2bf(float f)
 
 struct NetLayer {
     int kind, k, cin, cout, act;
-    int w_in, w_out;      // patch-level map sizes (Sections 2.1.1, 2.1.2)
+    int kx;               // columns of the kernel / pool (k: its rows; Section 2's rectangular case)
+    int h_in, h_out, w_in, w_out;  // patch-level map sizes (Sections 2.1.1, 2.1.2)
     // conv launch parameters fixed at creation
     bool vec = false;     // channel-vector path
     int nb = 1;           // output-channel blocks per wave
@@ -72,9 +73,10 @@ struct NetLayer {
 
 struct fs_net {
     std::vector<NetLayer> L;
-    int patch = 0, C = 0, dtype = 0, ncls = 0;
-    std::vector<int> pool_k;
-    int S = 1, F = 1;
+    int patch = 0, C = 0, dtype = 0, ncls = 0;  // patch: window rows h_0
+    int patch_x = 0;                             // window columns w_0
+    std::vector<int> pool_k, pool_kx;            // pool rows, columns, in layer order
+    int S = 1, Sx = 1, F = 1;                    // products of the pool rows / columns; fragments
     int device = 0;
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
@@ -117,7 +119,7 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
     const int KSTEP = kstep_of(dtype), LPE = KSTEP / 4, es = elem_of(dtype);
     const size_t n = (size_t)l.ksteps * l.nbt * 64 * LPE;
     out.assign(n * es, 0);
-    const int taps = l.k * l.k;
+    const int taps = l.k * l.kx;
     for (int s = 0; s < l.ksteps; ++s)
         for (int nb = 0; nb < l.nbt; ++nb)
             for (int lane = 0; lane < 64; ++lane)
@@ -136,8 +138,8 @@ void pack_conv_weights(const NetLayer &l, const float *w, int dtype, std::vector
                     }
                     float v = 0.f;
                     if (co < l.cout && tap < taps) {
-                        const int dy = tap / l.k, dx = tap % l.k;
-                        v = w[(((size_t)co * l.cin + ci) * l.k + dy) * l.k + dx];
+                        const int dy = tap / l.kx, dx = tap % l.kx;
+                        v = w[(((size_t)co * l.cin + ci) * l.k + dy) * l.kx + dx];
                     }
                     const size_t idx = (((size_t)s * l.nbt + nb) * 64 + lane) * LPE + e;
                     if (dtype == DT_BF16) {
@@ -201,7 +203,7 @@ void choose_channel_tile(int nbt, bool vec, int *nb, int *wn)
 // ---------------------------------------------------------------------------
 
 struct Geo {  // fragment set entering a layer
-    int Q = 1;                    // fragments per axis; F = Q * Q per image
+    int Qy = 1, Qx = 1;           // fragments per axis; F = Qy * Qx per image
     std::vector<int> ey, ex;      // true sizes per y / x index
     int hmax = 0, wmax = 0, C = 0;
     bool is_image = true;         // the input image (float32 even in bf16 nets)
@@ -250,10 +252,8 @@ size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 void fill_axis(AxisTable &t, const Geo &g)
 {
     std::memset(&t, 0, sizeof t);
-    for (int i = 0; i < g.Q; ++i) {
-        t.y[i] = (uint16_t)g.ey[i];
-        t.x[i] = (uint16_t)g.ex[i];
-    }
+    for (int i = 0; i < g.Qy; ++i) t.y[i] = (uint16_t)g.ey[i];
+    for (int i = 0; i < g.Qx; ++i) t.x[i] = (uint16_t)g.ex[i];
 }
 
 long long true_pixels(const Geo &g)
@@ -278,29 +278,33 @@ void plan_run_tiles(const NetLayer &l, const Geo &in, int mt, int cs, int es, in
 {
     if (const char *e = getenv("FRAGSCAN_RUN"); e && e[0] == '0') return;
     if (!conv_tile_supported(L.mb, l.nb, l.wn, l.wk, l.vec, true)) return;
-    const int k = l.k;
-    if (in.Q > kMaxAxis) return;
+    const int ky = l.k, kx = l.kx;
+    if (in.Qy > kMaxAxis || in.Qx > kMaxAxis) return;
     long long sy = 0, sx = 0;
     int hmin = 1 << 30, wmin = 1 << 30, wmax = 0;
     ConvArgs &a = L.conv;
     a.run_ypre[0] = a.run_xpre[0] = 0;
-    for (int i = 0; i < in.Q; ++i) {
-        const int ho = in.ey[i] - k + 1, wo = in.ex[i] - k + 1;
+    for (int i = 0; i < in.Qy; ++i) {
+        const int ho = in.ey[i] - ky + 1;
         hmin = std::min(hmin, ho);
+        sy += std::max(ho, 0);
+        if (sy >= 65536) return;  // uint16 prefix sums
+        a.run_ypre[i + 1] = (uint16_t)sy;
+    }
+    for (int i = 0; i < in.Qx; ++i) {
+        const int wo = in.ex[i] - kx + 1;
         wmin = std::min(wmin, wo);
         wmax = std::max(wmax, wo);
-        sy += std::max(ho, 0);
         sx += std::max(wo, 0);
-        if (sy >= 65536 || sx >= 65536) return;  // uint16 prefix sums
-        a.run_ypre[i + 1] = (uint16_t)sy;
+        if (sx >= 65536) return;
         a.run_xpre[i + 1] = (uint16_t)sx;
     }
     if (hmin <= 0 || wmin <= 0 || (long long)hmin * wmin < mt || sy * sx >= (1LL << 31)) return;
     // window rows of a tile: n0 pixels of one fragment from any column span
     // at most (n0 + w - 2) / w + 1 output rows, the n1 = mt - n0 of the next
-    // (from its column 0) (n1 - 1) / w + 1, each plus k - 1
-    const int rows = (mt + wmin - 1) / wmin + 2 * k;
-    const size_t lds = offtab + (size_t)rows * (wmax + k - 1) * cs * es;
+    // (from its column 0) (n1 - 1) / w + 1, each plus k_y - 1
+    const int rows = (mt + wmin - 1) / wmin + 2 * ky;
+    const size_t lds = offtab + (size_t)rows * (wmax + kx - 1) * cs * es;
     const size_t need = std::max(std::max(lds, other), (size_t)a.lds_bytes);
     if (need > kMaxLdsBytes) return;
     L.frag_tiles = a.tiles_per_band;
@@ -315,8 +319,8 @@ void plan_run_tiles(const NetLayer &l, const Geo &in, int mt, int cs, int es, in
 // Tile choice for a conv launch (the tiling itself is described in conv_impl.h).
 fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, Launch &L)
 {
-    const int k = l.k;
-    const int hout_max = in.hmax - k + 1, wout_max = in.wmax - k + 1;
+    const int ky = l.k, kx = l.kx;
+    const int hout_max = in.hmax - ky + 1, wout_max = in.wmax - kx + 1;
     const int es = elem_of(net->dtype);
     const int KSTEP = kstep_of(net->dtype);
     // pixel stride in LDS: +16 bytes per pixel spreads 16 consecutive pixels'
@@ -329,12 +333,12 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     // distinct output widths present; every fragment's output height and width
     std::vector<int> wouts, houts, wouts_all;
     for (int v : in.ex)
-        if (v - k + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - k + 1) == wouts.end())
-            wouts.push_back(v - k + 1);
+        if (v - kx + 1 > 0 && std::find(wouts.begin(), wouts.end(), v - kx + 1) == wouts.end())
+            wouts.push_back(v - kx + 1);
     for (int v : in.ey)
-        if (v - k + 1 > 0) houts.push_back(v - k + 1);
+        if (v - ky + 1 > 0) houts.push_back(v - ky + 1);
     for (int v : in.ex)
-        if (v - k + 1 > 0) wouts_all.push_back(v - k + 1);
+        if (v - kx + 1 > 0) wouts_all.push_back(v - kx + 1);
     const int wm = 4 / (l.wn * l.wk);
     int mb_force = 0, band_force = 0, lds_min = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force, nullptr, &lds_min);
@@ -376,7 +380,7 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
             // of every workgroup.  Row tiles (several bands): rows_t = mt /
             // band_w whole band rows, the same window rows in every band.
             // (the window of a tile in a band of width t spans the rows its
-            // pixels touch plus k - 1, and t + k - 1 columns: the largest over
+            // pixels touch plus k_y - 1, and t + k_x - 1 columns: the largest over
             // the bands present and the tile starts i * mt, which repeat
             // with period t)
             size_t lds_p = 0;
@@ -386,11 +390,11 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
                     if (t <= 0) break;
                     int span = 0;
                     for (int i = 0; i < t; ++i) span = std::max(span, (int)(((long long)i * mt) % t + mt - 1) / t + 1);
-                    const int rows = std::min(span + k - 1, in.hmax);
-                    lds_p = std::max(lds_p, offtab + (size_t)rows * (t + k - 1) * cs * es);
+                    const int rows = std::min(span + ky - 1, in.hmax);
+                    lds_p = std::max(lds_p, offtab + (size_t)rows * (t + kx - 1) * cs * es);
                 }
             const int rows_t = (nbands > 1 && mt >= band_w) ? mt / band_w : 0;
-            const size_t lds_r = rows_t ? offtab + (size_t)std::min(rows_t + k - 1, in.hmax) * (band_w + k - 1) * cs * es
+            const size_t lds_r = rows_t ? offtab + (size_t)std::min(rows_t + ky - 1, in.hmax) * (band_w + kx - 1) * cs * es
                                         : lds_p;
             if (std::min(lds_p, lds_r) > 96 * 1024) {
                 if (band_w <= 8) break;
@@ -449,19 +453,19 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile fits in LDS", L.layer);
 }
 
-// Children of a k x k pool (Eqs. 5-7): per axis, parent index i and offset
-// o give child i*k + o of size floor((s - o) / k).
-Geo pool_geo(const Geo &g, int k)
+// Children of a ky x kx pool (Eqs. 5-7, per axis): parent index i and
+// offset o give child i*k + o of size floor((s - o) / k).
+Geo pool_geo(const Geo &g, int ky, int kx)
 {
     Geo o;
-    o.Q = g.Q * k;
-    o.ey.assign(o.Q, 0);
-    o.ex.assign(o.Q, 0);
-    for (int i = 0; i < g.Q; ++i)
-        for (int off = 0; off < k; ++off) {
-            o.ey[i * k + off] = std::max(g.ey[i] - off, 0) / k;
-            o.ex[i * k + off] = std::max(g.ex[i] - off, 0) / k;
-        }
+    o.Qy = g.Qy * ky;
+    o.Qx = g.Qx * kx;
+    o.ey.assign(o.Qy, 0);
+    o.ex.assign(o.Qx, 0);
+    for (int i = 0; i < g.Qy; ++i)
+        for (int off = 0; off < ky; ++off) o.ey[i * ky + off] = std::max(g.ey[i] - off, 0) / ky;
+    for (int i = 0; i < g.Qx; ++i)
+        for (int off = 0; off < kx; ++off) o.ex[i * kx + off] = std::max(g.ex[i] - off, 0) / kx;
     o.C = g.C;
     o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
     o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
@@ -469,19 +473,20 @@ Geo pool_geo(const Geo &g, int k)
     return o;
 }
 
-// Tiles of a convolution with the following k x k pool fused in (kernel:
-// conv_impl.h, pool_k > 0).  Bands of ~16 columns of the stride-1 max filter;
-// a tile holds pool_rt filter rows, i.e. (pool_rt + kp - 1) x (band + kp - 1)
-// convolution outputs, which must fit the register tile (mt pixels).
-fs_status plan_conv_pool_tiles(const fs_net *net, const NetLayer &l, const Geo &in, int kp, Launch &L)
+// Tiles of a convolution with the following kpy x kpx pool fused in (kernel:
+// conv_impl.h, pool_ky > 0).  Bands of ~16 columns of the stride-1 max
+// filter; a tile holds pool_rt filter rows, i.e. (pool_rt + kpy - 1) x
+// (band + kpx - 1) convolution outputs, which must fit the register tile (mt
+// pixels).
+fs_status plan_conv_pool_tiles(const fs_net *net, const NetLayer &l, const Geo &in, int kpy, int kpx, Launch &L)
 {
-    const int k = l.k;
+    const int ky = l.k, kx = l.kx;
     const int es = elem_of(net->dtype);
     const int KSTEP = kstep_of(net->dtype);
     const int pad = 16 / es;
     const int cs = l.vec ? l.cin + pad : l.cin;
     const int offtab = l.vec ? 0 : (int)align_up((size_t)l.ksteps * KSTEP * 4, 16);
-    const int hM_max = in.hmax - k + 1 - kp + 1, wM_max = in.wmax - k + 1 - kp + 1;
+    const int hM_max = in.hmax - ky + 1 - kpy + 1, wM_max = in.wmax - kx + 1 - kpx + 1;
     const int wm = 4 / (l.wn * l.wk);
     int mb_force = 0, band_force = 0;
     tile_override(L.layer, &mb_force, nullptr, nullptr, &band_force);
@@ -498,10 +503,10 @@ fs_status plan_conv_pool_tiles(const fs_net *net, const NetLayer &l, const Geo &
         if (band_force) nbands = (wmax + band_force - 1) / band_force;
         for (; nbands <= wmax; ++nbands) {
             const int band_w = (wmax + nbands - 1) / nbands;
-            const int ew = band_w + kp - 1;
-            const int rt = std::min(mt / ew - (kp - 1), hmax);
+            const int ew = band_w + kpx - 1;
+            const int rt = std::min(mt / ew - (kpy - 1), hmax);
             if (rt < 1) continue;  // narrower bands
-            const size_t win = offtab + (size_t)(rt + kp - 1 + k - 1) * (ew + k - 1) * cs * es;
+            const size_t win = offtab + (size_t)(rt + kpy - 1 + ky - 1) * (ew + kx - 1) * cs * es;
             const size_t tile = (size_t)mt * (l.wn * l.nb * 16 + pad) * es;
             const size_t part = (size_t)(l.wk - 1) * (4 / l.wk) * mb * l.nb * 4 * 64 * 4;
             const size_t need = std::max(std::max(win, tile), part);
@@ -541,22 +546,37 @@ bool want_pool_fusion(const fs_net *net, int li)
     const NetLayer &l = net->L[li], &p = net->L[li + 1];
     if (l.kind == FS_MAXPOOL || p.kind != FS_MAXPOOL || l.nbt != l.nb * l.wn) return false;
     if (const char *e = getenv("FRAGSCAN_POOL_FUSE"); e && e[0]) return e[0] == '1';
-    const double ov = p.k == 2 ? 0.35 : 0.5;
+    const double ov = (p.k == 2 && p.kx == 2) ? 0.35 : 0.5;
     const double ridge = net->dtype == DT_BF16 ? 2516.6e12 / 8e12 : 157.3e12 / 8e12;  // FLOP per byte
-    return (double)l.cin * l.k * l.k * ov < elem_of(net->dtype) * ridge;
+    return (double)l.cin * l.k * l.kx * ov < elem_of(net->dtype) * ridge;
+}
+
+// First output coordinate (along one axis) of the final fragments' axis
+// index f: its offsets at the successive pools, sizes ks (first pool first),
+// are the mixed-radix digits of f read most significant first, and the
+// window offset they select is sum o_m * (k_1 * ... * k_{m-1}).
+int axis_base(const std::vector<int> &ks, int S, int f)
+{
+    int rest = f, base = 0;
+    for (int m = (int)ks.size() - 1; m >= 0; --m) {
+        S /= ks[m];
+        base += (rest % ks[m]) * S;
+        rest /= ks[m];
+    }
+    return base;
 }
 
 fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View *view = nullptr)
 {
     if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
-    if (H < net->patch || W < net->patch)
-        return fail(FS_ERR_SHAPE, "image %dx%d smaller than the patch size %d", H, W, net->patch);
+    if (H < net->patch || W < net->patch_x)
+        return fail(FS_ERR_SHAPE, "image %dx%d smaller than the window %dx%d", H, W, net->patch, net->patch_x);
     P = Plan();
     P.B = B;
     P.H = H;
     P.W = W;
     P.ny = H - net->patch + 1;
-    P.nx = W - net->patch + 1;
+    P.nx = W - net->patch_x + 1;
     if (view) P.view = *view;
     // the image's pitch (a view reads a region of a larger image) and the
     // output map's (a view writes a region of a larger map)
@@ -565,7 +585,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
     const int es = elem_of(net->dtype);
 
     Geo g;
-    g.Q = 1;
+    g.Qy = g.Qx = 1;
     g.ey = {H};
     g.ex = {W};
     g.hmax = H;
@@ -592,40 +612,41 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         L.src = cur;
         L.dst = (cur == 0) ? 1 : 0;
         L.in_f32 = g.is_image;
-        const int F = g.Q * g.Q;
+        const int F = g.Qy * g.Qx;
         const long long in_pix = true_pixels(g);
         Geo o;
         if (l.kind == 1) {  // pool
-            const int k = l.k;
-            o = pool_geo(g, k);
-            if (g.Q * k > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
+            const int ky = l.k, kx = l.kx;
+            if (g.Qy * ky > kMaxAxis || g.Qx * kx > kMaxAxis)
+                return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
+            o = pool_geo(g, ky, kx);
             L.type = 1;
             if (g.is_image && view) return fail(FS_ERR_UNSUPPORTED, "a tiled scan needs a convolution first");
             PoolArgs &a = L.pool;
             a.F = F;
-            a.Q = g.Q;
+            a.Qx = g.Qx;
             a.in_h = g.hmax;
             a.in_w = g.wmax;
             a.out_h = std::max(o.hmax, 1);
             a.out_w = std::max(o.wmax, 1);
             a.C = g.C;
-            a.k = k;
-            a.n_children = B * F * k * k;
+            a.ky = ky;
+            a.kx = kx;
+            a.n_children = B * F * ky * kx;
             fill_axis(a.ext, g);
-            L.gx = B * F * k * k * a.out_h;
-            L.frags = B * F * k * k;
+            L.gx = B * F * ky * kx * a.out_h;
+            L.frags = B * F * ky * kx;
             L.out_pixels = (long long)B * true_pixels(o);
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * o.C * es;
             L.name = pool_kernel_name(net->dtype, g.is_image);
         } else {  // conv or fc as convolution
-            const int k = l.k;
-            o.Q = g.Q;
-            o.ey.resize(g.Q);
-            o.ex.resize(g.Q);
-            for (int i = 0; i < g.Q; ++i) {
-                o.ey[i] = std::max(g.ey[i] - (k - 1), 0);
-                o.ex[i] = std::max(g.ex[i] - (k - 1), 0);
-            }
+            const int ky = l.k, kx = l.kx;
+            o.Qy = g.Qy;
+            o.Qx = g.Qx;
+            o.ey.resize(g.Qy);
+            o.ex.resize(g.Qx);
+            for (int i = 0; i < g.Qy; ++i) o.ey[i] = std::max(g.ey[i] - (ky - 1), 0);
+            for (int i = 0; i < g.Qx; ++i) o.ex[i] = std::max(g.ex[i] - (kx - 1), 0);
             o.C = l.cout;
             o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
             o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
@@ -637,13 +658,15 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             ConvArgs &a = L.conv;
             a.nfrag = B * F;
             a.F = F;
-            a.Q = g.Q;
+            a.Qy = g.Qy;
+            a.Qx = g.Qx;
             a.in_h = g.is_image ? img_h : g.hmax;  // fragment stride and row pitch
             a.in_w = g.is_image ? img_w : g.wmax;
             a.in_c = g.C;
             a.out_h = std::max(o.hmax, 1);
             a.out_w = std::max(o.wmax, 1);
-            a.k = k;
+            a.ky = ky;
+            a.kx = kx;
             a.cin = l.cin;
             a.cout = l.cout;
             // the last layer, when not fused into the head, leaves its
@@ -664,7 +687,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 L.direct = true;
                 L.conv.lds_bytes = 0;
             } else {
-                fs_status st = pool_fuse ? plan_conv_pool_tiles(net, l, g, net->L[li + 1].k, L)
+                fs_status st = pool_fuse ? plan_conv_pool_tiles(net, l, g, net->L[li + 1].k, net->L[li + 1].kx, L)
                                          : plan_conv_tiles(net, l, g, L);
                 if (st != FS_OK) return st;
             }
@@ -714,21 +737,23 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             }
             L.frags = B * F;
             L.out_pixels = (long long)B * true_pixels(o);
-            L.flops = (double)L.out_pixels * 2.0 * l.cin * k * k * l.cout;
+            L.flops = (double)L.out_pixels * 2.0 * l.cin * ky * kx * l.cout;
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * l.cout * es +
-                      (double)l.cin * k * k * l.cout * es;
-            L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, k)
+                      (double)l.cin * ky * kx * l.cout * es;
+            L.name = L.direct ? conv_direct_kernel_name(net->dtype, g.is_image, l.cin, ky * kx)
                               : conv_kernel_name(net->dtype, g.is_image, L.mb, L.nb, L.wn, L.wk, L.vec, a.run);
             if (pool_fuse) {
-                const int kp = net->L[li + 1].k;
-                if (g.Q * kp > kMaxAxis) return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
-                const Geo o2 = pool_geo(o, kp);
-                a.pool_k = kp;
+                const int kpy = net->L[li + 1].k, kpx = net->L[li + 1].kx;
+                if (g.Qy * kpy > kMaxAxis || g.Qx * kpx > kMaxAxis)
+                    return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
+                const Geo o2 = pool_geo(o, kpy, kpx);
+                a.pool_ky = kpy;
+                a.pool_kx = kpx;
                 a.pool_oh = std::max(o2.hmax, 1);
                 a.pool_ow = std::max(o2.wmax, 1);
                 L.n_layers = 2;
                 L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) +
-                          (double)B * true_pixels(o2) * l.cout * es + (double)l.cin * k * k * l.cout * es;
+                          (double)B * true_pixels(o2) * l.cout * es + (double)l.cin * ky * kx * l.cout * es;
                 L.name += "+pool";
                 o = o2;
                 ++li;  // the pool is done
@@ -741,23 +766,16 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 a.head_act = hl.act;
                 a.ny = map_h;  // output pitch
                 a.nx = map_w;
-                a.S = net->S;
-                for (int f = 0; f < o.Q; ++f) {  // first output coordinate of axis index f
-                    int rest = f, base = 0, S = net->S;
-                    for (int m = (int)net->pool_k.size() - 1; m >= 0; --m) {
-                        const int k2 = net->pool_k[m];
-                        S /= k2;
-                        base += (rest % k2) * S;
-                        rest /= k2;
-                    }
-                    a.base[f] = (uint16_t)base;
-                }
+                a.Sy = net->S;
+                a.Sx = net->Sx;
+                for (int f = 0; f < o.Qy; ++f) a.base_y[f] = (uint16_t)axis_base(net->pool_k, net->S, f);
+                for (int f = 0; f < o.Qx; ++f) a.base_x[f] = (uint16_t)axis_base(net->pool_kx, net->Sx, f);
                 L.dst = 2;
                 L.n_layers = 2;
                 const long long npix = (long long)B * P.ny * P.nx;
                 L.flops += (double)npix * 2.0 * hl.cin * hl.cout;
                 L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)npix * net->ncls * 4 +
-                          (double)l.cin * k * k * l.cout * es;
+                          (double)l.cin * ky * kx * l.cout * es;
                 L.name += "+head";
             }
             if (!L.direct && a.run) L.name += "+run";
@@ -768,7 +786,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             (long long)std::max(g.hmax, 1) * std::max(g.wmax, 1) * g.C >= (1LL << 31))
             return fail(FS_ERR_UNSUPPORTED, "layer %d: a fragment holds 2^31 or more elements", li);
         if (L.dst != 2) {
-            const size_t out_bytes = (size_t)B * o.Q * o.Q * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
+            const size_t out_bytes = (size_t)B * o.Qy * o.Qx * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
             buf = std::max(buf, out_bytes);
         }
         P.flops += L.flops;
@@ -790,8 +808,8 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         L.has_fc = net->head_fc;
         HeadArgs &a = L.head;
         a.B = B;
-        a.F = g.Q * g.Q;
-        a.Q = g.Q;
+        a.F = g.Qy * g.Qx;
+        a.Qx = g.Qx;
         a.in_h = std::max(g.hmax, 1);
         a.in_w = std::max(g.wmax, 1);
         if (g.is_image && view) return fail(FS_ERR_UNSUPPORTED, "a tiled scan needs a convolution first");
@@ -802,17 +820,22 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         a.out_nx = map_w;
         a.ncls = net->ncls;
         a.act = net->L.back().act;
-        a.S = net->S;
+        a.Sy = net->S;
+        a.Sx = net->Sx;
         // Y mod S -> per-axis fragment index: the mixed-radix digits of r
         // (least significant = first pool) read back most significant first
-        for (int r = 0; r < net->S; ++r) {
-            int rr = r, idx = 0;
-            for (int k : net->pool_k) {
-                idx = idx * k + rr % k;
-                rr /= k;
+        auto digits = [](const std::vector<int> &ks, int S, uint16_t *map) {
+            for (int r = 0; r < S; ++r) {
+                int rr = r, idx = 0;
+                for (int k : ks) {
+                    idx = idx * k + rr % k;
+                    rr /= k;
+                }
+                map[r] = (uint16_t)idx;
             }
-            a.digit_map[r] = (uint16_t)idx;
-        }
+        };
+        digits(net->pool_k, net->S, a.digit_y);
+        digits(net->pool_kx, net->Sx, a.digit_x);
         const long long npix = (long long)B * P.ny * P.nx;
         L.gx = (int)((npix + 15) / 16);
         L.frags = B * a.F;
@@ -853,7 +876,7 @@ fs_status border_plan(const fs_net *net, int B, int H, int W, int border, Plan &
     if (border != BORDER_VALID) {
         if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
         He = H + net->patch - 1;
-        We = W + net->patch - 1;
+        We = W + net->patch_x - 1;
     }
     fs_status st = make_plan(net, B, He, We, P);
     if (st != FS_OK) return st;
@@ -897,11 +920,12 @@ struct Tiled {
 fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Tiled &T)
 {
     if (th < 1 || tw < 1) return fail(FS_ERR_INVALID_ARG, "tile sizes must be >= 1 (got %d x %d)", th, tw);
-    if (B < 1 || H < net->patch || W < net->patch)
-        return fail(FS_ERR_SHAPE, "image %dx%d (batch %d) smaller than the patch size %d", H, W, B, net->patch);
+    if (B < 1 || H < net->patch || W < net->patch_x)
+        return fail(FS_ERR_SHAPE, "image %dx%d (batch %d) smaller than the window %dx%d", H, W, B, net->patch,
+                    net->patch_x);
     T = Tiled();
     T.ny = H - net->patch + 1;
-    T.nx = W - net->patch + 1;
+    T.nx = W - net->patch_x + 1;
     T.th = std::min(th, T.ny);
     T.tw = std::min(tw, T.nx);
     T.rows = (T.ny + T.th - 1) / T.th;
@@ -915,7 +939,7 @@ fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Til
             v.img_w = W;
             v.out_h = T.ny;
             v.out_w = T.nx;
-            fs_status st = make_plan(net, B, h + net->patch - 1, w + net->patch - 1, T.shape[lr][lc], &v);
+            fs_status st = make_plan(net, B, h + net->patch - 1, w + net->patch_x - 1, T.shape[lr][lc], &v);
             if (st != FS_OK) return st;
             T.ws_bytes = std::max(T.ws_bytes, T.shape[lr][lc].ws_bytes);
         }
@@ -1015,6 +1039,7 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         NetLayer &l = L[i];
         l.kind = s.kind;
         l.k = s.k;
+        l.kx = s.k_x ? s.k_x : s.k;
         l.cin = s.c_in;
         l.cout = s.c_out;
         l.act = s.act;
@@ -1030,7 +1055,7 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
             return fail(FS_ERR_UNSUPPORTED, "layer %d: more than %d channels", i, kMaxChannels);
         if (s.kind == FS_MAXPOOL) {
             if (seen_fc) return fail(FS_ERR_SHAPE, "layer %d: pooling after a fully connected layer", i);
-            if (s.k < 1) return fail(FS_ERR_SHAPE, "layer %d: pool size must be >= 1", i);
+            if (s.k < 1 || l.kx < 1) return fail(FS_ERR_SHAPE, "layer %d: pool size must be >= 1", i);
             if (s.c_out != s.c_in) return fail(FS_ERR_SHAPE, "layer %d: a pool keeps the channel count", i);
             if (s.weight || s.bias) return fail(FS_ERR_INVALID_ARG, "layer %d: a pool has no weights", i);
             if (s.act != FS_ACT_NONE) return fail(FS_ERR_UNSUPPORTED, "layer %d: activation on a pool", i);
@@ -1039,65 +1064,89 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
                 return fail(FS_ERR_SHAPE, "layer %d: convolution after a fully connected layer", i);
             if (s.kind == FS_FC) seen_fc = true;
             if (s.k < 0 || (s.k == 0 && s.kind != FS_FC)) return fail(FS_ERR_SHAPE, "layer %d: bad kernel size", i);
+            if (s.k_x < 0 || (s.k == 0) != (l.kx == 0))
+                return fail(FS_ERR_SHAPE, "layer %d: bad kernel columns %d", i, s.k_x);
             if (!s.weight) return fail(FS_ERR_INVALID_ARG, "layer %d: weight is NULL", i);
         }
         c = s.c_out;
     }
-    // patch-level sizes: derive w_0 when the fully connected sizes are given
+    // patch-level sizes: derive h_0 x w_0 when the fully connected sizes are
+    // given (each axis on its own: Section 2's rectangular case)
     bool derivable = true;
     for (auto &l : L)
         if (l.kind == FS_FC && l.k == 0) derivable = false;
-    int w0 = patch;
+    int h0 = patch, w0 = patch;
     if (derivable) {
-        int w = 1;
-        for (int i = n_layers - 1; i >= 0; --i) w = (L[i].kind == FS_MAXPOOL) ? w * L[i].k : w + L[i].k - 1;
-        if (patch == 0) w0 = w;
-        else if (patch != w) return fail(FS_ERR_SHAPE, "patch %d does not match the stack, which needs %d", patch, w);
+        int h = 1, w = 1;
+        for (int i = n_layers - 1; i >= 0; --i) {
+            h = (L[i].kind == FS_MAXPOOL) ? h * L[i].k : h + L[i].k - 1;
+            w = (L[i].kind == FS_MAXPOOL) ? w * L[i].kx : w + L[i].kx - 1;
+        }
+        if (patch == 0) {
+            h0 = h;
+            w0 = w;
+        } else if (patch != h || patch != w) {
+            return fail(FS_ERR_SHAPE, "patch %d does not match the stack, which needs %dx%d", patch, h, w);
+        }
     } else if (patch == 0) {
         return fail(FS_ERR_INVALID_ARG, "patch is 0 and a fully connected layer has k = 0");
     }
     {
-        int w = w0;
+        int h = h0, w = w0;
         for (int i = 0; i < n_layers; ++i) {
             NetLayer &l = L[i];
+            l.h_in = h;
             l.w_in = w;
             if (l.kind == FS_MAXPOOL) {
-                if (w % l.k) return fail(FS_ERR_SHAPE, "layer %d: pool %d does not divide the map size %d", i, l.k, w);
-                w /= l.k;
+                if (h % l.k || w % l.kx)
+                    return fail(FS_ERR_SHAPE, "layer %d: pool %dx%d does not divide the map %dx%d", i, l.k, l.kx, h,
+                                w);
+                h /= l.k;
+                w /= l.kx;
             } else {
-                if (l.kind == FS_FC && l.k == 0) l.k = w;
-                if (l.kind == FS_FC && l.k != w)
-                    return fail(FS_ERR_SHAPE, "layer %d: fully connected kernel %d on a %d map", i, l.k, w);
-                if (l.k > w) return fail(FS_ERR_SHAPE, "layer %d: kernel %d larger than the map %d", i, l.k, w);
-                w -= l.k - 1;
+                if (l.kind == FS_FC && l.k == 0) {
+                    l.k = h;
+                    l.kx = w;
+                }
+                if (l.kind == FS_FC && (l.k != h || l.kx != w))
+                    return fail(FS_ERR_SHAPE, "layer %d: fully connected kernel %dx%d on a %dx%d map", i, l.k, l.kx,
+                                h, w);
+                if (l.k > h || l.kx > w)
+                    return fail(FS_ERR_SHAPE, "layer %d: kernel %dx%d larger than the map %dx%d", i, l.k, l.kx, h, w);
+                h -= l.k - 1;
+                w -= l.kx - 1;
             }
+            l.h_out = h;
             l.w_out = w;
         }
-        if (w != 1) return fail(FS_ERR_SHAPE, "the last map is %dx%d, not 1x1", w, w);
+        if (h != 1 || w != 1) return fail(FS_ERR_SHAPE, "the last map is %dx%d, not 1x1", h, w);
     }
 
     fs_net *net = new (std::nothrow) fs_net();
     if (!net) return fail(FS_ERR_OOM, "host allocation failed");
-    net->patch = w0;
+    net->patch = h0;
+    net->patch_x = w0;
     net->C = in_channels;
     net->dtype = dtype;
     net->ncls = L.back().cout;
     for (auto &l : L)
         if (l.kind == FS_MAXPOOL) {
             net->pool_k.push_back(l.k);
+            net->pool_kx.push_back(l.kx);
             net->S *= l.k;
-            net->F *= l.k * l.k;
+            net->Sx *= l.kx;
+            net->F *= l.k * l.kx;
         }
-    if (net->S > kMaxAxis) {
+    if (net->S > kMaxAxis || net->Sx > kMaxAxis) {
         delete net;
-        return fail(FS_ERR_UNSUPPORTED, "pool sizes multiply to %d > %d per axis", net->S, kMaxAxis);
+        return fail(FS_ERR_UNSUPPORTED, "pool sizes multiply to %dx%d > %d per axis", net->S, net->Sx, kMaxAxis);
     }
     if (net->ncls > kMaxHeadClasses) {
         delete net;
         return fail(FS_ERR_UNSUPPORTED, "%d outputs; at most %d supported", net->ncls, kMaxHeadClasses);
     }
     const NetLayer &last = L.back();
-    net->head_fc = last.kind != FS_MAXPOOL && last.k == 1 && last.cin * last.cout <= kMaxHeadWeights;
+    net->head_fc = last.kind != FS_MAXPOOL && last.k == 1 && last.kx == 1 && last.cin * last.cout <= kMaxHeadWeights;
     net->head_cin = net->head_fc ? last.cin : 0;
 
     // --- pack parameters into one device block ---
@@ -1155,7 +1204,7 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         // narrow channel tiles with a long K walk: two waves split K so each
         // wave owns 4 pixel blocks (more products per operand load, measured
         // faster on the 48 -> 48 layers of N4) without a larger LDS window
-        l.wk = (l.vec && l.wn == 1 && l.nb == 3 && l.k * l.k * l.cin >= 16 * 16) ? 2 : 1;
+        l.wk = (l.vec && l.wn == 1 && l.nb == 3 && l.k * l.kx * l.cin >= 16 * 16) ? 2 : 1;
         tile_override(i, nullptr, &l.nb, &l.wn, nullptr, &l.wk);
         bool any = false;
         for (int mb : {1, 2, 4, 8}) any = any || conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec);
@@ -1166,7 +1215,7 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         }
         const int grp = l.nb * l.wn;
         l.nbt = (nbt0 + grp - 1) / grp * grp;
-        l.ksteps = l.vec ? l.k * l.k * (l.cin / KSTEP) : (l.k * l.k * l.cin + KSTEP - 1) / KSTEP;
+        l.ksteps = l.vec ? l.k * l.kx * (l.cin / KSTEP) : (l.k * l.kx * l.cin + KSTEP - 1) / KSTEP;
         if (l.ksteps < l.wk) {  // every K-splitting wave needs at least one step
             delete net;
             return fail(FS_ERR_UNSUPPORTED, "layer %d: %d K steps cannot be split over %d waves", i, l.ksteps, l.wk);
@@ -1181,23 +1230,23 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
             if (co < l.cout) bp[r] = bias[co];
         }
         l.b_off = push(bp.data(), bp.size() * 4);
-        if (!l.vec && conv_direct_supported(l.cin, l.k, l.cout)) {
-            // [rows][KP] copy for the direct kernel, K index (dy * k + dx) * c_in + ci,
+        if (!l.vec && conv_direct_supported(l.cin, l.k * l.kx, l.cout)) {
+            // [rows][KP] copy for the direct kernel, K index (dy * k_x + dx) * c_in + ci,
             // then the biases in channel order
-            const int kp = conv_direct_kp(l.cin, l.k);
+            const int kp = conv_direct_kp(l.cin, l.k * l.kx);
             const int rows = (l.cout + 7) / 8 * 8;
             std::vector<float> wd((size_t)rows * kp + l.cout, 0.f);
             std::copy(bias.begin(), bias.end(), wd.begin() + (size_t)rows * kp);
             for (int co = 0; co < l.cout; ++co)
                 for (int dy = 0; dy < l.k; ++dy)
-                    for (int dx = 0; dx < l.k; ++dx)
+                    for (int dx = 0; dx < l.kx; ++dx)
                         for (int ci = 0; ci < l.cin; ++ci) {
-                            float v = s.weight[(((size_t)co * l.cin + ci) * l.k + dy) * l.k + dx];
+                            float v = s.weight[(((size_t)co * l.cin + ci) * l.k + dy) * l.kx + dx];
                             if (dtype == FS_BF16) {
                                 const uint32_t u = (uint32_t)host_f2bf(v) << 16;
                                 std::memcpy(&v, &u, 4);
                             }
-                            wd[(size_t)co * kp + (dy * l.k + dx) * l.cin + ci] = v;
+                            wd[(size_t)co * kp + (dy * l.kx + dx) * l.cin + ci] = v;
                         }
             l.has_w32 = true;
             l.w32_off = push(wd.data(), wd.size() * 4);
@@ -1270,6 +1319,8 @@ fs_status fs_net_query(const fs_net *net, fs_net_info *out)
     out->stride = net->S;
     out->n_fragments = net->F;
     out->dtype = net->dtype;
+    out->patch_x = net->patch_x;
+    out->stride_x = net->Sx;
     return FS_OK;
 }
 
@@ -1380,8 +1431,8 @@ fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int
     const float *img = d_image;
     if (border != BORDER_VALID) {
         float *pad = reinterpret_cast<float *>(static_cast<char *>(d_workspace) + pad_off);
-        const int p0 = (net->patch - 1) / 2;
-        hipError_t e = launch_mirror_pad(d_image, pad, B, H, W, net->C, p0, He, We, border, s);
+        const int p0y = (net->patch - 1) / 2, p0x = (net->patch_x - 1) / 2;
+        hipError_t e = launch_mirror_pad(d_image, pad, B, H, W, net->C, p0y, p0x, He, We, border, s);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "mirror pad: %s", hipGetErrorString(e));
         img = pad;
     }
@@ -1498,37 +1549,37 @@ fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_
         if (l.kind == FS_MAXPOOL) {
             std::vector<int> ny, nx;
             for (size_t i = 0; i < ey.size(); ++i)
-                for (int o = 0; o < l.k; ++o) {
-                    ny.push_back(std::max(ey[i] - o, 0) / l.k);
-                    nx.push_back(std::max(ex[i] - o, 0) / l.k);
-                }
+                for (int o = 0; o < l.k; ++o) ny.push_back(std::max(ey[i] - o, 0) / l.k);
+            for (size_t i = 0; i < ex.size(); ++i)
+                for (int o = 0; o < l.kx; ++o) nx.push_back(std::max(ex[i] - o, 0) / l.kx);
             ey.swap(ny);
             ex.swap(nx);
         } else {
             for (auto &v : ey) v = std::max(v - (l.k - 1), 0);
-            for (auto &v : ex) v = std::max(v - (l.k - 1), 0);
+            for (auto &v : ex) v = std::max(v - (l.kx - 1), 0);
         }
     }
     std::vector<int32_t> r(rec);
     for (int f = 0; f < net->F; ++f) {
-        // digits of f, first pool most significant: d_m = o_y * k_m + o_x
+        // digits of f, first pool most significant: d_m = o_y * kx_m + o_x
         std::vector<int> ox(np), oy(np);
         int rest = f;
         for (int m = np - 1; m >= 0; --m) {
-            const int k = net->pool_k[m];
-            const int d = rest % (k * k);
-            rest /= k * k;
-            ox[m] = d % k;
-            oy[m] = d / k;
+            const int ky = net->pool_k[m], kx = net->pool_kx[m];
+            const int d = rest % (ky * kx);
+            rest /= ky * kx;
+            ox[m] = d % kx;
+            oy[m] = d / kx;
         }
-        int fy = 0, fx = 0, Y0 = 0, X0 = 0, S = 1;
+        int fy = 0, fx = 0, Y0 = 0, X0 = 0, Sy = 1, Sx = 1;
         for (int m = 0; m < np; ++m) {
-            const int k = net->pool_k[m];
-            fy = fy * k + oy[m];
-            fx = fx * k + ox[m];
-            Y0 += oy[m] * S;
-            X0 += ox[m] * S;
-            S *= k;
+            const int ky = net->pool_k[m], kx = net->pool_kx[m];
+            fy = fy * ky + oy[m];
+            fx = fx * kx + ox[m];
+            Y0 += oy[m] * Sy;
+            X0 += ox[m] * Sx;
+            Sy *= ky;
+            Sx *= kx;
         }
         r[0] = f;
         r[1] = ey[fy];
@@ -1560,10 +1611,10 @@ fs_status fs_reassembly_index(const fs_net *net, int32_t H, int32_t W, int32_t *
         for (int X = 0; X < P.nx; ++X) {
             int f = 0, ry = Y, rx = X;
             for (int m = 0; m < np; ++m) {
-                const int k = net->pool_k[m];
-                f = f * k * k + (ry % k) * k + (rx % k);
-                ry /= k;
-                rx /= k;
+                const int ky = net->pool_k[m], kx = net->pool_kx[m];
+                f = f * ky * kx + (ry % ky) * kx + (rx % kx);
+                ry /= ky;
+                rx /= kx;
             }
             const size_t base = ((size_t)Y * P.nx + X) * 3;
             const int32_t v[3] = {f, ry, rx};

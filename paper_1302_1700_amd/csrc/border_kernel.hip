@@ -1,7 +1,7 @@
 // Mirrored borders (Section 3.2: the image's edges are mirrored so that the
 // net can be applied at every position): builds the extended image
-// [B][H + w_0 - 1][W + w_0 - 1][C] the scan then reads, p0 rows / columns
-// before the image and w_0 - 1 - p0 after it.  One thread per extended
+// [B][H + h_0 - 1][W + w_0 - 1][C] the scan then reads, p0 rows / columns
+// before the image and (window side) - 1 - p0 after it, per axis.  One thread per extended
 // element, so the writes are contiguous; the reads follow the mirrored
 // index, contiguous inside the image and reversed in the borders.
 #include "fs_internal.h"
@@ -28,7 +28,7 @@ __device__ __forceinline__ int mirror_index(int i, int n, int mode)
 }
 
 __global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, float *__restrict__ out, int H, int W,
-                                                  int C, int p0, int He, int We, int mode, long long total)
+                                                  int C, int p0y, int p0x, int He, int We, int mode, long long total)
 {
     for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long long)gridDim.x * 256) {
         const int c = (int)(e % C);
@@ -37,20 +37,20 @@ __global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, 
         p /= We;
         const int y = (int)(p % He);
         const long long b = p / He;
-        const int sy = mirror_index(y - p0, H, mode), sx = mirror_index(x - p0, W, mode);
+        const int sy = mirror_index(y - p0y, H, mode), sx = mirror_index(x - p0x, W, mode);
         out[e] = in[((b * H + sy) * W + sx) * C + c];
     }
 }
 
 }  // namespace
 
-hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0, int He, int We,
-                             int mode, hipStream_t s)
+hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0y, int p0x, int He,
+                             int We, int mode, hipStream_t s)
 {
     const long long total = (long long)B * He * We * C;
     const long long blocks = (total + 255) / 256;
     const int grid = (int)(blocks < 65536 ? blocks : 65536);
-    hipLaunchKernelGGL(mirror_pad, dim3(grid), dim3(256), 0, s, in, out, H, W, C, p0, He, We, mode, total);
+    hipLaunchKernelGGL(mirror_pad, dim3(grid), dim3(256), 0, s, in, out, H, W, C, p0y, p0x, He, We, mode, total);
     return hipGetLastError();
 }
 

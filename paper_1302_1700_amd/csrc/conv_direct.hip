@@ -48,12 +48,12 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
     // output staging (dynamic): 4 waves x 64 pixels x (c_out + 16 bytes)
     extern __shared__ __align__(16) unsigned char ostage[];
 
-    const int K = a.cin * a.k * a.k;
+    const int K = a.cin * a.ky * a.kx;
     for (int kk = threadIdx.x; kk < KP; kk += 256) {
         int o = 0;  // padding taps read pixel (0, 0) and have zero weight
         if (kk < K) {
             const int tap = kk / a.cin, ci = kk - (kk / a.cin) * a.cin;
-            const int dy = tap / a.k, dx = tap - (tap / a.k) * a.k;
+            const int dy = tap / a.kx, dx = tap - (tap / a.kx) * a.kx;
             o = (dy * a.in_w + dx) * a.in_c + ci;
         }
         offs[kk] = o;
@@ -69,8 +69,8 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
     const int pix = pix0 + threadIdx.x;
     const int y = pix / a.out_w, x = pix - (pix / a.out_w) * a.out_w;
     const int rem = q % a.F;
-    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
-    const int hout = a.ext.y[fy] - a.k + 1, wout = a.ext.x[fx] - a.k + 1;
+    const int fy = rem / a.Qx, fx = rem - (rem / a.Qx) * a.Qx;
+    const int hout = a.ext.y[fy] - a.ky + 1, wout = a.ext.x[fx] - a.kx + 1;
     const bool valid = pix < a.out_h * a.out_w && y < hout && x < wout;
 
     const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * a.in_h * a.in_w * a.in_c +
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
 template <bool BF, bool IN_F32>
 hipError_t go(const ConvArgs &a, const float *wpk, int grid, hipStream_t s)
 {
-    const int K = a.cin * a.k * a.k;
+    const int K = a.cin * a.ky * a.kx;
     constexpr int G = BF ? 8 : 4;
     const int cpad = (a.cout + G - 1) / G * G;
     const size_t lds = (size_t)4 * 64 * (cpad + G) * (BF ? 2 : 4);
@@ -152,11 +152,11 @@ hipError_t go(const ConvArgs &a, const float *wpk, int grid, hipStream_t s)
 
 }  // namespace
 
-bool conv_direct_supported(int cin, int k, int cout) { return cin * k * k <= kMaxK && cout <= 48; }
+bool conv_direct_supported(int cin, int taps, int cout) { return cin * taps <= kMaxK && cout <= 48; }
 
-int conv_direct_kp(int cin, int k)
+int conv_direct_kp(int cin, int taps)
 {
-    const int K = cin * k * k;
+    const int K = cin * taps;
     return K <= 16 ? 16 : K <= 32 ? 32 : 64;
 }
 
@@ -167,9 +167,9 @@ hipError_t launch_conv_direct(const ConvArgs &a, const float *wpk, int dtype, bo
     return go<true, false>(a, wpk, grid, s);
 }
 
-std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int k)
+std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int taps)
 {
-    const int K = cin * k * k;
+    const int K = cin * taps;
     const int kp = K <= 16 ? 16 : K <= 32 ? 32 : 64;
     const bool bf = dtype == DT_BF16;
     return std::string("conv_direct<") + (bf ? "true" : "false") + ", " + (bf && !in_f32 ? "false" : "true") +

@@ -281,7 +281,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
             z[1] = 1.0f / (1.0f + expf(-d));
             int fy, fx, y, x;
             locate(m, fy, fx, y, x);
-            const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
+            const int Y = a.base_y[fy] + a.Sy * y, X = a.base_x[fx] + a.Sx * x;
             float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * 2;
             *reinterpret_cast<float2 *>(dst) = float2{z[0], z[1]};
             continue;
@@ -314,7 +314,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
         }
         int fy, fx, y, x;
         locate(m, fy, fx, y, x);
-        const int Y = a.base[fy] + a.S * y, X = a.base[fx] + a.S * x;
+        const int Y = a.base_y[fy] + a.Sy * y, X = a.base_x[fx] + a.Sx * x;
         float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * ncls;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
@@ -362,7 +362,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         const int np = min(a.mt, a.run_pix - p0);
         // row of fragments: the last fy with ypre[fy] * wsum <= p0
         const int v = p0 / a.run_wsum;
-        int lo = 0, hi = a.Q - 1;
+        int lo = 0, hi = a.Qy - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
             if ((int)a.run_ypre[mid] <= v) lo = mid; else hi = mid - 1;
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         const int r0 = p0 - (int)a.run_ypre[fy] * a.run_wsum;
         const int u = r0 / ho;
         lo = 0;
-        hi = a.Q - 1;
+        hi = a.Qx - 1;
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
             if ((int)a.run_xpre[mid] <= u) lo = mid; else hi = mid - 1;
@@ -382,15 +382,15 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         l0 = r0 - ho * (int)a.run_xpre[fx];
         lend = min(ho * twb, l0 + np);
         n1 = np - (lend - l0);
-        q = b * a.F + fy * a.Q + fx;
+        q = b * a.F + fy * a.Qx + fx;
         if (n1 > 0) {  // every fragment holds at least mt pixels: one more segment at most
             fy1 = fy;
             fx1 = fx + 1;
-            if (fx1 == a.Q) {
+            if (fx1 == a.Qx) {
                 fx1 = 0;
                 ++fy1;
             }
-            q1 = b * a.F + fy1 * a.Q + fx1;
+            q1 = b * a.F + fy1 * a.Qx + fx1;
             twb1 = a.run_xpre[fx1 + 1] - a.run_xpre[fx1];
         }
         hin = a.ext.y[fy];
@@ -398,29 +398,30 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     } else {
         q = bid / a.nbands;
         const int rem = q % a.F;
-        fy = rem / a.Q;
-        fx = rem - (rem / a.Q) * a.Q;
+        fy = rem / a.Qx;
+        fx = rem - (rem / a.Qx) * a.Qx;
         hin = a.ext.y[fy];
         win = a.ext.x[fx];
-        const int hout = hin - a.k + 1, wout = win - a.k + 1;
+        const int hout = hin - a.ky + 1, wout = win - a.kx + 1;
         if (hout <= 0 || wout <= 0) return;
         c0 = band * a.band_w;
-        if (a.pool_k) {
+        if (a.pool_ky) {
             // Section 2.2.2: child (o_x, o_y) of a k x k pool holds the stride-1
             // k x k max filter M of its parent at (o_y + k*ybar, o_x + k*xbar),
             // so every filter position y < hout - k + 1 (and likewise x) feeds
             // exactly one child.  The tile computes the convolution outputs its
-            // filter positions need: k - 1 more rows and columns.
-            const int hM = hout - a.pool_k + 1, wM = wout - a.pool_k + 1;
+            // filter positions need: k - 1 more rows and columns (per axis,
+            // for a k_y x k_x pool).
+            const int hM = hout - a.pool_ky + 1, wM = wout - a.pool_kx + 1;
             if (hM <= 0 || wM <= 0) return;
             twM = min(a.band_w, wM - c0);
             if (twM <= 0) return;
             y0 = t * a.pool_rt;
             if (y0 >= hM) return;
             rtM = min(a.pool_rt, hM - y0);
-            twb = twM + a.pool_k - 1;
+            twb = twM + a.pool_kx - 1;
             l0 = y0 * twb;
-            lend = l0 + (rtM + a.pool_k - 1) * twb;
+            lend = l0 + (rtM + a.pool_ky - 1) * twb;
         } else {
             twb = min(a.band_w, wout - c0);
             if (twb <= 0) return;
@@ -434,9 +435,9 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     const int n0 = lend - l0;
     const int yfirst = l0 / twb;
     const int ylast = (lend - 1) / twb;
-    const int R = ylast - yfirst + a.k;                      // window rows of segment 0
-    const int R1 = n1 > 0 ? (n1 - 1) / twb1 + a.k : 0;       // then those of segment 1
-    const int Cc = max(twb, n1 > 0 ? twb1 : 0) + a.k - 1;    // window columns
+    const int R = ylast - yfirst + a.ky;                     // window rows of segment 0
+    const int R1 = n1 > 0 ? (n1 - 1) / twb1 + a.ky : 0;      // then those of segment 1
+    const int Cc = max(twb, n1 > 0 ? twb1 : 0) + a.kx - 1;   // window columns
     const int hin1 = n1 > 0 ? a.ext.y[fy1] : 0, win1 = n1 > 0 ? a.ext.x[fx1] : 0;
     const int CS = a.lds_cs;
     const int kk_total = a.ksteps * KSTEP;
@@ -560,12 +561,12 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     if constexpr (RUN)
         if (R1 > 0) stage(inp1, 0, hin1, win1, R, R1);
     if constexpr (!VEC) {
-        const Div dci(a.cin), dk(a.k);
+        const Div dci(a.cin), dk(a.kx);
         for (int kk = threadIdx.x; kk < kk_total; kk += 256) {
             int tap, ci;
             dci.qr(kk, tap, ci);
             int off = -1;
-            if (tap < a.k * a.k) {
+            if (tap < a.ky * a.kx) {
                 int dy, dx;
                 dk.qr(tap, dy, dx);
                 off = (dy * Cc + dx) * CS + ci;
@@ -671,13 +672,13 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         const int nsteps = s_end - s_begin;
         // (branch-free: a straight-line loop body lets the compiler wait only
         // for the operands each product needs)
-        int cc = s_begin % ncc, dx = (s_begin / ncc) % a.k, dy = (s_begin / ncc) / a.k;
+        int cc = s_begin % ncc, dx = (s_begin / ncc) % a.kx, dy = (s_begin / ncc) / a.kx;
         auto advance = [&](int) {
             ++cc;
             const int w1 = cc == ncc;
             cc = w1 ? 0 : cc;
             dx += w1;
-            const int w2 = dx == a.k;
+            const int w2 = dx == a.kx;
             dx = w2 ? 0 : dx;
             dy += w2;
             return (dy * Cc + dx) * CS + cc * KSTEP;
@@ -870,28 +871,29 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         }
     };
 
-    if (!RUN && a.pool_k) {
+    if (!RUN && a.pool_ky) {
         // Fused k x k pool (the workgroup owns every channel): the filter
         // value at fragment position (y, x) = (y0 + r, c0 + c) is the
         // maximum over the tile's k x k outputs from (r, c), and goes to
         // child (o_y, o_x) = (y mod k, x mod k) at (y div k, x div k); the
         // child of (fy, fx) is fragment (fy*k + o_y, fx*k + o_x) of the next
-        // layer (Qc = Q*k per axis).  Same values as a separate pool kernel
-        // reading this layer's stored (rounded) outputs.
+        // layer (Qx*k fragments per row of its grid).  Per axis for a
+        // k_y x k_x pool.  Same values as a separate pool kernel reading this
+        // layer's stored (rounded) outputs.
         TC *tile = reinterpret_cast<TC *>(smem);
         __syncthreads();  // every wave is done with the window / partial sums
         stage_tile(tile, true);
         __syncthreads();
-        const int kp = a.pool_k, ew = twb;
-        const int Qc = a.Q * kp;
+        const int kpy = a.pool_ky, kpx = a.pool_kx, ew = twb;
+        const int Qc = a.Qx * kpx;
         const size_t child_px = (size_t)a.pool_oh * a.pool_ow;
-        const size_t cbase = (size_t)(q / a.F) * a.F * kp * kp;  // first child of image b
-        const Div dkp(kp), dtm(twM);
+        const size_t cbase = (size_t)(q / a.F) * a.F * kpy * kpx;  // first child of image b
+        const Div dky(kpy), dkx(kpx), dtm(twM);
         auto child_ptr = [&](int r, int c) {
             int ybar, oy, xbar, ox;
-            dkp.qr(y0 + r, ybar, oy);
-            dkp.qr(c0 + c, xbar, ox);
-            const size_t qc = cbase + (size_t)(fy * kp + oy) * Qc + (fx * kp + ox);
+            dky.qr(y0 + r, ybar, oy);
+            dkx.qr(c0 + c, xbar, ox);
+            const size_t qc = cbase + (size_t)(fy * kpy + oy) * Qc + (fx * kpx + ox);
             return reinterpret_cast<TC *>(a.out) + (qc * child_px + (size_t)ybar * a.pool_ow + xbar) * a.cout;
         };
         if ((a.cout % TPAD) == 0) {
@@ -909,8 +911,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
             const long long d_oy = (long long)Qc * child_px * a.cout;  // next o_y: the child Qc fragments on
             const long long d_yb = (long long)a.pool_ow * a.cout;      // next ybar
             auto walk = [&](auto kc) {
-                constexpr int KC = decltype(kc)::value;  // pool size if known here, else 0
-                const int K = KC ? KC : kp;
+                constexpr int KC = decltype(kc)::value;  // square pool size if known here, else 0
+                const int KY = KC ? KC : kpy, KX = KC ? KC : kpx;
                 for (int w = threadIdx.x; w < items * nrg; w += 256) {
                     int rg, it, c, v;
                     dit.qr(w, rg, it);
@@ -918,7 +920,7 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                     const int r0 = rg * rpt, r1 = min(r0 + rpt, rtM);
                     if (r0 >= r1) continue;
                     int ybar, oy;
-                    dkp.qr(y0 + r0, ybar, oy);
+                    dky.qr(y0 + r0, ybar, oy);
                     TC *dst = child_ptr(r0, c) + v * TPAD;
                     const TC *src = tile + __mul24(__mul24(r0, ew) + c, TS) + v * TPAD;
                     for (int r = r0; r < r1; ++r) {
@@ -946,8 +948,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                                 for (int j = 0; j < KC; ++j)
                                     if (i + j > 0) tap(i, j);
                         } else {
-                            for (int i = 0; i < K; ++i)
-                                for (int j = 0; j < K; ++j) tap(i, j);
+                            for (int i = 0; i < KY; ++i)
+                                for (int j = 0; j < KX; ++j) tap(i, j);
                         }
                         if constexpr (BF) {
 #pragma unroll
@@ -955,18 +957,18 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                         }
                         *reinterpret_cast<u4 *>(dst) = m;
                         src += ew * TS;
-                        if (++oy == K) {
+                        if (++oy == KY) {
                             oy = 0;
-                            dst += d_yb - (K - 1) * d_oy;
+                            dst += d_yb - (KY - 1) * d_oy;
                         } else {
                             dst += d_oy;
                         }
                     }
                 }
             };
-            if (kp == 2)
+            if (kpy == 2 && kpx == 2)
                 walk(std::integral_constant<int, 2>());
-            else if (kp == 3)
+            else if (kpy == 3 && kpx == 3)
                 walk(std::integral_constant<int, 3>());
             else
                 walk(std::integral_constant<int, 0>());
@@ -979,8 +981,8 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                 dtm.qr(p, r, c);
                 const TC *src = tile + __mul24(__mul24(r, ew) + c, TS) + ch;
                 TC m = src[0];
-                for (int i = 0; i < kp; ++i)
-                    for (int j = 0; j < kp; ++j) {
+                for (int i = 0; i < kpy; ++i)
+                    for (int j = 0; j < kpx; ++j) {
                         const TC x = src[__mul24(__mul24(i, ew) + j, TS)];
                         if constexpr (BF)
                             m = (TC)max_i16x2(m, x);  // keys in the low half

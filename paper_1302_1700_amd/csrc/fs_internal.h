@@ -4,8 +4,9 @@
 //   [B * F][Hmax][Wmax][C], channels innermost,
 // where F is the number of fragments per image at that layer, Hmax x Wmax the
 // largest fragment size, and the fragment of image b with per-axis indices
-// (fy, fx) sits at batch index b * F + fy * Q + fx (Q = product of the pool
-// sizes so far, F = Q * Q).  Fragment sizes are separable: a fragment's height
+// (fy, fx) sits at batch index b * F + fy * Qx + fx (Qy, Qx = products of the
+// pools' row and column sizes so far, F = Qy * Qx; square pools give
+// Qy = Qx).  Fragment sizes are separable: a fragment's height
 // depends only on its y-offset chain and its width only on its x-offset chain,
 // so one table per axis (indexed by fy or fx) holds every fragment's true
 // size.  Pixels beyond a fragment's true size are padding: never read for a
@@ -43,10 +44,10 @@ struct ConvArgs {
     const void *w;        // packed weights (api.hip: pack_conv_weights)
     const float *bias;    // [nbt * 16] in (block, row) order, zero padded
     int nfrag;            // B * F
-    int F, Q;             // fragments per image, per axis
+    int F, Qy, Qx;        // fragments per image, per axis
     int in_h, in_w, in_c; // padded input dims; in_c = channel pitch of the input
     int out_h, out_w;     // padded output dims
-    int k, cin, cout, act;
+    int ky, kx, cin, cout, act;  // kernel rows, columns
     int ksteps;           // K steps of the matrix-core loop
     int nbt;              // total 16-wide output-channel blocks
     int band_w;           // output columns per band
@@ -63,7 +64,7 @@ struct ConvArgs {
     // ([nfrag * k^2][pool_oh][pool_ow][cout]); bands then run over the
     // stride-1 max filter's columns, and a tile is pool_rt filter rows plus
     // the k - 1 rows and columns of convolution outputs they also need.
-    int pool_k, pool_rt, pool_oh, pool_ow;
+    int pool_ky, pool_kx, pool_rt, pool_oh, pool_ow;  // pool_ky == 0: no pool
     // Run tiles (run > 0; layers whose fragments each fit one band and hold
     // at least mt output pixels): per image the fragments' output pixels are
     // numbered in fragment order, fragment (fy, fx) holding
@@ -87,18 +88,18 @@ struct ConvArgs {
     const void *head_wbf;
     const float *head_b;  // [head_ncls]
     float *head_out;      // [B][ny][nx][head_ncls] (ny, nx: the output map's rows and row pitch)
-    int ny, nx, S;
-    uint16_t base[kMaxAxis];  // per-axis fragment index -> its first output coordinate
+    int ny, nx, Sy, Sx;       // Sy, Sx: products of the pools' row / column sizes
+    uint16_t base_y[kMaxAxis], base_x[kMaxAxis];  // per-axis fragment index -> its first output coordinate
 };
 
 struct PoolArgs {
     const void *in;      // parents  [B*F][in_h][in_w][C]
-    void *out;           // children [B*F*k*k][out_h][out_w][C]
-    int F, Q;            // parents per image, per axis
+    void *out;           // children [B*F*ky*kx][out_h][out_w][C]
+    int F, Qx;           // parents per image; per row of the fragment grid
     int in_h, in_w;
     int out_h, out_w;
-    int C, k;
-    int n_children;      // B * F * k * k
+    int C, ky, kx;       // pool rows, columns
+    int n_children;      // B * F * ky * kx
     AxisTable ext;       // true sizes of the parents
 };
 
@@ -109,12 +110,12 @@ struct HeadArgs {
     float *out;          // [B][out_ny][out_nx][ncls], windows at [.][0, ny)[0, nx)
     const float *w;      // [ncls][C] (has_fc) or unused
     const float *bias;   // [ncls]
-    int B, F, Q;
+    int B, F, Qx;
     int in_h, in_w, C;
     int ny, nx, ncls, act;  // windows per image (rows, columns)
     int out_ny, out_nx;  // the output map's rows and row pitch (>= ny, nx)
-    int S;               // product of pool sizes
-    uint16_t digit_map[kMaxAxis];  // output coordinate mod S -> per-axis fragment index
+    int Sy, Sx;          // products of the pools' row / column sizes
+    uint16_t digit_y[kMaxAxis], digit_x[kMaxAxis];  // output coordinate mod S -> per-axis fragment index
 };
 
 // Launchers (return hipSuccess or the launch error).  `dtype` selects the
@@ -126,10 +127,10 @@ hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb
                        int grid_x, int grid_y, hipStream_t s);
 hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipStream_t s);
 // Mirrored borders: out[B][He][We][C] from in[B][H][W][C], extended index
-// (y, x) reading image pixel (mirror(y - p0, H), mirror(x - p0, W)).
+// (y, x) reading image pixel (mirror(y - p0y, H), mirror(x - p0x, W)).
 enum BorderMode { BORDER_VALID = 0, BORDER_REFLECT = 1, BORDER_SYMMETRIC = 2 };
-hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0, int He, int We,
-                             int mode, hipStream_t s);
+hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0y, int p0x, int He,
+                             int We, int mode, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 // Whether a tile shape has an instance (run: one with run tiles).
@@ -137,15 +138,16 @@ bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec, bool run = fa
 // Workgroups of that convolution kernel resident per CU with `lds` bytes of
 // dynamic LDS, on the current device (0 if the query fails).
 int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run, int lds);
-// Direct (vector-ALU) convolution for tiny K = c_in * k * k (<= 64) and
-// c_out <= 48; wpk = weights as [rows][KP] float32 with rows = c_out rounded
-// up to 8 (zero rows past c_out), K index (dy * k + dx) * c_in + ci, zero
-// padded to KP = conv_direct_kp(c_in, k) (bf16 nets: values rounded to bf16),
-// followed by the c_out biases in channel order.  One thread per pixel.
-bool conv_direct_supported(int cin, int k, int cout);
-int conv_direct_kp(int cin, int k);
+// Direct (vector-ALU) convolution for tiny K = c_in * taps (taps = k_y * k_x,
+// K <= 64) and c_out <= 48; wpk = weights as [rows][KP] float32 with rows =
+// c_out rounded up to 8 (zero rows past c_out), K index (dy * k_x + dx) *
+// c_in + ci, zero padded to KP = conv_direct_kp(c_in, taps) (bf16 nets: values
+// rounded to bf16), followed by the c_out biases in channel order.  One thread
+// per pixel.
+bool conv_direct_supported(int cin, int taps, int cout);
+int conv_direct_kp(int cin, int taps);
 hipError_t launch_conv_direct(const ConvArgs &a, const float *wpk, int dtype, bool in_f32, int grid, hipStream_t s);
-std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int k);
+std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int taps);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run);

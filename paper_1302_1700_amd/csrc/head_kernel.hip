@@ -10,8 +10,9 @@
 // sizes k_1..k_P and S = k_1 * ... * k_P, the offsets a window's corner
 // selects at the successive pools are the mixed-radix digits of Y mod S (least
 // significant first: o_1 = Y mod k_1, then (Y div k_1) mod k_2, ...), and its
-// position inside the fragment is Y div S; the same holds for X.  The host
-// turns "Y mod S -> per-axis fragment index" into a small table.
+// position inside the fragment is Y div S; the same holds for X, with the
+// pools' column sizes.  The host turns "Y mod S_y -> row index of the
+// fragment grid" (and the same for X) into small tables.
 //
 // Mapping: 16 lanes per output pixel, consecutive groups take consecutive
 // output pixels, so the dense output is written contiguously while each group
@@ -45,9 +46,9 @@ __global__ __launch_bounds__(256) void head_softmax_reassemble(HeadArgs a)
     const int b = (int)(gp / ((long long)a.ny * a.nx));
     const int r = (int)(gp - (long long)b * a.ny * a.nx);
     const int Y = r / a.nx, X = r - (r / a.nx) * a.nx;
-    const int fy = a.digit_map[Y % a.S], fx = a.digit_map[X % a.S];
-    const int yf = Y / a.S, xf = X / a.S;
-    const size_t q = (size_t)b * a.F + (size_t)fy * a.Q + fx;
+    const int fy = a.digit_y[Y % a.Sy], fx = a.digit_x[X % a.Sx];
+    const int yf = Y / a.Sy, xf = X / a.Sx;
+    const size_t q = (size_t)b * a.F + (size_t)fy * a.Qx + fx;
     const TI *src = reinterpret_cast<const TI *>(a.in) + ((q * a.in_h + yf) * a.in_w + xf) * a.C;
 
     float z[kMaxHeadClasses];

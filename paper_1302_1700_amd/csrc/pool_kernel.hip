@@ -5,6 +5,8 @@
 // (xbar, ybar) is the maximum of the parent's pixels with
 //   o_x + k*xbar <= x <= o_x + k*xbar + k - 1 and the same in y       (Eq. 5)
 // and the child's size is div(s - o, k) per axis (Eqs. 6-7), never below 0.
+// A rectangular k_y x k_x pool (Section 2: the square case generalizes
+// directly) has k_y * k_x children and the same rules per axis.
 //
 // One workgroup writes one row of one child: the row is a contiguous run of
 // w_c * C elements, so stores are fully coalesced; the k parent rows it reads
@@ -37,28 +39,28 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
     using TO = typename std::conditional<BF, uint16_t, float>::type;
     using TI = typename std::conditional<IN_F32, float, TO>::type;
 
-    const int kk = a.k * a.k;
-    // blockIdx.x = ((b * F + f) * k*k + o) * out_h + ybar, grouped so that the
-    // k^2 children of a parent row band are neighbours:
+    const int kk = a.ky * a.kx;
+    // blockIdx.x = ((b * F + f) * ky*kx + o) * out_h + ybar, grouped so that
+    // the children of a parent row band are neighbours:
     const int ybar = blockIdx.x % a.out_h;
     const int rest = blockIdx.x / a.out_h;
     const int o = rest % kk;
-    const int p = rest / kk;            // parent batch index b * F + fy * Q + fx
-    const int oy = o / a.k, ox = o - (o / a.k) * a.k;
+    const int p = rest / kk;            // parent batch index b * F + fy * Qx + fx
+    const int oy = o / a.kx, ox = o - (o / a.kx) * a.kx;
     const int b = p / a.F;
     const int rem = p - b * a.F;
-    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
+    const int fy = rem / a.Qx, fx = rem - (rem / a.Qx) * a.Qx;
     const int hp = a.ext.y[fy], wp = a.ext.x[fx];
-    const int hc = hp >= oy ? (hp - oy) / a.k : 0;
-    const int wc = wp >= ox ? (wp - ox) / a.k : 0;
+    const int hc = hp >= oy ? (hp - oy) / a.ky : 0;
+    const int wc = wp >= ox ? (wp - ox) / a.kx : 0;
     if (ybar >= hc || wc <= 0) return;
 
-    // child batch index in the (fy * k + oy, fx * k + ox) grid of Q * k per axis
-    const int Qc = a.Q * a.k;
-    const size_t child = (size_t)b * a.F * kk + (size_t)(fy * a.k + oy) * Qc + (fx * a.k + ox);
+    // child batch index in the (fy * ky + oy, fx * kx + ox) grid (Qx * kx per row)
+    const int Qc = a.Qx * a.kx;
+    const size_t child = (size_t)b * a.F * kk + (size_t)(fy * a.ky + oy) * Qc + (fx * a.kx + ox);
 
     const TI *src = reinterpret_cast<const TI *>(a.in) +
-                    ((size_t)p * a.in_h + (oy + a.k * ybar)) * a.in_w * a.C;
+                    ((size_t)p * a.in_h + (oy + a.ky * ybar)) * a.in_w * a.C;
     TO *dst = reinterpret_cast<TO *>(a.out) + (child * a.out_h + ybar) * a.out_w * a.C;
     const size_t prow = (size_t)a.in_w * a.C;
 
@@ -67,12 +69,12 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
     for (int idx = threadIdx.x; idx < total; idx += 256) {
         const int xbar = idx / nv;
         const int cv = idx - xbar * nv;
-        const size_t base = (size_t)(ox + a.k * xbar) * a.C + cv * V;
+        const size_t base = (size_t)(ox + a.kx * xbar) * a.C + cv * V;
         float m[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) m[e] = -INFINITY;
-        for (int i = 0; i < a.k; ++i) {
-            for (int j = 0; j < a.k; ++j) {
+        for (int i = 0; i < a.ky; ++i) {
+            for (int j = 0; j < a.kx; ++j) {
                 const TI *s = src + i * prow + base + (size_t)j * a.C;
                 if constexpr (V == 1) {
                     float v;
@@ -129,10 +131,10 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
     const int chunk = bid % nchunks;
     bid /= nchunks;
     const int band = bid % nbands;
-    const int p = bid / nbands;  // parent batch index b * F + fy * Q + fx
+    const int p = bid / nbands;  // parent batch index b * F + fy * Qx + fx
     const int b = p / a.F;
     const int rem = p - b * a.F;
-    const int fy = rem / a.Q, fx = rem - (rem / a.Q) * a.Q;
+    const int fy = rem / a.Qx, fx = rem - (rem / a.Qx) * a.Qx;
     const int hp = a.ext.y[fy], wp = a.ext.x[fx];
     const int nv = a.C / V;
     const int pi = chunk * 256 + threadIdx.x;
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
 
     const TI *src = reinterpret_cast<const TI *>(a.in) + (size_t)p * a.in_h * a.in_w * a.C + (size_t)x * a.C + cv * V;
     const size_t prow = (size_t)a.in_w * a.C;
-    const int Qc = a.Q * K;
+    const int Qc = a.Qx * K;
     const size_t cbase = (size_t)b * a.F * K * K;
     TO *out = reinterpret_cast<TO *>(a.out);
 
@@ -228,9 +230,11 @@ hipError_t go_rows(const PoolArgs &a, hipStream_t s)
 template <bool BF, bool IN_F32, int V>
 hipError_t go_k(const PoolArgs &a, int grid, hipStream_t s)
 {
-    if (a.k == 2) return go_rows<2, BF, IN_F32, V>(a, s);
-    if (a.k == 3) return go_rows<3, BF, IN_F32, V>(a, s);
-    if (a.k == 4) return go_rows<4, BF, IN_F32, V>(a, s);
+    if (a.ky == a.kx) {
+        if (a.ky == 2) return go_rows<2, BF, IN_F32, V>(a, s);
+        if (a.ky == 3) return go_rows<3, BF, IN_F32, V>(a, s);
+        if (a.ky == 4) return go_rows<4, BF, IN_F32, V>(a, s);
+    }
     hipLaunchKernelGGL((pool_frag<BF, IN_F32, V>), dim3(grid), dim3(256), 0, s, a);
     return hipGetLastError();
 }

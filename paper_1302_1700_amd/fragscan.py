@@ -30,12 +30,13 @@ class FsError(RuntimeError):
 class fs_layer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("k", ctypes.c_int32), ("c_in", ctypes.c_int32),
                 ("c_out", ctypes.c_int32), ("act", ctypes.c_int32),
-                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p)]
+                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("k_x", ctypes.c_int32)]
 
 
 class fs_net_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("patch", "in_channels", "n_classes", "n_layers",
-                                              "n_pools", "stride", "n_fragments", "dtype")]
+                                              "n_pools", "stride", "n_fragments", "dtype",
+                                              "patch_x", "stride_x")]
 
 
 class fs_plan_info(ctypes.Structure):
@@ -114,7 +115,9 @@ def _stream_handle(stream=None):
 class Net:
     """A net loaded into the library.
 
-    layers : list of layer dicts (kind, k, c_in, c_out, act), see workloads.py
+    layers : list of layer dicts (kind, k, c_in, c_out, act; optional kx, the
+             kernel's / pool's columns when they differ from its rows k),
+             see workloads.py
     params : per layer (weight OIHW float32, bias float32) or None for pools
     in_channels, patch (0 = derive), dtype "f32" | "bf16".
     Created on the current HIP device; plan_only=True makes a host-only handle
@@ -128,6 +131,7 @@ class Net:
         for i, (L, p) in enumerate(zip(layers, params)):
             arr[i].kind = KIND[L["kind"]]
             arr[i].k = int(L["k"])
+            arr[i].k_x = int(L.get("kx") or 0)
             arr[i].c_in = int(L["c_in"])
             arr[i].c_out = int(L["c_out"])
             arr[i].act = ACT[L["act"]]
@@ -146,7 +150,8 @@ class Net:
         info = fs_net_info()
         _check(lib.fs_net_query(self._h, ctypes.byref(info)))
         self.info = {n: getattr(info, n) for n, _ in fs_net_info._fields_}
-        self.patch = self.info["patch"]
+        self.patch = self.info["patch"]      # window rows h_0
+        self.patch_x = self.info["patch_x"]  # window columns w_0
         self.n_classes = self.info["n_classes"]
 
     def close(self):
@@ -197,7 +202,7 @@ class Net:
         buf = np.zeros(need.value, np.int32)
         _check(lib.fs_reassembly_index(self._h, H, W, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
                                        need.value, None))
-        return buf.reshape(H - self.patch + 1, W - self.patch + 1, 3)
+        return buf.reshape(H - self.patch + 1, W - self.patch_x + 1, 3)
 
     # -- scanning --------------------------------------------------------------
     def plan_tiled(self, B, H, W, tile):
@@ -218,7 +223,7 @@ class Net:
         return ws
 
     def scan(self, image, out=None, workspace=None, stream=None, border="valid"):
-        """image: CUDA float32 tensor [B, H, W, C] (contiguous) -> [B, H-w0+1, W-w0+1, n]
+        """image: CUDA float32 tensor [B, H, W, C] (contiguous) -> [B, H-h0+1, W-w0+1, n]
         (border "valid"), or [B, H, W, n] with the image's edges mirrored
         ("reflect": about the edge pixels, "symmetric": edge pixels repeated)."""
         import torch
@@ -227,7 +232,7 @@ class Net:
         if border not in BORDER:
             raise ValueError("border must be one of %s" % sorted(BORDER))
         B, H, W, C = image.shape
-        oh, ow = (H - self.patch + 1, W - self.patch + 1) if border == "valid" else (H, W)
+        oh, ow = (H - self.patch + 1, W - self.patch_x + 1) if border == "valid" else (H, W)
         if out is None:
             out = torch.empty((B, oh, ow, self.n_classes), dtype=torch.float32, device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, border)
@@ -250,7 +255,7 @@ class Net:
             raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
         B, H, W, C = image.shape
         if out is None:
-            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes), dtype=torch.float32,
+            out = torch.empty((B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes), dtype=torch.float32,
                               device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, tile=tile)
         _check(load().fs_scan_tiled(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, int(tile[0]), int(tile[1]),
@@ -265,7 +270,7 @@ class Net:
         import torch
         B, H, W, C = image.shape
         if out is None:
-            out = torch.empty((B, H - self.patch + 1, W - self.patch + 1, self.n_classes),
+            out = torch.empty((B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes),
                               dtype=torch.float32, device=image.device)
         ws = self.workspace(B, H, W, image.device)
         n = self.plan(B, H, W)["n_launches"]

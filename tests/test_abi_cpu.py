@@ -42,8 +42,14 @@ def _plan_net(layers, params=None, c0=1, patch=0, dtype="f32"):
 
 def _check_tables(layers, H, W, c0=1):
     net = _plan_net(layers, c0=c0)
-    w0 = ix.patch_size(layers)
-    assert net.patch == w0
+    h0, w0 = ix.patch_hw(layers)
+    assert (net.patch, net.patch_x) == (h0, w0)
+    Sy = Sx = 1
+    for L in layers:
+        if L["kind"] == "pool":
+            Sy, Sx = Sy * ix.kyx(L)[0], Sx * ix.kyx(L)[1]
+    assert (net.info["stride"], net.info["stride_x"]) == (Sy, Sx)
+    assert net.info["n_fragments"] == ix.n_fragments(layers)
     # reassembly index, every output pixel
     got = net.reassembly_index(H, W)
     want = ix.reassembly_index(layers, H, W)
@@ -69,7 +75,7 @@ def _check_tables(layers, H, W, c0=1):
             assert h * w == 0
     # plan: output size and algorithmic FLOPs
     p = net.plan(2, H, W)
-    assert (p["out_h"], p["out_w"]) == (H - w0 + 1, W - w0 + 1)
+    assert (p["out_h"], p["out_w"]) == (H - h0 + 1, W - w0 + 1)
     assert p["flops"] == pytest.approx(sum(ix.algorithmic_flops(layers, 2, H, W)), rel=1e-12)
     net.close()
 
@@ -103,6 +109,51 @@ def test_tables_random_nets(seed):
     H = w0 + int(rng.integers(0, 20))
     W = w0 + int(rng.integers(0, 20))
     _check_tables(layers, H, W, c0)
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_tables_random_rect_nets(seed):
+    """Rectangular kernels and pools (Section 2: every rule per axis)."""
+    rng = np.random.default_rng(4500 + seed)
+    layers, (h0, w0), c0 = wl.random_rect_net(rng)
+    H = h0 + int(rng.integers(0, 20))
+    W = w0 + int(rng.integers(0, 20))
+    _check_tables(layers, H, W, c0)
+
+
+def test_rect_net_rules():
+    """A 2 x 3 pool gives 6 children (f * 6 + o_y * 3 + o_x); the window is
+    derived per axis; a square patch argument or a k_x on an FC layer that
+    takes its size from the map is rejected."""
+    layers = [wl.conv(2, 1, 2, "tanh", kx=3), wl.pool(2, 2, kx=3), wl.fc(2, 2, 3, "tanh", kx=1),
+              wl.fc(1, 3, 2, "softmax")]
+    net = _plan_net(layers)
+    assert (net.patch, net.patch_x) == (5, 5)
+    assert net.info["n_fragments"] == 6 and (net.info["stride"], net.info["stride_x"]) == (2, 3)
+    tab = net.fragment_table(12, 15)
+    assert [tuple(r[5:7]) for r in tab] == [(ox, oy) for oy in range(2) for ox in range(3)]
+    net.close()
+    layers = [wl.conv(3, 1, 2, "tanh", kx=1), wl.pool(1, 2, kx=2), wl.fc(2, 2, 2, "softmax", kx=3)]
+    assert ix.patch_hw(layers) == (4, 6)
+    net = _plan_net(layers)
+    assert (net.patch, net.patch_x) == (4, 6)
+    assert net.plan(1, 10, 20)["out_h"] == 7 and net.plan(1, 10, 20)["out_w"] == 15
+    with pytest.raises(fsb.FsError):
+        net.plan(1, 10, 5)  # narrower than w_0 = 6
+    net.close()
+    assert _status(layers, patch=4) == fsb.FS_ERR_SHAPE
+    assert _status(layers, patch=6) == fsb.FS_ERR_SHAPE
+    bad = [dict(L) for L in layers]
+    bad[-1]["k"], bad[-1]["kx"] = 0, 3
+    params = wl.make_weights(layers, 0, 0.1)
+    assert _status(bad, params, patch=4) == fsb.FS_ERR_SHAPE
+    # a 2 x 3 pool on a map whose columns it does not divide (5 x 5 window,
+    # 4 x 4 map after the convolution)
+    bad = [wl.conv(2, 1, 2, "tanh"), wl.pool(2, 2, kx=3), wl.fc(0, 2, 2, "softmax")]
+    params = [(np.zeros((2, 1, 2, 2), np.float32), None), None, (np.zeros((2, 2, 3, 2), np.float32), None)]
+    assert _status(bad, params, patch=5) == fsb.FS_ERR_SHAPE
+    # 6 x 6 map: 3 x 2 after the pool, and the last layer takes a 3 x 2 kernel
+    assert _status(bad, params, patch=7) == fsb.FS_OK
 
 
 def test_single_window_image():

@@ -45,22 +45,23 @@ def _scan(fsb, layers, params, img, c0, patch=0, dtype="f32", poison=False):
 def _sample_patches(layers, B, H, W, n_random, seed):
     """Corners, the first and last window of a spread of final fragments, and
     seeded random windows, as (b, Y, X) rows."""
-    w0 = ix.patch_size(layers)
-    ny, nx = H - w0 + 1, W - w0 + 1
+    h0, w0 = ix.patch_hw(layers)
+    ny, nx = H - h0 + 1, W - w0 + 1
     pts = set()
     for b in {0, B - 1}:
         for Y in (0, ny - 1):
             for X in (0, nx - 1):
                 pts.add((b, Y, X))
-    S = 1
+    Sy = Sx = 1
     for L in layers:
         if L["kind"] == "pool":
-            S *= L["k"]
+            Sy *= ix.kyx(L)[0]
+            Sx *= ix.kyx(L)[1]
     rng = np.random.default_rng(seed)
     for _ in range(8):
-        ry, rx = int(rng.integers(0, min(S, ny))), int(rng.integers(0, min(S, nx)))
-        lastY = ry + (ny - 1 - ry) // S * S
-        lastX = rx + (nx - 1 - rx) // S * S
+        ry, rx = int(rng.integers(0, min(Sy, ny))), int(rng.integers(0, min(Sx, nx)))
+        lastY = ry + (ny - 1 - ry) // Sy * Sy
+        lastX = rx + (nx - 1 - rx) // Sx * Sx
         pts.add((0, ry, rx))
         pts.add((B - 1, lastY, lastX))
     for _ in range(n_random):
@@ -544,3 +545,147 @@ def test_conv_kernel_choice(fsb, monkeypatch, wid, mode):
     monkeypatch.setenv("FRAGSCAN_DIRECT", mode)
     got = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
     assert np.abs(got - ref).max() <= TOL[w.dtype]
+
+
+# ---- rectangular kernels, pools and windows (Section 2: per axis) ----------
+
+@pytest.mark.parametrize("seed", range(10))
+def test_rect_random_nets(fsb, seed):
+    """Random stacks of rectangular kernels and pools, full output map
+    against the fragment oracle and sampled windows against the per-patch
+    oracle; odd seeds in bf16."""
+    rng = np.random.default_rng(7000 + seed)
+    layers, (h0, w0), c0 = wl.random_rect_net(rng)
+    dt = "bf16" if seed % 2 else "f32"
+    B = 1 + seed % 2
+    H, W = h0 + int(rng.integers(0, 40)), w0 + int(rng.integers(0, 40))
+    params = wl.make_weights(layers, 7100 + seed, 0.4)
+    img = wl.make_image(7200 + seed, B, H, W, c0)
+    print("rect net", seed, [(L["kind"], ix.kyx(L)) for L in layers], (B, H, W), dt, flush=True)
+    got = _scan(fsb, layers, params, img, c0, 0, dt)
+    ref = oracle.frag_cpu.frag_scan(layers, params, img, (h0, w0))
+    assert got.shape == ref.shape == (B, H - h0 + 1, W - w0 + 1, layers[-1]["c_out"])
+    assert np.abs(got - ref).max() <= TOL[dt]
+    pts = _sample_patches(layers, B, H, W, 16, seed)
+    ref_p = oracle.patch_forward(layers, params, img, (h0, w0), pts)
+    assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref_p).max() <= TOL[dt]
+
+
+def _rect_mfma_net():
+    """Matrix-core channel counts with 3x2 / 2x3 kernels and 2x3 / 3x2 pools:
+    a 16 x 25 window, 36 final fragments."""
+    layers = [wl.conv(3, 3, 32, kx=2), wl.pool(2, 32, kx=3), wl.conv(2, 32, 48, kx=3), wl.pool(3, 48, kx=2),
+              wl.fc(2, 48, 16, kx=3), wl.fc(1, 16, 2, "softmax")]
+    assert ix.patch_hw(layers) == (16, 25)
+    return layers
+
+
+@pytest.mark.parametrize("fuse", ["0", "1"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_rect_mfma_net(fsb, monkeypatch, dt, fuse):
+    """Vector-path matrix-core layers, pools fused into the convolutions or
+    not, the head fused into the last 2 x 3 layer, two images."""
+    layers = _rect_mfma_net()
+    params = wl.make_weights(layers, 61, 0.15)
+    img = wl.make_image(62, 2, 16 + 93, 25 + 118, 3)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", fuse)
+    net = fsb.Net(layers, params, 3, 0, dt)
+    names = [L["name"] for L in net.launches(2, img.shape[1], img.shape[2])]
+    net.close()
+    assert sum(n.endswith("+pool") or "+pool+" in n for n in names) == (2 if fuse == "1" else 0), names
+    print("rect mfma", dt, fuse, names, flush=True)
+    got = _scan(fsb, layers, params, img, 3, 0, dt)
+    ref = oracle.frag_cpu.frag_scan(layers, params, img, (16, 25))
+    assert np.abs(got - ref).max() <= TOL[dt]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_rect_tile_variants(fsb, monkeypatch, dt):
+    """The same values, bit for bit, from the gather path for the first
+    layer, from run tiles, and from row tiles, on the rectangular net."""
+    layers = _rect_mfma_net()
+    params = wl.make_weights(layers, 63, 0.15)
+    img = wl.make_image(64, 1, 16 + 161, 25 + 140, 3)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "0")
+    base = _scan(fsb, layers, params, img, 3, 0, dt)
+    for var, val in (("FRAGSCAN_DIRECT", "0"), ("FRAGSCAN_RUN", "0"), ("FRAGSCAN_ROWTILES", "1"),
+                     ("FRAGSCAN_ROWTILES", "0")):
+        monkeypatch.setenv(var, val)
+        print("rect variant", dt, var, val, flush=True)
+        got = _scan(fsb, layers, params, img, 3, 0, dt)
+        monkeypatch.delenv(var)
+        if var == "FRAGSCAN_DIRECT":
+            # another first-layer kernel: another summation order
+            assert np.abs(got - base).max() <= TOL[dt]
+        else:
+            assert np.array_equal(got, base), (var, val)
+    ref = oracle.frag_cpu.frag_scan(layers, params, img, (16, 25))
+    assert np.abs(base - ref).max() <= TOL[dt]
+
+
+def test_rect_reassembly_bit_exact(fsb):
+    """Position-encoding probe with rectangular kernels and pools: a single
+    bottom-left tap per convolution and an image growing along y and x make
+    every output an exact copy of one image pixel."""
+    c = 2
+    layers, params = [], []
+    for kind, (ky, kx) in [("conv", (3, 2)), ("pool", (2, 3)), ("conv", (2, 3)), ("pool", (3, 1)),
+                           ("pool", (1, 2))]:
+        if kind == "pool":
+            layers.append(wl.pool(ky, c, kx=kx))
+            params.append(None)
+        else:
+            layers.append(wl.conv(ky, c, c, "none", kx=kx))
+            wt = np.zeros((c, c, ky, kx), np.float32)
+            for i in range(c):
+                wt[i, i, ky - 1, 0] = 1.0
+            params.append((wt, np.zeros(c, np.float32)))
+    layers.append(wl.fc(2, c, c, "none", kx=3))
+    wt = np.zeros((c, c, 2, 3), np.float32)
+    for i in range(c):
+        wt[i, i, 0, 2] = 1.0
+    params.append((wt, np.zeros(c, np.float32)))
+    h0, w0 = ix.patch_hw(layers)
+    H, W = h0 + 70, w0 + 83
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    img = np.stack([yy, xx], -1)[None].astype(np.float32)
+    got = _scan(fsb, layers, params, img, c)
+    ref = oracle.patch_forward(layers, params, img, (h0, w0))
+    assert np.array_equal(got, ref)
+    ny, nx = H - h0 + 1, W - w0 + 1
+    Y, X = np.meshgrid(np.arange(ny), np.arange(nx), indexing="ij")
+    off_y, off_x = got[0, :, :, 0] - Y, got[0, :, :, 1] - X
+    assert (off_y == off_y[0, 0]).all() and (off_x == off_x[0, 0]).all()
+
+
+@pytest.mark.parametrize("mode", ["reflect", "symmetric"])
+def test_rect_mirrored_borders(fsb, mode):
+    """Mirrored borders with an h_0 x w_0 window: each axis extended for its
+    own side; the map is H x W."""
+    layers = _rect_mfma_net()
+    params = wl.make_weights(layers, 65, 0.15)
+    img = wl.make_image(66, 1, 41, 57, 3)
+    net = fsb.Net(layers, params, 3)
+    x = torch.from_numpy(img).cuda()
+    got = net.scan(x, border=mode).cpu().numpy().astype(np.float64)
+    net.close()
+    ref = oracle.border.scan_mirrored(layers, params, img, (16, 25), mode)
+    assert got.shape == ref.shape == (1, 41, 57, 2)
+    assert np.abs(got - ref).max() <= TOL["f32"]
+
+
+def test_rect_tiled_scan(fsb):
+    """Tiled scan of the rectangular net: the untiled values bit for bit."""
+    layers = _rect_mfma_net()
+    params = wl.make_weights(layers, 67, 0.15)
+    img = wl.make_image(68, 2, 16 + 120, 25 + 131, 3)
+    net = fsb.Net(layers, params, 3)
+    x = torch.from_numpy(img).cuda()
+    ref = net.scan(x).cpu().numpy()
+    for tile in [(37, 50), (121, 7), (1000, 1000)]:
+        print("rect tiled", tile, flush=True)
+        out = torch.full_like(torch.from_numpy(ref), float("nan")).cuda()
+        net.scan_tiled(x, tile, out=out)
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), ref), tile
+    net.close()
