@@ -19,9 +19,10 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = ["-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         # accumulate matrix-core products in ordinary VGPRs (no AGPR copies)
-         "-mllvm", "-amdgpu-mfma-vgpr-form=1",
          "-Wall", "-Wno-unused-result", "-I", os.path.join(ROOT, "include")]
+# accumulate matrix-core products in ordinary VGPRs (no AGPR copies); the
+# *_wide.hip register tiles need the accumulation registers and go without
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 
 
 def sources():
@@ -30,7 +31,8 @@ def sources():
 
 def _compile(src, quiet):
     obj = os.path.join(BUILD, os.path.basename(src)[:-4] + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+    form = [] if src.endswith("_wide.hip") else VGPR_FORM
+    cmd = [HIPCC] + FLAGS + form + ["-c", src, "-o", obj]
     if not quiet:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -317,7 +317,9 @@ void plan_run_tiles(const NetLayer &l, const Geo &in, int mt, int cs, int es, in
 }
 
 // Tile choice for a conv launch (the tiling itself is described in conv_impl.h).
-fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, Launch &L)
+// wide: the float32 4 x 13 tile of conv_f32_wide.hip (l.nb = 13, l.wn = 1),
+// which has no entry in the shared tile lists.
+fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, Launch &L, bool wide = false)
 {
     const int ky = l.k, kx = l.kx;
     const int hout_max = in.hmax - ky + 1, wout_max = in.wmax - kx + 1;
@@ -349,7 +351,7 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     const int mbs[4] = {4, 2, 1, 8};
     for (int mi = 0; mi < 4; ++mi) {
         const int mb = mb_force ? mb_force : mbs[mi];
-        if (!conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
+        if (wide ? mb != 4 : !conv_tile_supported(mb, l.nb, l.wn, l.wk, l.vec)) {
             if (mb_force) break;
             continue;
         }
@@ -690,8 +692,33 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 fs_status st = pool_fuse ? plan_conv_pool_tiles(net, l, g, net->L[li + 1].k, net->L[li + 1].kx, L)
                                          : plan_conv_tiles(net, l, g, L);
                 if (st != FS_OK) return st;
+                // The float32 FC layer with the fused head on a grid that
+                // runs it one workgroup per CU (the rule below), with 14
+                // blocks of 16 for at most 208 channels (200 in N4): the
+                // 4 x 13 tile drops the padding block and covers 256 pixels
+                // per workgroup (N4 on 512 x 512: 305 -> 286 us; on larger
+                // grids, where the 7 x 2 tiles run two per CU, 14% slower).
+                // FRAGSCAN_WIDE=1 / 0 forces it on / off where it applies.
+                if (fused_here && !pool_fuse && net->dtype == DT_F32 && l.vec && l.nb == 7 && l.wn == 2 &&
+                    l.wk == 1 && l.nbt == 14 && l.cout <= 13 * 16) {
+                    const long long tiles = (long long)B * F * a.nbands * (a.run ? L.frag_tiles : a.tiles_per_band);
+                    bool wide = net->ncu > 0 && tiles <= 12LL * net->ncu &&
+                                conv_blocks_per_cu(net->dtype, g.is_image, L.mb, l.nb, l.wn, l.wk, l.vec, false,
+                                                   a.lds_bytes) == 2;
+                    if (const char *e = getenv("FRAGSCAN_WIDE"); e && e[0]) wide = e[0] == '1';
+                    if (wide) {
+                        NetLayer lw = l;
+                        lw.nb = 13;
+                        lw.wn = 1;
+                        Launch Lw = L;
+                        Lw.nb = 13;
+                        Lw.wn = 1;
+                        Lw.conv.run = 0;
+                        if (plan_conv_tiles(net, lw, g, Lw, true) == FS_OK) L = Lw;
+                    }
+                }
             }
-            L.gy = L.direct ? 1 : l.nbt / (l.nb * l.wn);
+            L.gy = L.direct ? 1 : std::max(l.nbt / (L.nb * L.wn), 1);
             if (L.direct) {
                 L.gx = B * F * ((a.out_h * a.out_w + 255) / 256);
             } else {

@@ -27,7 +27,9 @@ int conv_blocks_per_cu(int dtype, bool in_f32, int mb, int nb, int wn, int wk, b
         if (it != memo.end()) return it->second;
     }
     int n;
-    if (dtype == DT_BF16)
+    if (dtype != DT_BF16 && vec && !run && mb == 4 && nb == 13 && wn == 1 && wk == 1)
+        n = lds > 0 && (size_t)lds <= kMaxLdsBytes ? 1 : 0;  // 464 registers per lane: one wave per SIMD
+    else if (dtype == DT_BF16)
         n = conv_blocks_per_cu_bf16(in_f32, mb, nb, wn, wk, vec, run, lds);
     else
         n = vec ? conv::tile_blocks_per_cu<false, false, true>(mb, nb, wn, wk, run, lds)
@@ -60,6 +62,7 @@ hipError_t launch_conv(const ConvArgs &a, int dtype, bool in_f32, int mb, int nb
                        int gx, int gy, hipStream_t s)
 {
     if (dtype == DT_BF16) return launch_conv_bf16(a, in_f32, mb, nb, wn, wk, vec, gx, gy, s);
+    if (vec && !a.run && mb == 4 && nb == 13 && wn == 1 && wk == 1) return launch_conv_f32_wide(a, gx, gy, s);
     return vec ? conv::dispatch_tile<false, false, true>(a, mb, nb, wn, wk, gx, gy, s)
                : conv::dispatch_tile<false, false, false>(a, mb, nb, wn, wk, gx, gy, s);
 }

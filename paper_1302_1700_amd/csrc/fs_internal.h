@@ -133,6 +133,9 @@ hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, i
                              int We, int mode, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
+// The float32 4 x 13 x 1 x 1 vector-path tile (conv_f32_wide.hip; no run
+// tiles, one workgroup per CU); launch_conv routes that shape there.
+hipError_t launch_conv_f32_wide(const ConvArgs &a, int gx, int gy, hipStream_t s);
 // Whether a tile shape has an instance (run: one with run tiles).
 bool conv_tile_supported(int mb, int nb, int wn, int wk, bool vec, bool run = false);
 // Workgroups of that convolution kernel resident per CU with `lds` bytes of

@@ -286,6 +286,29 @@ def test_row_tiles_where_one_workgroup_per_cu(monkeypatch):
     assert auto["out_pixels"] == pix["out_pixels"] == rows["out_pixels"]
 
 
+def test_wide_fc_tile_plan(monkeypatch):
+    """The float32 4 x 13 tile for a 200-output FC layer with the fused head:
+    forced on, one 256-pixel tile per workgroup and a single channel-block
+    group; forced off, the 7 x 2 tiles."""
+    w = wl.WORKLOADS[2]
+    names = {}
+    for mode in ("1", "0"):
+        monkeypatch.setenv("FRAGSCAN_WIDE", mode)
+        net = _plan_net(w.layers, c0=w.channels)
+        fc = [L for L in net.launches(1, w.height, w.width) if L["name"].endswith("+head")][0]
+        names[mode] = fc
+        net.close()
+    assert names["1"]["name"].startswith("conv_frag_mfma<4, 13, 1, 1, false")
+    assert names["0"]["name"].startswith("conv_frag_mfma<4, 7, 2, 1, false")
+    assert names["1"]["grid"] * 2 == names["0"]["grid"]  # 256- against 128-pixel tiles
+    assert names["1"]["flops"] == names["0"]["flops"]
+    # bf16 nets and other channel counts keep their tiles
+    monkeypatch.setenv("FRAGSCAN_WIDE", "1")
+    net = _plan_net(w.layers, c0=w.channels, dtype="bf16")
+    assert all("<4, 13," not in L["name"] for L in net.launches(1, w.height, w.width))
+    net.close()
+
+
 def test_tiled_plans():
     """Tiled scan plans: the same output map, a workspace bounded by the
     tile, one scan's launches per tile, and the halo recomputed (more FLOPs

@@ -689,3 +689,27 @@ def test_rect_tiled_scan(fsb):
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), ref), tile
     net.close()
+
+
+@pytest.mark.parametrize("ncls", [2, 3])
+def test_wide_fc_tile(fsb, monkeypatch, ncls):
+    """The float32 4 x 13 register tile of a 200-output FC layer with the
+    fused head (two-class and general head epilogues), forced on and off,
+    against the per-patch oracle; ragged final fragments, B = 2."""
+    layers = [wl.conv(3, 1, 16), wl.pool(2, 16), wl.conv(2, 16, 48), wl.pool(2, 48),
+              wl.fc(3, 48, 200), wl.fc(1, 200, ncls, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 71 + ncls, 0.1)
+    img = wl.make_image(73 + ncls, 2, w0 + 95, w0 + 88, 1)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    got = {}
+    for mode in ("1", "0"):
+        monkeypatch.setenv("FRAGSCAN_WIDE", mode)
+        net = fsb.Net(layers, params, 1)
+        names = [L["name"] for L in net.launches(2, img.shape[1], img.shape[2])]
+        net.close()
+        assert any(n.startswith("conv_frag_mfma<4, 13, 1, 1") for n in names) == (mode == "1"), names
+        print("wide fc", ncls, mode, names[-1], flush=True)
+        got[mode] = _scan(fsb, layers, params, img, 1)
+        assert np.abs(got[mode] - ref).max() <= TOL["f32"]
+    assert np.abs(got["1"] - got["0"]).max() <= 1e-5
