@@ -713,3 +713,31 @@ def test_wide_fc_tile(fsb, monkeypatch, ncls):
         got[mode] = _scan(fsb, layers, params, img, 1)
         assert np.abs(got[mode] - ref).max() <= TOL["f32"]
     assert np.abs(got["1"] - got["0"]).max() <= 1e-5
+
+
+def test_concurrent_streams(fsb):
+    """One net, two non-default streams, distinct workspaces and outputs,
+    scans enqueued on both before either is waited for: the values of
+    scans run one at a time, bit for bit."""
+    w = wl.WORKLOADS[2]
+    params, img_a = wl.workload_inputs(2, height=230, width=210)
+    img_b = wl.make_image(91, 1, 230, 210, 1)
+    net = fsb.Net(w.layers, params, 1)
+    xa = torch.from_numpy(img_a).cuda()
+    xb = torch.from_numpy(np.ascontiguousarray(img_b)).cuda()
+    ref_a = net.scan(xa).clone()
+    ref_b = net.scan(xb).clone()
+    torch.cuda.synchronize()
+    nbytes = net.plan(1, 230, 210)["workspace_bytes"]
+    ws = [torch.empty(nbytes, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    outs = [torch.full_like(ref_a, float("nan")) for _ in range(2)]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        net.scan(xa, out=outs[0], workspace=ws[0], stream=s1)
+        net.scan(xb, out=outs[1], workspace=ws[1], stream=s2)
+    s1.synchronize()
+    s2.synchronize()
+    assert torch.equal(outs[0], ref_a)
+    assert torch.equal(outs[1], ref_b)
+    net.close()
