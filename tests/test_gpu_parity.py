@@ -741,3 +741,46 @@ def test_concurrent_streams(fsb):
     assert torch.equal(outs[0], ref_a)
     assert torch.equal(outs[1], ref_b)
     net.close()
+
+
+# ---- degenerate and maximum cases of the method ----------------------------
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_degenerate_nets(fsb, dt):
+    """Stacks at the method's corners, full map against the per-patch
+    oracle: a 1 x 1 pool (one child, the identity), 1 x 1 kernels only (the
+    window is one pixel), a lone fully connected layer (the window is the
+    whole net's input: one fragment, no pools), and an FC layer on a
+    1-pixel-wide map after pools."""
+    cases = [
+        [wl.conv(2, 2, 3), wl.pool(1, 3), wl.conv(2, 3, 4), wl.pool(2, 4), wl.fc(2, 4, 5), wl.fc(1, 5, 2, "softmax")],
+        [wl.conv(1, 3, 8), wl.conv(1, 8, 4, "none"), wl.fc(1, 4, 3, "softmax")],
+        [wl.fc(7, 2, 3, "softmax")],
+        [wl.conv(3, 2, 4), wl.pool(3, 4), wl.pool(2, 4), wl.fc(1, 4, 2, "softmax")],
+    ]
+    for n, layers in enumerate(cases):
+        c0 = layers[0]["c_in"]
+        w0 = ix.patch_size(layers)
+        params = wl.make_weights(layers, 80 + n, 0.3)
+        img = wl.make_image(90 + n, 2, w0 + 29 + n, w0 + 22, c0)
+        print("degenerate", n, dt, w0, img.shape, flush=True)
+        got = _scan(fsb, layers, params, img, c0, dtype=dt)
+        ref = oracle.patch_forward(layers, params, img, w0)
+        assert got.shape == ref.shape
+        assert np.abs(got - ref).max() <= TOL[dt], n
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_max_fragments_per_axis(fsb, dt):
+    """Pools whose sizes multiply to 256 per axis, the library's limit:
+    65,536 final fragments per image, most of them empty on this image,
+    against the per-patch oracle on every window."""
+    layers = [wl.conv(2, 1, 3), wl.pool(4, 3), wl.pool(4, 3), wl.pool(4, 3), wl.pool(4, 3),
+              wl.fc(1, 3, 2, "softmax")]
+    w0 = ix.patch_size(layers)
+    assert w0 == 257 and ix.n_fragments(layers) == 65536
+    params = wl.make_weights(layers, 95, 0.5)
+    img = wl.make_image(96, 1, w0 + 43, w0 + 33, 1)
+    got = _scan(fsb, layers, params, img, 1, dtype=dt)
+    ref = oracle.patch_forward(layers, params, img, w0)
+    assert np.abs(got - ref).max() <= TOL[dt]
