@@ -480,8 +480,17 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
 #pragma unroll
                 for (int u = 0; u < UN; ++u) {
                     const bool in = p < npx;
-                    val[u] = {};
-                    if (in && gy0 + r < hh && c0 + c < ww) val[u] = load(soff);
+                    // A tile of one fragment never reaches past its true
+                    // size: its last window row is at most hout - 1 + k_y - 1
+                    // = hh - 1, its last column c0 + twb - 1 + k_x - 1 <= ww - 1
+                    // (also for the fused pool's filter tiles).  Run tiles
+                    // stage two fragments with the wider one's columns.
+                    if constexpr (RUN) {
+                        val[u] = {};
+                        if (in && gy0 + r < hh && c0 + c < ww) val[u] = load(soff);
+                    } else {
+                        if (in) val[u] = load(soff);
+                    }
                     dsto[u] = in ? doff : -1;
                     p += P;
                     doff += dstep;
@@ -581,7 +590,11 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     // wk-th of WK equal parts of the K steps (their partial sums are added up
     // through LDS after the loop)
     constexpr int WMN = 4 / WK;
-    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    // the wave index is the same in every lane of a wave; read it from the
+    // first lane so that everything derived from it (the wave's K range,
+    // the step counters and LDS offsets of the K walk, its weight and bias
+    // addresses) is computed once per wave in scalar registers
+    const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wk = wv / WMN, wmn = wv - (wv / WMN) * WMN;
     const int wm = wmn / WN, wn = wmn - (wmn / WN) * WN;
     const int lm = lane & 15, g = lane >> 4;
