@@ -936,45 +936,66 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
                     dky.qr(y0 + r0, ybar, oy);
                     TC *dst = child_ptr(r0, c) + v * TPAD;
                     const TC *src = tile + __mul24(__mul24(r0, ew) + c, TS) + v * TPAD;
-                    for (int r = r0; r < r1; ++r) {
-                        u4 m = *reinterpret_cast<const u4 *>(src);
-                        auto tap = [&](int ii, int jj) {
-                            const u4 x = *reinterpret_cast<const u4 *>(src + __mul24(__mul24(ii, ew) + jj, TS));
+                    auto vmax = [&](u4 m, const u4 x) {
 #pragma unroll
-                            for (int e = 0; e < 4; ++e) {
-                                if constexpr (BF)
-                                    m[e] = max_i16x2(m[e], x[e]);
-                                else
-                                    m[e] = __float_as_uint(fmaxf(__uint_as_float(m[e]), __uint_as_float(x[e])));
-                            }
-                        };
-                        if constexpr (KC == 2) {
-                            tap(0, 1);
-                            tap(1, 0);
-                            tap(1, 1);
-                        } else if constexpr (KC > 0) {
-                            // one row of taps in flight (fewer registers for
-                            // the kernel as a whole)
-#pragma unroll 1
-                            for (int i = 0; i < KC; ++i)
-#pragma unroll
-                                for (int j = 0; j < KC; ++j)
-                                    if (i + j > 0) tap(i, j);
-                        } else {
-                            for (int i = 0; i < KY; ++i)
-                                for (int j = 0; j < KX; ++j) tap(i, j);
+                        for (int e = 0; e < 4; ++e) {
+                            if constexpr (BF)
+                                m[e] = max_i16x2(m[e], x[e]);
+                            else
+                                m[e] = __float_as_uint(fmaxf(__uint_as_float(m[e]), __uint_as_float(x[e])));
                         }
+                        return m;
+                    };
+                    auto put = [&](u4 m) {
                         if constexpr (BF) {
 #pragma unroll
                             for (int e = 0; e < 4; ++e) m[e] = bf16x2_key(m[e]);
                         }
                         *reinterpret_cast<u4 *>(dst) = m;
-                        src += ew * TS;
                         if (++oy == KY) {
                             oy = 0;
                             dst += d_yb - (KY - 1) * d_oy;
                         } else {
                             dst += d_oy;
+                        }
+                    };
+                    if constexpr (KC > 0) {
+                        // Separable: the filter value at row r is the maximum
+                        // of the KC row maxima h(r) .. h(r + KC - 1), where
+                        // h(rr) = max_j tile[rr][c + j]; a run keeps the last
+                        // KC - 1 row maxima, so each row is read once per run
+                        // (KC reads and 2 (KC - 1) maxima per value instead of
+                        // KC^2 reads and KC^2 - 1 maxima).  max is exact, so
+                        // the values are those of the direct form.
+                        auto hrow = [&](const TC *row) {
+                            u4 h = *reinterpret_cast<const u4 *>(row);
+#pragma unroll
+                            for (int j = 1; j < KC; ++j) h = vmax(h, *reinterpret_cast<const u4 *>(row + j * TS));
+                            return h;
+                        };
+                        const int rstep = ew * TS;
+                        u4 hr[KC];
+#pragma unroll
+                        for (int i = 0; i + 1 < KC; ++i) hr[i] = hrow(src + i * rstep);
+                        src += (KC - 1) * rstep;
+                        for (int r = r0; r < r1; ++r) {
+                            hr[KC - 1] = hrow(src);
+                            u4 m = hr[0];
+#pragma unroll
+                            for (int i = 1; i < KC; ++i) m = vmax(m, hr[i]);
+                            put(m);
+#pragma unroll
+                            for (int i = 0; i + 1 < KC; ++i) hr[i] = hr[i + 1];
+                            src += rstep;
+                        }
+                    } else {
+                        for (int r = r0; r < r1; ++r) {
+                            u4 m = *reinterpret_cast<const u4 *>(src);
+                            for (int i = 0; i < KY; ++i)
+                                for (int j = 0; j < KX; ++j)
+                                    m = vmax(m, *reinterpret_cast<const u4 *>(src + __mul24(__mul24(i, ew) + j, TS)));
+                            put(m);
+                            src += ew * TS;
                         }
                     }
                 }
