@@ -420,6 +420,33 @@ def test_pool_fusion_modes(fsb, monkeypatch, fuse, dt):
     assert np.abs(got - ref).max() <= TOL[dt]
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_pool_fusion_bit_exact(fsb, monkeypatch, dt):
+    """A pool fused into the convolution's epilogue gives the values of the
+    separate pool kernel bit for bit (same K walk per pixel, and the maximum
+    is exact): 3x3 and 2x2 pools, 32 and 64 channels (one wave per pixel
+    block, no split K), ragged fragments, B = 2."""
+    layers = [wl.conv(2, 3, 32), wl.pool(3, 32), wl.conv(3, 32, 32), wl.pool(2, 32),
+              wl.conv(2, 32, 64), wl.pool(2, 64), wl.fc(2, 64, 24), wl.fc(1, 24, 3, "softmax")]
+    w0 = ix.patch_size(layers)
+    params = wl.make_weights(layers, 71, 0.2)
+    img = wl.make_image(72, 2, w0 + 53, w0 + 61, 3)
+    outs = {}
+    for fuse in ("0", "1"):
+        monkeypatch.setenv("FRAGSCAN_POOL_FUSE", fuse)
+        net = fsb.Net(layers, params, 3, 0, dt)
+        names = [L["name"] for L in net.launches(2, img.shape[1], img.shape[2])]
+        net.close()
+        assert sum(n.endswith("+pool") for n in names) == (3 if fuse == "1" else 0), names
+        print("pool fusion bit-exact", dt, fuse, names, flush=True)
+        outs[fuse] = _scan(fsb, layers, params, img, 3, dtype=dt)
+    assert np.array_equal(outs["0"], outs["1"])
+    pts = np.array([(b, y, x) for b in range(2) for y in (0, 17, img.shape[1] - w0)
+                    for x in (0, 29, img.shape[2] - w0)], np.int32)
+    ref = oracle.patch_forward(layers, params, img, w0, pts)
+    assert np.abs(outs["1"][pts[:, 0], pts[:, 1], pts[:, 2]] - ref).max() <= TOL[dt]
+
+
 def test_pool_fusion_split_k(fsb, monkeypatch):
     """Split-K (two waves per pixel block) feeding the fused pool."""
     layers = [wl.conv(2, 1, 48), wl.pool(2, 48), wl.conv(3, 48, 48), wl.pool(2, 48),
