@@ -383,3 +383,24 @@ def test_status_strings():
     lib = fsb.load()
     for s in range(7):
         assert lib.fs_status_str(s)
+
+
+def test_bench_cpu_fragment_leg():
+    """bench.py's CPU fragment leg: the full image when it is small enough, a
+    top-left crop of image 0 with the requested number of windows otherwise,
+    and a crop scan that gives the full scan's values on those windows."""
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+    import oracle
+    w = wl.WORKLOADS[1]
+    params, img = wl.workload_inputs(1)
+    full = bench.cpu_fragment_baseline(w, params, img)
+    assert full["sample"] == "full image" and full["value"] > 0
+    crop = bench.cpu_fragment_baseline(w, params, img, max_windows=144)
+    assert crop["sample"] == "top-left crop 25x25 of image 0 (144 windows)", crop["sample"]
+    whole = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    part = oracle.frag_cpu.frag_scan(w.layers, params, img[:1, :25, :25], w.patch)
+    assert part.shape == (1, 12, 12, w.n_classes)
+    assert np.abs(part - whole[:1, :12, :12]).max() <= 1e-12
