@@ -2,6 +2,7 @@
 table: per kernel name, calls, total and mean duration.
 
     python -m paper_1302_1700_amd.profsum <results.db | kernel_trace.csv | dir> [--pmc]
+    python -m paper_1302_1700_amd.profsum util <pmc dir>
     python -m paper_1302_1700_amd.profsum copy <MiB>
     python -m paper_1302_1700_amd.profsum traffic <fetch_dir> <write_dir> <copy_fetch_dir>
            <copy_write_dir> <copy_MiB> <workload> [--out profiles/traffic.json]
@@ -128,6 +129,31 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, workload, ou
     print("scales: FETCH x%.4f  WRITE x%.4f  -> %s" % (fscale, wscale, out))
 
 
+def utilisation(path, simds=1024, xcds=8):
+    """Per kernel name, from one SQ counter pass (SQ_WAVES, SQ_INSTS_VALU,
+    SQ_INSTS_MFMA, SQ_INSTS_SALU, SQ_INSTS_LDS, SQ_INSTS_VMEM_RD,
+    SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE): the matrix cores' busy
+    fraction over the dispatch (busy cycles summed over all SIMDs, against
+    the GPU-active cycles of one XCD times the SIMD count) and the
+    instructions each wave issued."""
+    rows = []
+    for k, cs in pmc_stats(path).items():
+        if not k or not k.startswith("void fs::"):
+            continue
+        waves = cs.get("SQ_WAVES", 0.0) or 1.0
+        active = cs.get("GRBM_GUI_ACTIVE", 0.0) / xcds
+        busy = cs.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        mfma = cs.get("SQ_INSTS_MFMA", 0.0)
+        rows.append((k, busy / (active * simds) if active else 0.0, mfma / waves,
+                     (cs.get("SQ_INSTS_VALU", 0.0) - mfma) / waves, cs.get("SQ_INSTS_SALU", 0.0) / waves,
+                     cs.get("SQ_INSTS_LDS", 0.0) / waves, cs.get("SQ_INSTS_VMEM_RD", 0.0) / waves,
+                     busy / mfma if mfma else 0.0, waves))
+    print("%-78s %6s %7s %7s %6s %5s %5s %6s %8s" % ("kernel", "mfma%", "mfma/w", "valu/w", "salu/w",
+                                                      "lds/w", "vmr/w", "cyc/mf", "waves"))
+    for r in sorted(rows, key=lambda r: -r[1]):
+        print("%-78s %5.1f%% %7.1f %7.1f %6.1f %5.1f %5.1f %6.1f %8.0f" % ((r[0][:78], 100 * r[1]) + r[2:]))
+
+
 def main():
     args = [a for a in sys.argv[1:] if not a.startswith("--")]
     if args and args[0] == "traffic":
@@ -139,6 +165,9 @@ def main():
         return
     if args and args[0] == "copy":
         copy_probe(int(args[1]))
+        return
+    if args and args[0] == "util":
+        utilisation(args[1])
         return
     if "--pmc" in sys.argv:
         for k, cs in pmc_stats(args[0]).items():
