@@ -12,17 +12,22 @@ one JSON line:
                back-to-back runs of that launch on the scan's stream), against
                the MI355X peak for its bound
   launches     the same for every launch of the scan
-  cpu_baseline the per-patch CPU oracle on a bounded sample of windows, on
-               this host's cores
-  cpu_fragment the fragment method on the CPU (float64) on the same host:
-               the full image of the default workload, a crop of about as
-               many windows for the larger ones
-Default workload: net N4 (the paper's Table 1 net) on a 512 x 512 greyscale
-image, 418 x 418 windows.  --border reflect / symmetric scans with mirrored
-edges instead (Section 3.2's setup: one output per pixel, 512 x 512); the
-per-launch figures then come from the scan of the extended image.  --tile R,C
-scans in output tiles (fs_scan_tiled: a workspace bounded by the tile); the
-per-launch figures stay those of the untiled scan.
+  cpu_baseline the per-patch CPU oracle on a deterministic sample of
+               windows (every image's corners, the first and last window of
+               every final fragment of every image, 4096 seeded random
+               windows), on this host's cores
+  cpu_fragment the fragment method on the CPU (float64) on the same host, on
+               all cores and on one core: the full image when it has at most
+               418 x 418 windows, else a top-left crop of image 0 with about
+               that many
+Default workload: net N4 (the paper's Table 1 net) on a batch of eight
+1024 x 1024 greyscale images (8 x 930 x 930 windows), the largest of the
+workloads; --workload 2 is the paper's own size, one 512 x 512 slice.
+--border reflect / symmetric scans with mirrored edges instead (Section 3.2's
+setup: one output per pixel); the per-launch figures then come from the scan
+of the extended image.  --tile R,C scans in output tiles (fs_scan_tiled: a
+workspace bounded by the tile); the per-launch figures stay those of the
+untiled scan.
 """
 import argparse
 import json
@@ -40,8 +45,9 @@ PEAK = {  # MI355X published dense peaks
 }
 
 
-def measured_traffic(kernel_name, workload):
-    """HBM bytes per launch from the committed rocprofv3 counter summary
+def measured_traffic(launch_name, layer, workload):
+    """HBM bytes of one launch (the scan's launch of that name and first
+    layer) from the committed rocprofv3 counter summary
     (profiles/traffic.json), if it was taken on the current kernel sources;
     else None."""
     from paper_1302_1700_amd.profsum import source_digest
@@ -50,46 +56,73 @@ def measured_traffic(kernel_name, workload):
         return None
     with open(path) as f:
         entries = json.load(f)
-    base = kernel_name.split("+")[0]
     for e in entries:
-        if base in e.get("kernel", "") and e.get("workload") == workload \
+        if e.get("launch") == launch_name and e.get("layer") == layer and e.get("workload") == workload \
                 and e.get("source_digest") == source_digest():
             return e.get("bytes_per_launch")
     return None
 
 
-def cpu_baseline(w, params, img, seconds_target=15.0):
-    """Per-patch oracle on a deterministic sample of windows."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_windows(w, n_random=4096, seed=1234):
+    """The deterministic window sample of the per-patch baseline: every
+    image's corners, the first and the last window of every final fragment
+    of every image (from the oracle's corner tracking), and n_random seeded
+    random windows; (b, Y, X) rows."""
     import numpy as np
-    import oracle
-    rng = np.random.default_rng(1234)
+    from oracle import index as ix
     ny, nx = w.out_h, w.out_w
-    # calibrate on a small sample, then size the timed sample
-    cal = np.stack([rng.integers(0, w.batch, 16), rng.integers(0, ny, 16), rng.integers(0, nx, 16)], 1)
-    t0 = time.perf_counter()
-    oracle.patch_forward(w.layers, params, img, w.patch, cal)
-    rate = 16 / max(time.perf_counter() - t0, 1e-6)
-    n = int(min(max(rate * seconds_target, 32), 20000))
-    pts = np.stack([rng.integers(0, w.batch, n), rng.integers(0, ny, n), rng.integers(0, nx, n)], 1)
+    f = ix.reassembly_index(w.layers, w.height, w.width)[..., 0].ravel()
+    _, first = np.unique(f, return_index=True)
+    _, last_rev = np.unique(f[::-1], return_index=True)
+    flat = np.concatenate([first, f.size - 1 - last_rev])
+    rng = np.random.default_rng(seed)
+    rows = [np.array([(b, Y, X) for b in range(w.batch) for Y in (0, ny - 1) for X in (0, nx - 1)])]
+    for b in range(w.batch):
+        rows.append(np.stack([np.full(flat.size, b), flat // nx, flat % nx], 1))
+    rows.append(np.stack([rng.integers(0, w.batch, n_random), rng.integers(0, ny, n_random),
+                          rng.integers(0, nx, n_random)], 1))
+    return np.unique(np.concatenate(rows), axis=0).astype(np.int32)
+
+
+def cpu_baseline(w, params, img):
+    """Per-patch oracle on the deterministic window sample (oracle_windows)."""
+    import oracle
+    pts = oracle_windows(w)
+    n = len(pts)
     t0 = time.perf_counter()
     oracle.patch_forward(w.layers, params, img, w.patch, pts)
     dt = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", 0)) or len(os.sched_getaffinity(0))
-    total = w.batch * ny * nx
+    cores = min(int(os.environ.get("OMP_NUM_THREADS", 0)) or 1 << 30, len(os.sched_getaffinity(0)))
+    total = w.batch * w.out_h * w.out_w
     return {
         "value": n / dt,
         "unit": "output px/s",
         "cores": cores,
         "kind": "oracle",
-        "sample": "%d seeded random windows of the same image, per-patch float64 forward "
-                  "(C, OpenMP); full map extrapolates to %.0f s" % (n, total / (n / dt)),
+        "cpu_model": cpu_model(),
+        "seconds": dt,
+        "sample": "%d windows of the same images: corners, the first and last window of every final "
+                  "fragment of every image, 4096 seeded random; per-patch float64 forward (C, OpenMP); "
+                  "the full map extrapolates to %.0f s" % (n, total / (n / dt)),
     }
 
 
-def cpu_fragment_baseline(w, params, img, max_windows=418 * 418):
+def cpu_fragment_baseline(w, params, img, max_windows=418 * 418, one_core=True):
     """The fragment method on the CPU (float64, numpy/BLAS): the full image
-    when it has at most max_windows windows (the default workload), else a
-    top-left crop of image 0 with about that many."""
+    when it has at most max_windows windows, else a top-left crop of image 0
+    with about that many; on all cores, then (one_core) the same on one core
+    (BLAS limited to one thread)."""
     import oracle
     ny, nx = w.out_h, w.out_w
     sample = "full image"
@@ -98,13 +131,25 @@ def cpu_fragment_baseline(w, params, img, max_windows=418 * 418):
         ny, nx = min(ny, side), min(nx, side)
         img = img[:1, :ny + w.patch - 1, :nx + w.patch - 1]
         sample = "top-left crop %dx%d of image 0 (%d windows)" % (img.shape[1], img.shape[2], ny * nx)
+    n = ny * nx if sample != "full image" else w.batch * ny * nx
     t0 = time.perf_counter()
     oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
     dt = time.perf_counter() - t0
-    n = ny * nx if sample != "full image" else w.batch * ny * nx
-    return {"value": n / dt, "unit": "output px/s", "seconds": dt,
-            "cores": len(os.sched_getaffinity(0)), "kind": "cpu fragment method (float64)",
-            "sample": sample}
+    from threadpoolctl import threadpool_info
+    blas = [p.get("num_threads", 1) for p in threadpool_info() if p.get("user_api") == "blas"]
+    cores = min(max(blas) if blas else 1, len(os.sched_getaffinity(0)))
+    res = {"value": n / dt, "unit": "output px/s", "seconds": dt,
+           "cores": cores, "kind": "cpu fragment method (float64)",
+           "cpu_model": cpu_model(), "sample": sample}
+    if one_core:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+            dt1 = time.perf_counter() - t0
+        res["one_core"] = {"value": n / dt1, "unit": "output px/s", "seconds": dt1, "cores": 1,
+                           "sample": sample}
+    return res
 
 
 def main():
@@ -112,7 +157,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--workload", type=int, default=4)
     ap.add_argument("--profile-reps", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU baseline legs")
     ap.add_argument("--no-cpu-fragment", action="store_true",
@@ -195,7 +240,7 @@ def main():
     dom = max(rows, key=lambda r: r["ms"])
     conv_flops = sum(r["flops"] for r in rows)
     conv_ms = sum(r["ms"] for r in rows if r["flops"] > 0)
-    traffic = measured_traffic(dom["name"], w.name)
+    traffic = measured_traffic(dom["name"], dom["layer"], w.name) if border == "valid" else None
     if dom["bound"] == "mfma":
         roof = {"bound": "mfma", "achieved": dom["tflops"], "peak": peak_mm, "unit": "TFLOP/s",
                 "frac": dom["tflops"] / peak_mm}

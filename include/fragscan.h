@@ -173,7 +173,11 @@ fs_status fs_net_query(const fs_net *net, fs_net_info *out);
 
 /* Sizes and work of a scan of B images of H x W (Section 2.2: an s x s image
  * with s >= w_0 gives (s - w_0 + 1)^2 windows; rectangular images are the
- * per-axis generalisation).  FS_ERR_SHAPE if H or W < w_0 or B < 1. */
+ * per-axis generalisation).  FS_ERR_SHAPE if H or W < w_0 or B < 1.
+ * FS_ERR_UNSUPPORTED if H or W is above 65535 (fragment sizes are kept in
+ * 16-bit tables; fs_scan_tiled scans such an image in regions of at most that
+ * size), if B times the net's final fragment count reaches 2^24, or if a
+ * fragment would hold 2^31 or more elements. */
 fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_plan_info *out);
 
 /* Per-launch description of the scan fs_scan would enqueue; writes
@@ -181,10 +185,18 @@ fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_pl
 fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W,
                            fs_launch_info *h_out, int32_t capacity);
 
-/* Scan B images.  d_image: device [B][H][W][C] float32; d_out: device
- * [B][H-w_0+1][W-w_0+1][n_classes] float32; d_workspace: device scratch of at
- * least fs_scan_plan's workspace_bytes (contents need not be initialised and
- * are clobbered).  All three 256-byte aligned, non-overlapping.  `stream` is a
+/* Scan B images: the fragment-based forward propagation of Section 2.2 (every
+ * convolution computed once on the extended maps of every fragment, Eqs. 3-4;
+ * every k x k max-pool splitting each fragment into its k^2 offset children,
+ * Eqs. 5-7), then the last layer's softmax and the reassembly of the final
+ * fragments into one output per window (Section 3: the fragments cover every
+ * window exactly once).  Same limits as fs_scan_plan.
+ * d_image: device [B][H][W][C] float32, 16-byte aligned; d_out: device
+ * [B][H-w_0+1][W-w_0+1][n_classes] float32, 16-byte aligned; d_workspace:
+ * device scratch of at least fs_scan_plan's workspace_bytes, 256-byte aligned
+ * (contents need not be initialised and are clobbered); the three must not
+ * overlap.  FS_ERR_INVALID_ARG for a NULL or misaligned pointer,
+ * FS_ERR_WORKSPACE for a workspace below the plan's size.  `stream` is a
  * hipStream_t (NULL = the default stream).  Asynchronous: returns once every
  * kernel is enqueued; a device fault shows up at the caller's next stream
  * synchronisation.  Calls on different streams with distinct workspaces and

@@ -249,6 +249,10 @@ struct Plan {
 
 size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
+// Workgroups of one launch dimension: HIP takes fewer than 2^32 work-items
+// per dimension (256 per workgroup here).
+constexpr long long kMaxGrid = (1LL << 32) / 256;
+
 void fill_axis(AxisTable &t, const Geo &g)
 {
     std::memset(&t, 0, sizeof t);
@@ -573,6 +577,14 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
     if (B < 1 || H < 1 || W < 1) return fail(FS_ERR_SHAPE, "B, H, W must be >= 1");
     if (H < net->patch || W < net->patch_x)
         return fail(FS_ERR_SHAPE, "image %dx%d smaller than the window %dx%d", H, W, net->patch, net->patch_x);
+    // fragment sizes travel as 16-bit per-axis tables; a larger image (or
+    // tiled-scan region) goes through fs_scan_tiled with fewer rows / columns
+    if (H > kMaxSide || W > kMaxSide)
+        return fail(FS_ERR_UNSUPPORTED, "image (or tile region) %dx%d has a side above %d; scan it in tiles "
+                    "(fs_scan_tiled) of fewer rows / columns", H, W, kMaxSide);
+    // fragment batch indices (B * F) and per-launch fragment counts are int
+    if ((long long)B * net->F >= (1LL << 24))
+        return fail(FS_ERR_UNSUPPORTED, "batch %d x %d fragments: scan fewer images per call", B, net->F);
     P = Plan();
     P.B = B;
     P.H = H;
@@ -636,11 +648,11 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             a.kx = kx;
             a.n_children = B * F * ky * kx;
             fill_axis(a.ext, g);
-            L.gx = B * F * ky * kx * a.out_h;
+            L.gx = (int)std::min<long long>((long long)B * F * ky * kx * a.out_h, kMaxGrid);
             L.frags = B * F * ky * kx;
             L.out_pixels = (long long)B * true_pixels(o);
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * o.C * es;
-            L.name = pool_kernel_name(net->dtype, g.is_image);
+            L.name = pool_kernel_name(net->dtype, g.is_image, ky, kx, g.C);
         } else {  // conv or fc as convolution
             const int ky = l.k, kx = l.kx;
             o.Qy = g.Qy;
@@ -720,13 +732,14 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             }
             L.gy = L.direct ? 1 : std::max(l.nbt / (L.nb * L.wn), 1);
             if (L.direct) {
-                L.gx = B * F * ((a.out_h * a.out_w + 255) / 256);
+                L.gx = (int)std::min<long long>((long long)B * F * (((long long)a.out_h * a.out_w + 255) / 256),
+                                                kMaxGrid);
             } else {
                 // grid (a multiple of 8 for the XCD-contiguous tile order)
                 // and dynamic LDS of either tiling; returns the rounds of
                 // workgroups the device needs for it
-                auto finish = [&](bool run, int tiles, int &lds, int &gx) {
-                    gx = (tiles + 7) / 8 * 8;
+                auto finish = [&](bool run, long long tiles, int &lds, int &gx) {
+                    gx = (int)std::min<long long>((tiles + 7) / 8 * 8, kMaxGrid);
                     // The FC layer with the fused head, when its register
                     // tile fits only two workgroups per CU, ran 2-7% faster
                     // one per CU on grids of at most 12 workgroups per CU
@@ -743,14 +756,15 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                     return ((long long)gx * L.gy + slots - 1) / slots;
                 };
                 int lds = a.lds_bytes, gx = 0;
-                const long long rounds = finish(a.run, (a.run ? B : B * F) * a.nbands * a.tiles_per_band, lds, gx);
+                const long long rounds =
+                    finish(a.run, (long long)(a.run ? B : B * F) * a.nbands * a.tiles_per_band, lds, gx);
                 if (a.run) {
                     // Run tiles only where they save a round of workgroups:
                     // with equal rounds their two-fragment windows cost
                     // 2% (N4's 3x3 layer on 512 x 512: 1375 run tiles
                     // against 1536, 6 rounds each); FRAGSCAN_RUN=1 keeps them.
                     int lds_f = L.frag_lds, gx_f = 0;
-                    const long long rounds_f = finish(false, B * F * L.frag_tiles, lds_f, gx_f);
+                    const long long rounds_f = finish(false, (long long)B * F * L.frag_tiles, lds_f, gx_f);
                     const char *e = getenv("FRAGSCAN_RUN");
                     if (rounds >= rounds_f && !(e && e[0] == '1')) {
                         a.run = 0;
@@ -808,10 +822,14 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             if (!L.direct && a.run) L.name += "+run";
         }
         o.is_image = false;
-        // kernels address within one fragment (or image) with 32-bit offsets
+        // kernels address within one fragment (or image) with 32-bit offsets;
+        // a tiled scan's first layer reads its region with the image's pitch
         if ((long long)std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C >= (1LL << 31) ||
-            (long long)std::max(g.hmax, 1) * std::max(g.wmax, 1) * g.C >= (1LL << 31))
+            (long long)std::max(g.hmax, 1) * std::max(g.wmax, 1) * g.C >= (1LL << 31) ||
+            (g.is_image && (long long)g.hmax * img_w * g.C >= (1LL << 31)))
             return fail(FS_ERR_UNSUPPORTED, "layer %d: a fragment holds 2^31 or more elements", li);
+        if (L.gx >= kMaxGrid || L.gx < 1)
+            return fail(FS_ERR_UNSUPPORTED, "layer %d: grid too large; scan the image in tiles", li);
         if (L.dst != 2) {
             const size_t out_bytes = (size_t)B * o.Qy * o.Qx * std::max(o.hmax, 1) * std::max(o.wmax, 1) * o.C * es;
             buf = std::max(buf, out_bytes);
@@ -864,6 +882,10 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         digits(net->pool_k, net->S, a.digit_y);
         digits(net->pool_kx, net->Sx, a.digit_x);
         const long long npix = (long long)B * P.ny * P.nx;
+        // the head numbers a window within its image with 32-bit integers
+        if ((long long)P.ny * P.nx >= (1LL << 31) || (npix + 15) / 16 >= kMaxGrid)
+            return fail(FS_ERR_UNSUPPORTED, "%d x %d windows per image (batch %d): scan the image in tiles", P.ny,
+                        P.nx, B);
         L.gx = (int)((npix + 15) / 16);
         L.frags = B * a.F;
         L.out_pixels = npix;

@@ -21,6 +21,7 @@
 namespace fs {
 
 constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of pool sizes)
+constexpr int kMaxSide = 65535; // image rows / columns of one scan (fragment sizes are 16-bit)
 constexpr int kMaxHeadClasses = 16;
 constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
 constexpr size_t kMaxLdsBytes = 160 * 1024;  // LDS of one CDNA4 compute unit
@@ -154,7 +155,7 @@ std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int taps);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run);
-const char *pool_kernel_name(int dtype, bool in_f32);
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int C);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
 }  // namespace fs

@@ -17,6 +17,7 @@
 // stored back unchanged.
 #include "fs_internal.h"
 
+#include <cstdio>
 #include <type_traits>
 
 namespace fs {
@@ -249,9 +250,18 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
     return (a.C % 8 == 0) ? go_k<true, false, 8>(a, grid, s) : go_k<true, false, 1>(a, grid, s);
 }
 
-const char *pool_kernel_name(int dtype, bool in_f32)
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int C)
 {
-    return dtype == DT_F32 ? "pool_frag<f32>" : (in_f32 ? "pool_frag<bf16<-f32>" : "pool_frag<bf16>");
+    // the instance launch_pool picks, as the profiler names it
+    const bool bf = dtype == DT_BF16, bin = bf && in_f32;
+    const int v = !bf ? (C % 4 == 0 ? 4 : 1) : (in_f32 ? 1 : (C % 8 == 0 ? 8 : 1));
+    const char *t = bf ? "true" : "false", *ti = bin ? "true" : "false";
+    char buf[64];
+    if (ky == kx && ky >= 2 && ky <= 4)
+        snprintf(buf, sizeof buf, "pool_frag_rows<%d, %s, %s, %d>", ky, t, ti, v);
+    else
+        snprintf(buf, sizeof buf, "pool_frag<%s, %s, %d>", t, ti, v);
+    return buf;
 }
 
 }  // namespace fs

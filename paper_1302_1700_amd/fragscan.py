@@ -106,6 +106,38 @@ def _check(st):
         raise FsError(st, lib.fs_last_error().decode())
 
 
+def check_tensors(image, out, workspace, in_channels, out_shape, require_cuda=True):
+    """Argument checks done before any pointer reaches the library, which
+    only sees addresses and sizes: the image must be a contiguous float32
+    [B, H, W, in_channels] tensor (on a GPU unless require_cuda is False);
+    `out`, when given, a contiguous float32 tensor of exactly out_shape on
+    the image's device; `workspace`, when given, a contiguous tensor on the
+    image's device.  Raises ValueError."""
+    import torch
+    if image.dim() != 4 or image.dtype != torch.float32 or not image.is_contiguous():
+        raise ValueError("image must be a contiguous float32 tensor [B, H, W, C]")
+    if require_cuda and not image.is_cuda:
+        raise ValueError("image must be on a GPU")
+    if image.shape[3] != in_channels:
+        raise ValueError("image has %d channels, the net takes %d" % (image.shape[3], in_channels))
+    if out is not None:
+        if out.dtype != torch.float32 or not out.is_contiguous():
+            raise ValueError("out must be a contiguous float32 tensor")
+        if tuple(out.shape) != tuple(out_shape):
+            raise ValueError("out has shape %s, the scan writes %s" % (tuple(out.shape), tuple(out_shape)))
+        if out.device != image.device:
+            raise ValueError("out is on %s, the image on %s" % (out.device, image.device))
+    if workspace is not None:
+        if not workspace.is_contiguous():
+            raise ValueError("workspace must be contiguous")
+        if workspace.device != image.device:
+            raise ValueError("workspace is on %s, the image on %s" % (workspace.device, image.device))
+
+
+def _nbytes(t):
+    return t.numel() * t.element_size()
+
+
 def _stream_handle(stream=None):
     import torch
     s = stream if stream is not None else torch.cuda.current_stream()
@@ -227,23 +259,24 @@ class Net:
         (border "valid"), or [B, H, W, n] with the image's edges mirrored
         ("reflect": about the edge pixels, "symmetric": edge pixels repeated)."""
         import torch
-        if not image.is_cuda or image.dtype != torch.float32 or not image.is_contiguous():
-            raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
         if border not in BORDER:
             raise ValueError("border must be one of %s" % sorted(BORDER))
+        if image.dim() != 4:
+            raise ValueError("image must be [B, H, W, C]")
         B, H, W, C = image.shape
         oh, ow = (H - self.patch + 1, W - self.patch_x + 1) if border == "valid" else (H, W)
+        check_tensors(image, out, workspace, self.info["in_channels"], (B, oh, ow, self.n_classes))
         if out is None:
             out = torch.empty((B, oh, ow, self.n_classes), dtype=torch.float32, device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, border)
         if border == "valid":
             _check(load().fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
                                   ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                  ws.numel(), _stream_handle(stream)))
+                                  _nbytes(ws), _stream_handle(stream)))
         else:
             _check(load().fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
                                          ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                         ws.numel(), _stream_handle(stream)))
+                                         _nbytes(ws), _stream_handle(stream)))
         return out
 
     def scan_tiled(self, image, tile, out=None, workspace=None, stream=None):
@@ -251,15 +284,16 @@ class Net:
         most tile = (rows, cols) windows, each a fragment scan of the image
         region it covers, sharing one workspace sized for a tile."""
         import torch
-        if not image.is_cuda or image.dtype != torch.float32 or not image.is_contiguous():
-            raise ValueError("image must be a contiguous float32 CUDA tensor [B, H, W, C]")
+        if image.dim() != 4:
+            raise ValueError("image must be [B, H, W, C]")
         B, H, W, C = image.shape
+        shape = (B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes)
+        check_tensors(image, out, workspace, self.info["in_channels"], shape)
         if out is None:
-            out = torch.empty((B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes), dtype=torch.float32,
-                              device=image.device)
+            out = torch.empty(shape, dtype=torch.float32, device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, tile=tile)
         _check(load().fs_scan_tiled(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, int(tile[0]), int(tile[1]),
-                                    ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), ws.numel(),
+                                    ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), _nbytes(ws),
                                     _stream_handle(stream)))
         return out
 
@@ -268,14 +302,17 @@ class Net:
         times back to back between two HIP events on the stream
         (synchronises; `out` ends as after one scan)."""
         import torch
+        if image.dim() != 4:
+            raise ValueError("image must be [B, H, W, C]")
         B, H, W, C = image.shape
+        shape = (B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes)
+        check_tensors(image, out, None, self.info["in_channels"], shape)
         if out is None:
-            out = torch.empty((B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes),
-                              dtype=torch.float32, device=image.device)
+            out = torch.empty(shape, dtype=torch.float32, device=image.device)
         ws = self.workspace(B, H, W, image.device)
         n = self.plan(B, H, W)["n_launches"]
         ms = (ctypes.c_float * n)()
         _check(load().fs_scan_profile(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
                                       ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                      ws.numel(), _stream_handle(stream), reps, ms, n))
+                                      _nbytes(ws), _stream_handle(stream), reps, ms, n))
         return list(ms)

@@ -5,16 +5,20 @@ table: per kernel name, calls, total and mean duration.
     python -m paper_1302_1700_amd.profsum util <pmc dir>
     python -m paper_1302_1700_amd.profsum copy <MiB>
     python -m paper_1302_1700_amd.profsum traffic <fetch_dir> <write_dir> <copy_fetch_dir>
-           <copy_write_dir> <copy_MiB> <workload> [--out profiles/traffic.json]
+           <copy_write_dir> <copy_MiB> <bench_log> [--out profiles/traffic.json]
 
 With --pmc, counter values per kernel dispatch are averaged per kernel name
 (FETCH_SIZE / WRITE_SIZE and the like).  `copy` runs a plain device-to-device
 copy of a tensor of the given size (read once, written once): the calibration
 point for the FETCH_SIZE / WRITE_SIZE counters.  `traffic` turns a FETCH_SIZE
-pass and a WRITE_SIZE pass of a workload, plus the same two passes of the copy
-probe, into HBM bytes per launch: each counter is scaled by (bytes the copy
-moved) / (what the counter read for it), and the entry records the digest of
-the kernel sources it was taken on.
+pass and a WRITE_SIZE pass of bench.py over a workload, plus the same two
+passes of the copy probe, into HBM bytes per launch of the scan: each counter
+is scaled by (bytes the copy moved) / (what the counter read for it).  The
+dispatches of the library's kernels are matched to the scan's launches by
+their order (bench.py's JSON line, in <bench_log>, lists the launches; its
+warm-up and timed scans run them in that order), so a kernel instance used by
+several layers gets one entry per layer; each entry records the digest of the
+kernel sources it was taken on.
 """
 import csv
 import glob
@@ -77,7 +81,48 @@ def pmc_stats(path):
     return {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in acc.items()}
 
 
+def pmc_dispatches(path):
+    """[(dispatch id, kernel name, {counter: value})] in dispatch order, the
+    counter values summed over the dispatch's records."""
+    db = _find(path, "*_results.db")
+    per = {}
+    if db and db.endswith(".db"):
+        con = sqlite3.connect(db)
+        for did, name, cname, v in con.execute(
+                "select dispatch_id, name, counter_name, counter_value from pmc_events"):
+            e = per.setdefault(did, [name, defaultdict(float)])
+            e[1][cname] += v
+    else:
+        f = _find(path, "*counter_collection.csv")
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                did = int(r["Dispatch_Id"])
+                e = per.setdefault(did, [r["Kernel_Name"], defaultdict(float)])
+                e[1][r["Counter_Name"]] += float(r["Counter_Value"])
+    return [(d, per[d][0], dict(per[d][1])) for d in sorted(per)]
+
+
+def bench_line(log):
+    """The JSON line bench.py printed (the last line that parses)."""
+    import json
+    res = None
+    with open(log) as f:
+        for line in f:
+            line = line.strip()
+            if line.startswith("{"):
+                try:
+                    res = json.loads(line)
+                except ValueError:
+                    pass
+    if res is None:
+        raise ValueError("no bench.py JSON line in %s" % log)
+    return res
+
+
 def copy_probe(mib):
+    """Calibration kernels of known traffic on a tensor of `mib` MiB: a
+    device-to-device copy (reads and writes it once), a sum (reads it once,
+    writes one value) and a fill (writes it once), three times each."""
     import torch
     n = mib * (1 << 20) // 4
     src = torch.rand(n, device="cuda")
@@ -85,8 +130,12 @@ def copy_probe(mib):
     torch.cuda.synchronize()
     for _ in range(3):
         dst.copy_(src)
+    for _ in range(3):
+        src.sum()
+    for _ in range(3):
+        dst.fill_(1.0)
     torch.cuda.synchronize()
-    print("copied %d MiB x 3" % mib)
+    print("copied, summed and filled %d MiB x 3" % mib)
 
 
 def source_digest():
@@ -100,7 +149,35 @@ def source_digest():
     return h.hexdigest()[:16]
 
 
-def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, workload, out):
+def per_launch(path, bench, counter):
+    """Mean of one counter per launch of the scan, over the plain scans of a
+    bench.py run (warm-up and timed steps: every launch once per scan, in
+    order); [(kernel name, mean)] in launch order."""
+    return [(k, cs[counter]) for k, cs in per_launch_counters(path, bench)]
+
+
+def per_launch_counters(path, bench):
+    """[(kernel name, {counter: mean over the plain scans})] in launch order."""
+    launches = bench["launches"]
+    n = len(launches)
+    disp = [d for d in pmc_dispatches(path) if d[1].startswith("void fs::")]
+    scans = (bench["warmup"] + bench["steps"]) * n
+    if len(disp) < scans:
+        raise ValueError("%s: %d dispatches of the library, %d scans of %d launches expected"
+                         % (path, len(disp), bench["warmup"] + bench["steps"], n))
+    vals = [defaultdict(list) for _ in range(n)]
+    names = [None] * n
+    for i, (_, name, cs) in enumerate(disp[:scans]):
+        L = launches[i % n]
+        if L["name"].split("<")[0] not in name:
+            raise ValueError("dispatch %d is %s, launch %d of the scan is %s" % (i, name, i % n, L["name"]))
+        for c, v in cs.items():
+            vals[i % n][c].append(v)
+        names[i % n] = name
+    return [(names[i], {c: sum(v) / len(v) for c, v in vs.items()}) for i, vs in enumerate(vals)]
+
+
+def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, bench_log, out):
     import json
     copy_bytes = copy_mib * (1 << 20)
     cf = pmc_stats(cfetch_dir)
@@ -108,38 +185,54 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, workload, ou
     ck = [k for k in cf if "copyBuffer" in k or "copy" in k.lower()]
     fscale = copy_bytes / (cf[ck[0]]["FETCH_SIZE"] * 1024.0)
     wscale = copy_bytes / (cw[ck[0]]["WRITE_SIZE"] * 1024.0)
-    fe = pmc_stats(fetch_dir)
-    wr = pmc_stats(write_dir)
+    # second calibration points: a read-only reduction and a write-only fill
+    # of the same tensor (the copy's factors are the ones applied)
+    rk = [k for k in cf if "reduce" in k.lower()]
+    fk = [k for k in cw if "fill" in k.lower()]
+    fscale2 = copy_bytes / (cf[rk[0]]["FETCH_SIZE"] * 1024.0) if rk else None
+    wscale2 = copy_bytes / (cw[fk[0]]["WRITE_SIZE"] * 1024.0) if fk else None
+    print("calibration: copy FETCH x%.4f WRITE x%.4f; read-only sum FETCH x%s; write-only fill WRITE x%s"
+          % (fscale, wscale, "%.4f" % fscale2 if fscale2 else "-", "%.4f" % wscale2 if wscale2 else "-"))
+    bench = bench_line(bench_log)
+    workload = bench["config"]["workload"]
+    fe = per_launch(fetch_dir, bench, "FETCH_SIZE")
+    wr = per_launch(write_dir, bench, "WRITE_SIZE")
     entries = []
     if os.path.exists(out):
         with open(out) as f:
             entries = [e for e in json.load(f) if e.get("workload") != workload]
     dig = source_digest()
-    for k in fe:
-        if not k or not k.startswith("void fs::"):
-            continue
-        fb = fe[k]["FETCH_SIZE"] * 1024.0 * fscale
-        wb = wr.get(k, {}).get("WRITE_SIZE", 0.0) * 1024.0 * wscale
-        entries.append({"kernel": k, "workload": workload, "source_digest": dig,
-                        "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
-                        "bytes_per_launch": fb + wb, "fetch_scale": fscale, "write_scale": wscale})
-        print("%-80s fetch %10.3f MB  write %10.3f MB" % (k[:80], fb / 1e6, wb / 1e6))
+    for L, (k, f), (_, w) in zip(bench["launches"], fe, wr):
+        fb = f * 1024.0 * fscale
+        wb = w * 1024.0 * wscale
+        entries.append({"workload": workload, "launch": L["name"], "layer": L["layer"], "kernel": k,
+                        "source_digest": dig, "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+                        "bytes_per_launch": fb + wb, "algorithmic_bytes": L["bytes"],
+                        "fetch_scale": fscale, "write_scale": wscale,
+                        "fetch_scale_sum": fscale2, "write_scale_fill": wscale2})
+        print("L%-2d %-58s fetch %10.3f MB  write %10.3f MB  (algorithmic %10.3f MB)"
+              % (L["layer"], L["name"][:58], fb / 1e6, wb / 1e6, L["bytes"] / 1e6))
     with open(out, "w") as f:
         json.dump(entries, f, indent=1)
     print("scales: FETCH x%.4f  WRITE x%.4f  -> %s" % (fscale, wscale, out))
 
 
-def utilisation(path, simds=1024, xcds=8):
-    """Per kernel name, from one SQ counter pass (SQ_WAVES, SQ_INSTS_VALU,
-    SQ_INSTS_MFMA, SQ_INSTS_SALU, SQ_INSTS_LDS, SQ_INSTS_VMEM_RD,
-    SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE): the matrix cores' busy
-    fraction over the dispatch (busy cycles summed over all SIMDs, against
-    the GPU-active cycles of one XCD times the SIMD count) and the
-    instructions each wave issued."""
+def utilisation(path, simds=1024, xcds=8, bench_log=None):
+    """Per kernel name (or, given the bench.py log of the run, per launch of
+    the scan: 'L<layer> <launch>'), from one SQ counter pass (SQ_WAVES,
+    SQ_INSTS_VALU, SQ_INSTS_MFMA, SQ_INSTS_SALU, SQ_INSTS_LDS,
+    SQ_INSTS_VMEM_RD, SQ_VALU_MFMA_BUSY_CYCLES, GRBM_GUI_ACTIVE): the matrix
+    cores' busy fraction over the dispatch (busy cycles summed over all
+    SIMDs, against the GPU-active cycles of one XCD times the SIMD count) and
+    the instructions each wave issued."""
     rows = []
-    for k, cs in pmc_stats(path).items():
-        if not k or not k.startswith("void fs::"):
-            continue
+    if bench_log:
+        bench = bench_line(bench_log)
+        items = [("L%d %s" % (L["layer"], L["name"]), cs)
+                 for L, (_, cs) in zip(bench["launches"], per_launch_counters(path, bench))]
+    else:
+        items = [(k, cs) for k, cs in pmc_stats(path).items() if k and k.startswith("void fs::")]
+    for k, cs in items:
         waves = cs.get("SQ_WAVES", 0.0) or 1.0
         active = cs.get("GRBM_GUI_ACTIVE", 0.0) / xcds
         busy = cs.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
@@ -167,7 +260,7 @@ def main():
         copy_probe(int(args[1]))
         return
     if args and args[0] == "util":
-        utilisation(args[1])
+        utilisation(args[1], bench_log=args[2] if len(args) > 2 else None)
         return
     if "--pmc" in sys.argv:
         for k, cs in pmc_stats(args[0]).items():

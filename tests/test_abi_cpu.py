@@ -404,3 +404,115 @@ def test_bench_cpu_fragment_leg():
     part = oracle.frag_cpu.frag_scan(w.layers, params, img[:1, :25, :25], w.patch)
     assert part.shape == (1, 12, 12, w.n_classes)
     assert np.abs(part - whole[:1, :12, :12]).max() <= 1e-12
+
+
+def test_misaligned_pointers_named_in_error():
+    """The alignment contract of fs_scan (16-byte image and output, 256-byte
+    workspace), checked before anything else touches the pointers."""
+    lib = fsb.load()
+    net = _plan_net(wl.WORKLOADS[1].layers)
+    n = net.plan(1, 64, 64)["workspace_bytes"]
+    img, out, ws = ctypes.c_void_p(1 << 20), ctypes.c_void_p(2 << 20), ctypes.c_void_p(4 << 20)
+    for bad_img, bad_out in (((1 << 20) + 8, 2 << 20), (1 << 20, (2 << 20) + 4)):
+        st = lib.fs_scan(net._h, ctypes.c_void_p(bad_img), 1, 64, 64, ctypes.c_void_p(bad_out), ws, n, None)
+        assert st == fsb.FS_ERR_INVALID_ARG and b"16-byte" in lib.fs_last_error()
+    # 16 bytes is enough for the image and output; the workspace needs 256
+    st = lib.fs_scan(net._h, ctypes.c_void_p((1 << 20) + 16), 1, 64, 64, ctypes.c_void_p((2 << 20) + 48),
+                     ctypes.c_void_p((4 << 20) + 128), n, None)
+    assert st == fsb.FS_ERR_INVALID_ARG and b"256-byte" in lib.fs_last_error()
+    for fn, extra in ((lib.fs_scan_border, (1,)), ):
+        st = fn(net._h, ctypes.c_void_p((1 << 20) + 4), 1, 64, 64, *extra, out, ws, 1 << 30, None)
+        assert st == fsb.FS_ERR_INVALID_ARG and b"16-byte" in lib.fs_last_error()
+    st = lib.fs_scan_tiled(net._h, ctypes.c_void_p((1 << 20) + 4), 1, 64, 64, 8, 8, out, ws, 1 << 30, None)
+    assert st == fsb.FS_ERR_INVALID_ARG and b"16-byte" in lib.fs_last_error()
+    net.close()
+
+
+def test_image_side_limit():
+    """Fragment sizes travel in 16-bit tables: an image side above 65535 is
+    refused (not scanned wrongly), and the tiled scan takes such an image in
+    regions below the limit."""
+    net = _plan_net(wl.WORKLOADS[1].layers)
+    assert net.plan(1, 64, 65535)["out_w"] == 65535 - 14 + 1
+    for H, W in ((64, 65536), (65536, 64), (64, 70000)):
+        with pytest.raises(fsb.FsError) as e:
+            net.plan(1, H, W)
+        assert e.value.status == fsb.FS_ERR_UNSUPPORTED and "fs_scan_tiled" in str(e.value)
+    t = net.plan_tiled(1, 64, 70000, (64, 4096))
+    assert (t["out_h"], t["out_w"]) == (51, 70000 - 13)
+    with pytest.raises(fsb.FsError) as e:
+        net.plan_tiled(1, 64, 70000, (64, 65535))  # a region of 65548 columns
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+    with pytest.raises(fsb.FsError) as e:  # the mirrored border extends past the limit
+        net.plan(1, 64, 65530, "reflect")
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+    net.close()
+
+
+def test_batch_and_grid_limits():
+    """Batch times fragments stays below 2^24 (fragment indices), and a head
+    with too many windows is refused instead of overflowing."""
+    net = _plan_net(wl.WORKLOADS[2].layers)  # 256 final fragments
+    assert net.plan(1000, 95, 95)["out_h"] == 1
+    with pytest.raises(fsb.FsError) as e:
+        net.plan(65536, 95, 95)
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED and "fragments" in str(e.value)
+    with pytest.raises(fsb.FsError) as e:  # 65535 images: a pool's grid passes 2^24 workgroups
+        net.plan(65535, 95, 95)
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED and "grid" in str(e.value)
+    net.close()
+    # a lone 1 x 1 fully connected layer on a 65535 x 65535 image: 2^32 windows
+    net = _plan_net([wl.fc(1, 1, 2, "softmax")])
+    with pytest.raises(fsb.FsError) as e:
+        net.plan(1, 65535, 65535)
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+    net.close()
+
+
+def test_binding_tensor_checks():
+    """The binding refuses, before any pointer reaches the library, images
+    with the wrong channel count, dtype or layout and outputs or workspaces
+    that do not match (on the CPU here; the device checks use meta tensors)."""
+    torch = pytest.importorskip("torch")
+    img = torch.zeros((2, 20, 21, 3))
+    shape = (2, 7, 8, 4)
+    fsb.check_tensors(img, torch.zeros(shape), torch.zeros(64, dtype=torch.uint8), 3, shape, require_cuda=False)
+    bad = [
+        (img, None, None, 1),                                   # channels
+        (img.double(), None, None, 3),                          # dtype
+        (img.permute(0, 2, 1, 3), None, None, 3),               # layout
+        (img[0], None, None, 3),                                # rank
+        (img, torch.zeros((2, 7, 8, 3)), None, 3),              # output shape
+        (img, torch.zeros(shape, dtype=torch.float64), None, 3),
+        (img, torch.zeros((2, 8, 7, 4)).transpose(1, 2), None, 3),
+        (img, torch.zeros(shape, device="meta"), None, 3),      # output device
+        (img, None, torch.zeros((8, 8), dtype=torch.uint8).t(), 3),
+        (img, None, torch.zeros(64, dtype=torch.uint8, device="meta"), 3),
+    ]
+    for im, out, ws, c in bad:
+        with pytest.raises(ValueError):
+            fsb.check_tensors(im, out, ws, c, shape, require_cuda=False)
+    with pytest.raises(ValueError):
+        fsb.check_tensors(img, None, None, 3, shape)  # a CPU image for a scan
+
+
+def test_bench_oracle_window_sample():
+    """bench.py's per-patch sample: every image's four corners, the first
+    and last window of every final fragment of every image (found by the
+    oracle's corner tracking), and 4096 seeded random windows, each once."""
+    import sys
+    sys.path.insert(0, ROOT)
+    import bench
+    w = wl.WORKLOADS[4]
+    pts = bench.oracle_windows(w)
+    assert len(pts) == len(np.unique(pts, axis=0))
+    assert pts.min(0).tolist() == [0, 0, 0] and pts.max(0).tolist() == [7, 929, 929]
+    fr = ix.reassembly_index(w.layers, w.height, w.width)
+    for b in range(w.batch):
+        mine = pts[pts[:, 0] == b]
+        for Y in (0, 929):
+            for X in (0, 929):
+                assert ((mine[:, 1] == Y) & (mine[:, 2] == X)).any()
+        f = fr[mine[:, 1], mine[:, 2], 0]
+        assert set(f.tolist()) == set(range(256))  # every final fragment is hit
+    assert 2 * 256 * 8 <= len(pts) <= 2 * 256 * 8 + 32 + 4096

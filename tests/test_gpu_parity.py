@@ -155,19 +155,64 @@ def test_workload_net_small_image(fsb, wid, H, W, B):
 
 # ---- full-size workloads (the benchmarked configurations), sampled ----------
 
+def _fragment_windows(layers, B, H, W):
+    """(b, Y, X) of the first and the last window of every final fragment of
+    every image (the fragments' extreme pixels: where a wrong size, base or
+    stride would show first), from the oracle's own corner tracking."""
+    f = ix.reassembly_index(layers, H, W)[..., 0].ravel()
+    nx = W - ix.patch_hw(layers)[1] + 1
+    _, first = np.unique(f, return_index=True)
+    _, last_rev = np.unique(f[::-1], return_index=True)
+    last = f.size - 1 - last_rev
+    flat = np.concatenate([first, last])
+    rows = []
+    for b in range(B):
+        rows.append(np.stack([np.full(flat.size, b), flat // nx, flat % nx], 1))
+    return np.concatenate(rows)
+
+
+def _full_size_windows(layers, B, H, W, n_random, seed):
+    """Every image's corners, the first and last window of every final
+    fragment of every image, and n_random seeded random windows."""
+    h0, w0 = ix.patch_hw(layers)
+    ny, nx = H - h0 + 1, W - w0 + 1
+    rng = np.random.default_rng(seed)
+    corners = np.array([(b, Y, X) for b in range(B) for Y in (0, ny - 1) for X in (0, nx - 1)])
+    rand = np.stack([rng.integers(0, B, n_random), rng.integers(0, ny, n_random), rng.integers(0, nx, n_random)], 1)
+    pts = np.concatenate([corners, _fragment_windows(layers, B, H, W), rand])
+    return np.unique(pts, axis=0).astype(np.int32)
+
+
 @pytest.mark.parametrize("wid", [2, 3, 4, 5])
 def test_workload_full_size_sampled(fsb, wid):
+    """The benchmarked configurations at full size, in the launch
+    configuration the benchmark times: every final fragment's first and last
+    window in every image, the corners, and 4096 seeded random windows
+    against the per-patch oracle; the whole map finite and normalised."""
     w = wl.WORKLOADS[wid]
     params, img = wl.workload_inputs(wid)
-    print("full-size workload", wid, img.shape, flush=True)
+    pts = _full_size_windows(w.layers, w.batch, w.height, w.width, 4096, 50 + wid)
+    print("full-size workload", wid, img.shape, "windows checked:", len(pts), flush=True)
     got = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
     assert got.shape == (w.batch, w.out_h, w.out_w, w.n_classes)
     assert np.isfinite(got).all()
     assert np.abs(got.sum(-1) - 1.0).max() <= 1e-5
-    n_rand = {2: 40, 3: 200, 4: 40, 5: 80}[wid]
-    pts = _sample_patches(w.layers, w.batch, w.height, w.width, n_rand, 50 + wid)
+    F = ix.n_fragments(w.layers)
+    assert len(pts) >= 4096 + min(2 * F, w.out_h * w.out_w) * w.batch // 2
     ref = oracle.patch_forward(w.layers, params, img, w.patch, pts)
     assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref).max() <= TOL[w.dtype]
+
+
+def test_workload2_full_map_cpu_fragment(fsb):
+    """Net N4 on the full 512 x 512 image: every one of the 174,724 outputs
+    against the CPU fragment method (float64), itself pinned to the per-patch
+    definition."""
+    w = wl.WORKLOADS[2]
+    params, img = wl.workload_inputs(2)
+    got = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    assert got.shape == ref.shape == (1, 418, 418, 2)
+    assert np.abs(got - ref).max() <= TOL["f32"]
 
 
 def test_workload3_logits(fsb):
@@ -558,6 +603,53 @@ def test_tiled_scan(fsb, wid, B, H, W, tiles):
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), ref), tile
     net.close()
+
+
+def _seam_windows(B, ny, nx, th, tw, rng, per_line=6):
+    """Windows on both sides of every boundary between output tiles of
+    th x tw windows, and at every crossing of two boundaries."""
+    pts = set()
+    rows = [r for k in range(1, -(-ny // th)) for r in (k * th - 1, k * th)]
+    cols = [c for k in range(1, -(-nx // tw)) for c in (k * tw - 1, k * tw)]
+    for b in range(B):
+        for r in rows:
+            for c in rng.integers(0, nx, per_line):
+                pts.add((b, r, int(c)))
+            for c in cols:
+                pts.add((b, r, c))
+        for c in cols:
+            for r in rng.integers(0, ny, per_line):
+                pts.add((b, int(r), c))
+        for Y in (0, ny - 1):
+            for X in (0, nx - 1):
+                pts.add((b, Y, X))
+    return np.array(sorted(pts), np.int32)
+
+
+@pytest.mark.parametrize("wid,B,H,W,tile", [
+    (2, 1, 330, 301, (61, 47)),
+    (4, 2, 260, 231, (37, 64)),
+    (3, 1, 290, 270, (100, 81)),
+    (5, 1, 200, 190, (45, 29)),
+])
+def test_tiled_scan_seams_against_oracle(fsb, wid, B, H, W, tile):
+    """The tiled scan against the per-patch oracle on windows next to every
+    tile seam (each tile recomputes the image rows and columns it shares with
+    its neighbours), every seam crossing and the corners."""
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid, batch=B, height=H, width=W)
+    net = fsb.Net(w.layers, params, w.channels, 0, w.dtype)
+    x = torch.from_numpy(np.ascontiguousarray(img, np.float32)).cuda()
+    out = torch.full((B, H - w.patch + 1, W - w.patch + 1, w.n_classes), float("nan"), device="cuda")
+    net.scan_tiled(x, tile, out=out)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().astype(np.float64)
+    net.close()
+    assert np.isfinite(got).all()
+    pts = _seam_windows(B, H - w.patch + 1, W - w.patch + 1, tile[0], tile[1], np.random.default_rng(wid))
+    print("tiled seams", wid, tile, len(pts), flush=True)
+    ref = oracle.patch_forward(w.layers, params, img, w.patch, pts)
+    assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref).max() <= TOL[w.dtype]
 
 
 @pytest.mark.parametrize("wid,mode", [(1, "0"), (3, "0"), (2, "1"), (5, "1")])
