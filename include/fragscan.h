@@ -204,6 +204,25 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W,
 fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
                   float *d_out, void *d_workspace, size_t workspace_bytes, void *stream);
 
+/* Bytes of the per-GPU scratch array that stands in for the workspace of
+ * fs_scan_noalloc (128 MiB: net N4 on a 512 x 512 image needs 99 MB). */
+#define FS_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* fs_scan for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): no
+ * workspace argument, and the call allocates nothing.  The workspace is a
+ * static device array of FS_NOALLOC_SCRATCH_BYTES that every GPU using the
+ * library holds until the process ends (its address is looked up when a net
+ * is created on that GPU, or at the first call there).  Every call on one GPU
+ * shares that array: calls that overlap on one GPU (on two streams, or from
+ * two threads) race and give undefined outputs; the caller serialises them.
+ * The array keeps the last call's contents, which no scan depends on.
+ * FS_ERR_WORKSPACE when fs_scan_plan's workspace_bytes for this scan exceeds
+ * FS_NOALLOC_SCRATCH_BYTES (fs_scan then takes a workspace of the caller's);
+ * otherwise the arguments, limits and errors of fs_scan. */
+fs_status fs_scan_noalloc(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
+                          float *d_out, void *stream);
+
 /* Border handling (Section 3.2: the image's edges are mirrored so that the
  * net can be applied at every position).  FS_BORDER_VALID is the plain scan
  * above.  The mirrored modes extend the image by p0 = floor((w_0 - 1) / 2)

@@ -18,11 +18,19 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
 
 using namespace fs;
+
+// Workspace of fs_scan_noalloc, for callers that cannot allocate device
+// memory: one static array in every GPU's copy of this code object, held
+// until the process ends.  Host code never uses the name itself (on the host
+// it is a stand-in, not a device address): the address each device gives for
+// it, from hipGetSymbolAddress, is kept per device below.
+static __device__ __align__(256) unsigned char scratch[FS_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -42,6 +50,27 @@ fs_status fail(fs_status s, const char *fmt, ...)
 fs_status hip_fail(hipError_t e, const char *what)
 {
     return fail(FS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Device address of `scratch` on `device` (which must be current), looked up
+// once per device; nullptr with the error set when the lookup fails.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+fs_status scratch_on(int device, void **out)
+{
+    if (device < 0 || device >= kMaxDevices) return fail(FS_ERR_UNSUPPORTED, "device %d: no scratch slot", device);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[device]) {
+        void *p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (scratch)");
+        if (!p || ((uintptr_t)p & 255)) return fail(FS_ERR_HIP, "scratch at %p is not 256-byte aligned", p);
+        g_scratch_ptr[device] = p;
+    }
+    *out = g_scratch_ptr[device];
+    return FS_OK;
 }
 
 uint16_t host_f2bf(float f)
@@ -1322,6 +1351,12 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, net->device) == hipSuccess && n > 0)
             net->ncu = n;
     }
+    {
+        // set-up of the no-allocation entry point on this device: its scratch
+        // address (a failure here is reported by fs_scan_noalloc itself)
+        void *p = nullptr;
+        if (scratch_on(net->device, &p) != FS_OK) g_err.clear();
+    }
     net->mem_bytes = blob.size();
     e = hipMalloc(&net->d_mem, blob.size());
     if (e != hipSuccess) {
@@ -1534,6 +1569,33 @@ fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H,
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int i = 0; i < (int)P.launches.size(); ++i) {
         hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+        if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
+                                         hipGetErrorString(e));
+    }
+    return FS_OK;
+}
+
+fs_status fs_scan_noalloc(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, float *d_out,
+                          void *stream)
+{
+    if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
+    if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
+    if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
+        return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
+    Plan P;
+    fs_status st = make_plan(net, B, H, W, P);
+    if (st != FS_OK) return st;
+    if (P.ws_bytes > FS_NOALLOC_SCRATCH_BYTES)
+        return fail(FS_ERR_WORKSPACE, "the scan needs %zu bytes of workspace; fs_scan_noalloc has %zu (use fs_scan)",
+                    P.ws_bytes, (size_t)FS_NOALLOC_SCRATCH_BYTES);
+    st = check_device(net);
+    if (st != FS_OK) return st;
+    void *ws = nullptr;
+    st = scratch_on(net->device, &ws);
+    if (st != FS_OK) return st;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int i = 0; i < (int)P.launches.size(); ++i) {
+        hipError_t e = enqueue(net, P, d_image, d_out, ws, s, i);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
                                          hipGetErrorString(e));
     }

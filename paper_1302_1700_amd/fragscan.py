@@ -56,7 +56,7 @@ class fs_launch_info(ctypes.Structure):
 EXPORTS = ["fs_net_create", "fs_net_create_plan_only", "fs_net_destroy", "fs_net_query", "fs_scan_plan", "fs_scan_launches",
            "fs_scan", "fs_scan_profile", "fs_fragment_table", "fs_reassembly_index",
            "fs_status_str", "fs_last_error", "fs_scan_plan_border", "fs_scan_border",
-           "fs_scan_plan_tiled", "fs_scan_tiled"]
+           "fs_scan_plan_tiled", "fs_scan_tiled", "fs_scan_noalloc"]
 
 _lib = None
 
@@ -83,6 +83,7 @@ def load():
         "fs_scan_tiled": [VP, VP, I32, I32, I32, I32, I32, VP, VP, SZ, VP],
         "fs_scan_launches": [VP, I32, I32, I32, P(fs_launch_info), I32],
         "fs_scan": [VP, VP, I32, I32, I32, VP, VP, SZ, VP],
+        "fs_scan_noalloc": [VP, VP, I32, I32, I32, VP, VP],
         "fs_scan_profile": [VP, VP, I32, I32, I32, VP, VP, SZ, VP, I32, P(ctypes.c_float), I32],
         "fs_fragment_table": [VP, I32, I32, P(I32), SZ, P(SZ)],
         "fs_reassembly_index": [VP, I32, I32, P(I32), SZ, P(SZ)],
@@ -277,6 +278,21 @@ class Net:
             _check(load().fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
                                          ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
                                          _nbytes(ws), _stream_handle(stream)))
+        return out
+
+    def scan_noalloc(self, image, out, stream=None):
+        """As scan (valid windows) through fs_scan_noalloc: no workspace, no
+        device allocation in the call (the library's per-GPU scratch array;
+        calls overlapping on one GPU race).  `out` is required."""
+        if image.dim() != 4:
+            raise ValueError("image must be [B, H, W, C]")
+        B, H, W, C = image.shape
+        shape = (B, H - self.patch + 1, W - self.patch_x + 1, self.n_classes)
+        if out is None:
+            raise ValueError("scan_noalloc writes into a given output tensor")
+        check_tensors(image, out, None, self.info["in_channels"], shape)
+        _check(load().fs_scan_noalloc(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                      ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)))
         return out
 
     def scan_tiled(self, image, tile, out=None, workspace=None, stream=None):

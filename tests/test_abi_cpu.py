@@ -516,3 +516,25 @@ def test_bench_oracle_window_sample():
         f = fr[mine[:, 1], mine[:, 2], 0]
         assert set(f.tolist()) == set(range(256))  # every final fragment is hit
     assert 2 * 256 * 8 <= len(pts) <= 2 * 256 * 8 + 32 + 4096
+
+
+def test_noalloc_scan_limits_without_device():
+    """fs_scan_noalloc checks its arguments and the scratch size before any
+    device work: a scan whose workspace exceeds the per-GPU scratch array is
+    refused with FS_ERR_WORKSPACE (checked with a planning-only net and
+    addresses that are never touched)."""
+    lib = fsb.load()
+    net = _plan_net(wl.WORKLOADS[2].layers)
+    scratch = 128 << 20
+    assert net.plan(1, 512, 512)["workspace_bytes"] <= scratch < net.plan(1, 1024, 1024)["workspace_bytes"]
+    img, out = ctypes.c_void_p(1 << 20), ctypes.c_void_p(2 << 20)
+    st = lib.fs_scan_noalloc(net._h, img, 1, 1024, 1024, out, None)
+    assert st == fsb.FS_ERR_WORKSPACE and b"fs_scan_noalloc" in lib.fs_last_error()
+    st = lib.fs_scan_noalloc(net._h, ctypes.c_void_p((1 << 20) + 4), 1, 512, 512, out, None)
+    assert st == fsb.FS_ERR_INVALID_ARG
+    st = lib.fs_scan_noalloc(net._h, img, 1, 90, 512, out, None)
+    assert st == fsb.FS_ERR_SHAPE
+    # within the limit, a planning-only net still never launches
+    st = lib.fs_scan_noalloc(net._h, img, 1, 512, 512, out, None)
+    assert st == fsb.FS_ERR_INVALID_ARG and b"planning only" in lib.fs_last_error()
+    net.close()
