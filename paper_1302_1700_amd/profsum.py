@@ -187,8 +187,10 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_mib, bench_log, o
     wscale = copy_bytes / (cw[ck[0]]["WRITE_SIZE"] * 1024.0)
     # second calibration points: a read-only reduction and a write-only fill
     # of the same tensor (the copy's factors are the ones applied)
-    rk = [k for k in cf if "reduce" in k.lower()]
-    fk = [k for k in cw if "fill" in k.lower()]
+    # (the kernels of those names that moved the most: torch also launches
+    # small fills and reductions of its own)
+    rk = sorted((k for k in cf if "reduce" in k.lower()), key=lambda k: -cf[k]["FETCH_SIZE"])
+    fk = sorted((k for k in cw if "fill" in k.lower()), key=lambda k: -cw[k]["WRITE_SIZE"])
     fscale2 = copy_bytes / (cf[rk[0]]["FETCH_SIZE"] * 1024.0) if rk else None
     wscale2 = copy_bytes / (cw[fk[0]]["WRITE_SIZE"] * 1024.0) if fk else None
     print("calibration: copy FETCH x%.4f WRITE x%.4f; read-only sum FETCH x%s; write-only fill WRITE x%s"
