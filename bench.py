@@ -209,8 +209,10 @@ def main():
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record(stream)
+    h0 = time.perf_counter()
     for _ in range(args.steps):
         step()
+    host_ms = (time.perf_counter() - h0) * 1e3 / args.steps  # enqueue time per scan on the host
     t1.record(stream)
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / args.steps
@@ -270,6 +272,7 @@ def main():
                    "patch": w.patch, "outputs": [w.batch, oh, ow], "fragments": net.info["n_fragments"],
                    "border": border, "tile": list(tile) if tile else None,
                    "workspace_bytes": ws.numel()},
+        "host_enqueue_ms_per_step": host_ms,
         "tflops": plan["flops"] / (ms * 1e-3) / 1e12,
         "pct_mfma_peak": 100.0 * plan["flops"] / (ms * 1e-3) / 1e12 / peak_mm,
         "conv_tflops_in_conv_kernels": conv_flops / (conv_ms * 1e-3) / 1e12 if conv_ms else 0.0,

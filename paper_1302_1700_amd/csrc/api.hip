@@ -18,6 +18,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
 #include <mutex>
 #include <new>
 #include <string>
@@ -100,6 +101,8 @@ struct NetLayer {
 
 }  // namespace
 
+struct PlanCache;  // scan plans of a net, by size (defined with the planner)
+
 struct fs_net {
     std::vector<NetLayer> L;
     int patch = 0, C = 0, dtype = 0, ncls = 0;  // patch: window rows h_0
@@ -116,6 +119,8 @@ struct fs_net {
     int head_cin = 0;
     void *d_mem = nullptr;
     size_t mem_bytes = 0;
+    PlanCache *plans = nullptr;  // owned; shared by the scans of all threads (locked inside)
+    ~fs_net();
 };
 
 namespace {
@@ -930,6 +935,78 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
     return FS_OK;
 }
 
+}  // namespace
+
+// Plans already made for a net, by batch, image size, view and the planner
+// switches in the environment, so a scan repeated at the same size enqueues
+// its launches without planning again.  Plans are immutable once made and
+// shared through shared_ptr, so a plan stays valid for a scan that holds it
+// while another thread adds plans.
+struct PlanCache {
+    struct Key {
+        int B, H, W, img_h, img_w, out_h, out_w;
+        std::string env;
+        bool operator==(const Key &o) const
+        {
+            return B == o.B && H == o.H && W == o.W && img_h == o.img_h && img_w == o.img_w && out_h == o.out_h &&
+                   out_w == o.out_w && env == o.env;
+        }
+    };
+    static constexpr size_t kMax = 16;  // most recently used last
+    std::mutex mu;
+    std::vector<std::pair<Key, std::shared_ptr<const Plan>>> plans;
+};
+
+fs_net::~fs_net() { delete plans; }
+
+namespace {
+
+// The planner switches (tuning and test overrides) a plan was made under.
+std::string planner_env()
+{
+    static const char *const vars[] = {"FRAGSCAN_TILE", "FRAGSCAN_DIRECT", "FRAGSCAN_POOL_FUSE",
+                                       "FRAGSCAN_NO_FUSED_HEAD", "FRAGSCAN_RUN", "FRAGSCAN_ROWTILES",
+                                       "FRAGSCAN_STORE", "FRAGSCAN_LDS_PAD", "FRAGSCAN_WIDE"};
+    std::string sig;
+    for (const char *v : vars) {
+        const char *e = getenv(v);
+        sig += e ? e : "\x01";
+        sig += '\x02';
+    }
+    return sig;
+}
+
+fs_status get_plan(const fs_net *net, int B, int H, int W, std::shared_ptr<const Plan> &out,
+                   const View *view = nullptr)
+{
+    PlanCache::Key k{B, H, W, view ? view->img_h : 0, view ? view->img_w : 0, view ? view->out_h : 0,
+                     view ? view->out_w : 0, planner_env()};
+    PlanCache *c = net->plans;
+    if (c) {
+        std::lock_guard<std::mutex> lock(c->mu);
+        for (size_t i = 0; i < c->plans.size(); ++i)
+            if (c->plans[i].first == k) {
+                out = c->plans[i].second;
+                if (i + 1 != c->plans.size()) {  // move to the back (most recent)
+                    auto e = c->plans[i];
+                    c->plans.erase(c->plans.begin() + i);
+                    c->plans.push_back(e);
+                }
+                return FS_OK;
+            }
+    }
+    auto P = std::make_shared<Plan>();
+    fs_status st = make_plan(net, B, H, W, *P, view);
+    if (st != FS_OK) return st;
+    out = P;
+    if (c) {
+        std::lock_guard<std::mutex> lock(c->mu);
+        if (c->plans.size() >= PlanCache::kMax) c->plans.erase(c->plans.begin());
+        c->plans.emplace_back(k, P);
+    }
+    return FS_OK;
+}
+
 fs_status check_device(const fs_net *net)
 {
     if (net->device < 0) return fail(FS_ERR_INVALID_ARG, "net was created for planning only");
@@ -944,8 +1021,8 @@ fs_status check_device(const fs_net *net)
 // Plan of a scan with a border mode: the mirrored modes scan the extended
 // image (H + w_0 - 1) x (W + w_0 - 1), built in the workspace after the
 // scan's own buffers (from byte pad_off).
-fs_status border_plan(const fs_net *net, int B, int H, int W, int border, Plan &P, int &He, int &We,
-                      size_t &pad_off, size_t &ws_total)
+fs_status border_plan(const fs_net *net, int B, int H, int W, int border, std::shared_ptr<const Plan> &PP,
+                      int &He, int &We, size_t &pad_off, size_t &ws_total)
 {
     if (border != BORDER_VALID && border != BORDER_REFLECT && border != BORDER_SYMMETRIC)
         return fail(FS_ERR_INVALID_ARG, "unknown border mode %d", border);
@@ -956,8 +1033,9 @@ fs_status border_plan(const fs_net *net, int B, int H, int W, int border, Plan &
         He = H + net->patch - 1;
         We = W + net->patch_x - 1;
     }
-    fs_status st = make_plan(net, B, He, We, P);
+    fs_status st = get_plan(net, B, He, We, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     pad_off = P.ws_bytes;
     ws_total = P.ws_bytes;
     if (border != BORDER_VALID) {
@@ -968,14 +1046,15 @@ fs_status border_plan(const fs_net *net, int B, int H, int W, int border, Plan &
 }
 
 fs_status validate_scan(const fs_net *net, const float *d_image, int B, int H, int W, float *d_out,
-                        void *d_ws, size_t ws_bytes, Plan &P)
+                        void *d_ws, size_t ws_bytes, std::shared_ptr<const Plan> &PP)
 {
     if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
     if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
     if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
         return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
-    fs_status st = make_plan(net, B, H, W, P);
+    fs_status st = get_plan(net, B, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     if (ws_bytes < P.ws_bytes)
         return fail(FS_ERR_WORKSPACE, "workspace of %zu bytes, the scan needs %zu", ws_bytes, P.ws_bytes);
     if (P.ws_bytes && !d_ws) return fail(FS_ERR_INVALID_ARG, "workspace pointer is NULL");
@@ -989,7 +1068,7 @@ fs_status validate_scan(const fs_net *net, const float *d_image, int B, int H, i
 // Tiles of one shape share a plan (at most four shapes: full and last).
 struct Tiled {
     int ny = 0, nx = 0, th = 0, tw = 0, rows = 0, cols = 0;
-    Plan shape[2][2];  // [last row of tiles][last column of tiles]
+    std::shared_ptr<const Plan> shape[2][2];  // [last row of tiles][last column of tiles]
     size_t ws_bytes = 0;
     int n_launches = 0;
     double flops = 0, bytes = 0;
@@ -1017,13 +1096,13 @@ fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Til
             v.img_w = W;
             v.out_h = T.ny;
             v.out_w = T.nx;
-            fs_status st = make_plan(net, B, h + net->patch - 1, w + net->patch_x - 1, T.shape[lr][lc], &v);
+            fs_status st = get_plan(net, B, h + net->patch - 1, w + net->patch_x - 1, T.shape[lr][lc], &v);
             if (st != FS_OK) return st;
-            T.ws_bytes = std::max(T.ws_bytes, T.shape[lr][lc].ws_bytes);
+            T.ws_bytes = std::max(T.ws_bytes, T.shape[lr][lc]->ws_bytes);
         }
     for (int r = 0; r < T.rows; ++r)
         for (int c = 0; c < T.cols; ++c) {
-            const Plan &P = T.shape[r == T.rows - 1][c == T.cols - 1];
+            const Plan &P = *T.shape[r == T.rows - 1][c == T.cols - 1];
             T.n_launches += (int)P.launches.size();
             T.flops += P.flops;
             T.bytes += P.bytes;
@@ -1031,13 +1110,16 @@ fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Til
     return FS_OK;
 }
 
-hipError_t enqueue(const fs_net *net, Plan &P, const float *d_image, float *d_out, void *d_ws,
-                   hipStream_t s, int i)
+// Launch i of plan P.  The plan is shared (cached) and left untouched: the
+// launch's arguments are copied and given their buffers here.  img_off /
+// out_off (floats) place a tiled scan's region in the image and the map.
+hipError_t enqueue(const fs_net *net, const Plan &P, const float *d_image, float *d_out, void *d_ws,
+                   hipStream_t s, int i, size_t img_off = 0, size_t out_off = 0)
 {
-    Launch &L = P.launches[i];
+    Launch L = P.launches[i];
     char *ws = static_cast<char *>(d_ws);
-    d_image += P.view.img_off;
-    d_out += P.view.out_off;
+    d_image += img_off;
+    d_out += out_off;
     auto ptr = [&](int which) -> void * {
         if (which == -1) return const_cast<float *>(d_image);
         if (which == 2) return d_out;
@@ -1336,6 +1418,7 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         net->head_b_off = push(z.data(), z.size() * 4);
     }
     net->L = L;
+    net->plans = new (std::nothrow) PlanCache();  // (without one, every scan plans afresh)
     if (!upload) {  // planning-only handle: no device memory
         net->device = -1;
         *out = net;
@@ -1444,12 +1527,11 @@ fs_status fs_scan_tiled(const fs_net *net, const float *d_image, int32_t B, int3
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int r = 0; r < T.rows; ++r)
         for (int c = 0; c < T.cols; ++c) {
-            Plan &P = T.shape[r == T.rows - 1][c == T.cols - 1];
+            const Plan &P = *T.shape[r == T.rows - 1][c == T.cols - 1];
             const size_t y0 = (size_t)r * T.th, x0 = (size_t)c * T.tw;
-            P.view.img_off = (y0 * W + x0) * net->C;
-            P.view.out_off = (y0 * T.nx + x0) * net->ncls;
+            const size_t img_off = (y0 * W + x0) * net->C, out_off = (y0 * T.nx + x0) * net->ncls;
             for (int i = 0; i < (int)P.launches.size(); ++i) {
-                hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+                hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i, img_off, out_off);
                 if (e != hipSuccess)
                     return fail(FS_ERR_HIP, "tile (%d, %d) launch %d (%s): %s", r, c, i, P.launches[i].name.c_str(),
                                 hipGetErrorString(e));
@@ -1461,9 +1543,10 @@ fs_status fs_scan_tiled(const fs_net *net, const float *d_image, int32_t B, int3
 fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_plan_info *out)
 {
     if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
-    Plan P;
-    fs_status st = make_plan(net, B, H, W, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = get_plan(net, B, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     out->batch = B;
     out->out_h = P.ny;
     out->out_w = P.nx;
@@ -1478,11 +1561,12 @@ fs_status fs_scan_plan_border(const fs_net *net, int32_t B, int32_t H, int32_t W
                               fs_plan_info *out)
 {
     if (!net || !out) return fail(FS_ERR_INVALID_ARG, "NULL argument");
-    Plan P;
+    std::shared_ptr<const Plan> PP;
     int He, We;
     size_t pad_off, ws_total;
-    fs_status st = border_plan(net, B, H, W, border, P, He, We, pad_off, ws_total);
+    fs_status st = border_plan(net, B, H, W, border, PP, He, We, pad_off, ws_total);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     out->batch = B;
     out->out_h = P.ny;
     out->out_w = P.nx;
@@ -1500,11 +1584,12 @@ fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int
     if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
     if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
         return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
-    Plan P;
+    std::shared_ptr<const Plan> PP;
     int He, We;
     size_t pad_off, ws_total;
-    fs_status st = border_plan(net, B, H, W, border, P, He, We, pad_off, ws_total);
+    fs_status st = border_plan(net, B, H, W, border, PP, He, We, pad_off, ws_total);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     if (workspace_bytes < ws_total)
         return fail(FS_ERR_WORKSPACE, "workspace of %zu bytes, the scan needs %zu", workspace_bytes, ws_total);
     if (ws_total && !d_workspace) return fail(FS_ERR_INVALID_ARG, "workspace pointer is NULL");
@@ -1532,9 +1617,10 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, f
                            int32_t capacity)
 {
     if (!net || (!h_out && capacity > 0) || capacity < 0) return fail(FS_ERR_INVALID_ARG, "bad argument");
-    Plan P;
-    fs_status st = make_plan(net, B, H, W, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = get_plan(net, B, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     const int n = std::min<int>(capacity, (int)P.launches.size());
     for (int i = 0; i < n; ++i) {
         const Launch &L = P.launches[i];
@@ -1563,9 +1649,10 @@ fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, f
 fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, float *d_out,
                   void *d_workspace, size_t workspace_bytes, void *stream)
 {
-    Plan P;
-    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int i = 0; i < (int)P.launches.size(); ++i) {
         hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
@@ -1582,9 +1669,10 @@ fs_status fs_scan_noalloc(const fs_net *net, const float *d_image, int32_t B, in
     if (!d_image || !d_out) return fail(FS_ERR_INVALID_ARG, "image or output pointer is NULL");
     if (((uintptr_t)d_image & 15) || ((uintptr_t)d_out & 15))
         return fail(FS_ERR_INVALID_ARG, "image and output must be 16-byte aligned");
-    Plan P;
-    fs_status st = make_plan(net, B, H, W, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = get_plan(net, B, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     if (P.ws_bytes > FS_NOALLOC_SCRATCH_BYTES)
         return fail(FS_ERR_WORKSPACE, "the scan needs %zu bytes of workspace; fs_scan_noalloc has %zu (use fs_scan)",
                     P.ws_bytes, (size_t)FS_NOALLOC_SCRATCH_BYTES);
@@ -1608,9 +1696,10 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
 {
     if (reps < 1 || capacity < 0 || (!h_launch_ms && capacity > 0))
         return fail(FS_ERR_INVALID_ARG, "bad reps / output");
-    Plan P;
-    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = validate_scan(net, d_image, B, H, W, d_out, d_workspace, workspace_bytes, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     hipStream_t s = static_cast<hipStream_t>(stream);
     const int n = (int)P.launches.size();
     // Launch i runs `reps` times back to back between two events.  Every
@@ -1646,9 +1735,10 @@ fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_
                             size_t *n_needed)
 {
     if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
-    Plan P;
-    fs_status st = make_plan(net, 1, H, W, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = get_plan(net, 1, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     const int np = (int)net->pool_k.size();
     const size_t rec = 5 + 2 * (size_t)np;
     const size_t need = rec * net->F;
@@ -1711,9 +1801,10 @@ fs_status fs_reassembly_index(const fs_net *net, int32_t H, int32_t W, int32_t *
                               size_t *n_needed)
 {
     if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
-    Plan P;
-    fs_status st = make_plan(net, 1, H, W, P);
+    std::shared_ptr<const Plan> PP;
+    fs_status st = get_plan(net, 1, H, W, PP);
     if (st != FS_OK) return st;
+    const Plan &P = *PP;
     const size_t need = (size_t)3 * P.ny * P.nx;
     if (n_needed) *n_needed = need;
     if (!h_out) return FS_OK;

@@ -92,6 +92,8 @@ struct ConvArgs {
     int ny, nx, Sy, Sx;       // Sy, Sx: products of the pools' row / column sizes
     uint16_t base_y[kMaxAxis], base_x[kMaxAxis];  // per-axis fragment index -> its first output coordinate
 };
+// Passed by value: the launch arguments of one dispatch (4 KiB at most).
+static_assert(sizeof(ConvArgs) <= 4096, "ConvArgs must stay within the kernel-argument limit");
 
 struct PoolArgs {
     const void *in;      // parents  [B*F][in_h][in_w][C]

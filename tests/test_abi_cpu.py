@@ -538,3 +538,41 @@ def test_noalloc_scan_limits_without_device():
     st = lib.fs_scan_noalloc(net._h, img, 1, 512, 512, out, None)
     assert st == fsb.FS_ERR_INVALID_ARG and b"planning only" in lib.fs_last_error()
     net.close()
+
+
+def test_plan_cache(monkeypatch):
+    """Plans are cached per net and size: a repeated plan is the same, a
+    planner switch set in between gives the plan made under it, and planning
+    from several threads at once (more sizes than the cache holds) gives
+    every thread the single-threaded answers."""
+    import threading
+    monkeypatch.delenv("FRAGSCAN_POOL_FUSE", raising=False)
+    w = wl.WORKLOADS[2]
+    net = _plan_net(w.layers)
+    a = net.launches(1, 300, 280)
+    assert net.launches(1, 300, 280) == a
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "0")
+    b = net.launches(1, 300, 280)
+    assert [L["name"] for L in b] != [L["name"] for L in a] and len(b) == len(a) + 1
+    monkeypatch.delenv("FRAGSCAN_POOL_FUSE")
+    assert net.launches(1, 300, 280) == a
+    sizes = [(1 + i % 3, 95 + 7 * i, 120 + 5 * i) for i in range(24)]
+    want = {s: net.plan(*s) for s in sizes}
+    errors = []
+
+    def worker(k):
+        try:
+            for rep in range(20):
+                for s in sizes[k % 5:] + sizes[:k % 5]:
+                    if net.plan(*s) != want[s]:
+                        errors.append(s)
+        except Exception as e:  # noqa: BLE001
+            errors.append(e)
+
+    th = [threading.Thread(target=worker, args=(k,)) for k in range(6)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    assert not errors, errors[:3]
+    net.close()
