@@ -23,7 +23,10 @@ between its neighbouring pixels: the input fragment starts at (0, 0) with step
 1; the child at offset o of a fragment with base b and step t gets base
 b + o*t and step t*k, since its window xbar starts at parent pixel o + k*xbar
 (per axis: with a k_y x k_x pool, Section 2's rectangular case, the steps of
-the two axes differ).
+the two axes differ).  A pool whose stride s differs from its size k (not in
+the paper, whose pools do not overlap) has s^2 children per fragment, one per
+offset o in {0..s-1}^2, child pixel xbar covering parent pixels
+o + s*xbar .. o + s*xbar + k - 1: base b + o*t and step t*s.
 A fragment pixel (y, x) at the end is the patch whose top-left corner is
 (base_y + step*y, base_x + step*x): a crop of a fragment's maps is one patch's
 maps (Section 3).
@@ -47,18 +50,21 @@ def _conv(a, w, b, act):
     return out
 
 
-def _pool_children(a, ky, kx):
-    """The ky*kx children of fragment a [h, w, c] in offset order (o_y, o_x)."""
+def _pool_children(a, ky, kx, sy, sx):
+    """The sy*sx children of fragment a [h, w, c] under a ky x kx pool with
+    stride (sy, sx), in offset order (o_y, o_x): child pixel (ybar, xbar) is
+    the maximum over rows o_y + sy*ybar .. + ky - 1 and columns
+    o_x + sx*xbar .. + kx - 1, for every window that ends inside a."""
     h, wd, c = a.shape
     kids = []
-    for oy in range(ky):
-        for ox in range(kx):
-            hc, wc = max((h - oy) // ky, 0), max((wd - ox) // kx, 0)
+    for oy in range(sy):
+        for ox in range(sx):
+            hc, wc = max(h - oy - ky + sy, 0) // sy, max(wd - ox - kx + sx, 0) // sx
             m = np.full((hc, wc, c), -np.inf)
             for i in range(ky):
                 for j in range(kx):
                     y0, x0 = oy + i, ox + j
-                    m = np.maximum(m, a[y0:y0 + ky * hc:ky, x0:x0 + kx * wc:kx, :][:hc, :wc])
+                    m = np.maximum(m, a[y0:y0 + sy * hc:sy, x0:x0 + sx * wc:sx, :][:hc, :wc])
             kids.append(((oy, ox), m))
     return kids
 
@@ -78,10 +84,11 @@ def frag_scan(layers, params, image, patch):
         for L, p in zip(layers, params):
             if L["kind"] == "pool":
                 ky, kx = L["k"], L.get("kx", L["k"])
+                sy, sx = L.get("stride", ky), L.get("stride_x", kx)
                 nxt = []
                 for (by, bx, ty, tx, a) in frags:
-                    for (oy, ox), m in _pool_children(a, ky, kx):
-                        nxt.append((by + oy * ty, bx + ox * tx, ty * ky, tx * kx, m))
+                    for (oy, ox), m in _pool_children(a, ky, kx, sy, sx):
+                        nxt.append((by + oy * ty, bx + ox * tx, ty * sy, tx * sx, m))
                 frags = nxt
             else:
                 w = np.asarray(p[0], np.float64)

@@ -23,6 +23,16 @@ rectangular ones follow directly: a layer's "k" is its rows (the y axis) and
 its optional "kx" its columns; every rule above then holds per axis (a
 k_y x k_x pool has k_y * k_x children, numbered parent*k_y*k_x + o_y*k_x +
 o_x).
+
+Pools whose stride s differs from their size k (optional "stride",
+"stride_x"; the paper's pools are non-overlapping, s = k) generalise the same
+way: at patch level a side w gives (w - k) / s + 1 (requiring (w - k) mod s
+= 0); in the fragment method a fragment has s^2 children, one per offset o in
+{0..s-1}^2, child pixel xbar taking the maximum over o + s*xbar ..
+o + s*xbar + k - 1 (Eq. 5 with the window start stepping by s), so the child
+holds div(s_f - o - k + s, s) pixels per axis (Eqs. 6-7: the windows starting
+at o, o + s, ... that end inside the fragment), and tracking a corner x
+through the pool selects offset x mod s at position x div s.
   fragment_table    per final fragment: offsets, base output pixel, size,
                     all found by tracking every output pixel
   reassembly_index  per output pixel: (f, y_f, x_f), by tracking
@@ -39,6 +49,12 @@ def kyx(L):
     return L["k"], L.get("kx", L["k"])
 
 
+def syx(L):
+    """(rows, columns) stride of a pool (its size unless given)."""
+    ky, kx = kyx(L)
+    return L.get("stride", ky), L.get("stride_x", kx)
+
+
 def patch_sizes(layers, w0, axis=0):
     """[w_0, w_1, ..., w_n] along one axis (0: rows, 1: columns) for a patch
     of that size; raises on a pool that does not divide its map or a kernel
@@ -48,9 +64,10 @@ def patch_sizes(layers, w0, axis=0):
     for L in layers:
         k = kyx(L)[axis]
         if L["kind"] == "pool":
-            if w % k:
-                raise ValueError("pool %d does not divide map %d" % (k, w))
-            w //= k
+            st = syx(L)[axis]
+            if w < k or (w - k) % st:
+                raise ValueError("pool %d (stride %d) does not tile map %d" % (k, st, w))
+            w = (w - k) // st + 1
         else:
             if k > w:
                 raise ValueError("kernel %d larger than map %d" % (k, w))
@@ -65,7 +82,7 @@ def patch_size(layers, axis=0):
     w = 1
     for L in reversed(layers):
         k = kyx(L)[axis]
-        w = w * k if L["kind"] == "pool" else w + k - 1
+        w = (w - 1) * syx(L)[axis] + k if L["kind"] == "pool" else w + k - 1
     return w
 
 
@@ -84,10 +101,10 @@ def track(layers, Y, X):
     for L in layers:
         if L["kind"] != "pool":
             continue  # a valid convolution keeps the corner where it is
-        ky, kx = kyx(L)
-        ox, oy = x % kx, y % ky
-        x, y = x // kx, y // ky
-        f = f * ky * kx + oy * kx + ox
+        sy, sx = syx(L)
+        ox, oy = x % sx, y % sy
+        x, y = x // sx, y // sy
+        f = f * sy * sx + oy * sx + ox
         offs.append((ox, oy))
     return f, y, x, offs
 
@@ -100,11 +117,12 @@ def fragment_extents(layers, H, W):
     for L in layers:
         ky, kx = kyx(L)
         if L["kind"] == "pool":
+            ty, tx = syx(L)
             nxt = []
             for (sy, sx) in frags:
-                for oy in range(ky):
-                    for ox in range(kx):
-                        nxt.append((max((sy - oy) // ky, 0), max((sx - ox) // kx, 0)))
+                for oy in range(ty):
+                    for ox in range(tx):
+                        nxt.append((max(sy - oy - ky + ty, 0) // ty, max(sx - ox - kx + tx, 0) // tx))
             frags = nxt
         else:
             frags = [(max(sy - (ky - 1), 0), max(sx - (kx - 1), 0)) for (sy, sx) in frags]
@@ -116,7 +134,7 @@ def n_fragments(layers):
     F = 1
     for L in layers:
         if L["kind"] == "pool":
-            F *= kyx(L)[0] * kyx(L)[1]
+            F *= syx(L)[0] * syx(L)[1]
     return F
 
 

@@ -22,7 +22,8 @@ class _OLayer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int), ("k", ctypes.c_int), ("kx", ctypes.c_int), ("c_in", ctypes.c_int),
                 ("c_out", ctypes.c_int), ("act", ctypes.c_int),
                 ("w", ctypes.POINTER(ctypes.c_double)),
-                ("b", ctypes.POINTER(ctypes.c_double))]
+                ("b", ctypes.POINTER(ctypes.c_double)),
+                ("s", ctypes.c_int), ("sx", ctypes.c_int)]
 
 
 def _open(path):
@@ -56,7 +57,8 @@ def patch_forward(layers, params, image, patch, patches=None, lib_path=None):
     """Outputs of the net on the requested patches, in float64.
 
     layers  : layer dicts (kind, k, c_in, c_out, act; optional kx, the
-              kernel's / pool's columns when they differ from its rows k)
+              kernel's / pool's columns when they differ from its rows k;
+              pools: optional stride, stride_x when they differ from k, kx)
     params  : per layer (weight OIHW, bias) or None for pools
     image   : [B][H][W][C] array (any float type; promoted to float64)
     patch   : w_0, or (h_0, w_0) for a rectangular window
@@ -72,6 +74,7 @@ def patch_forward(layers, params, image, patch, patches=None, lib_path=None):
     for i, (L, p) in enumerate(zip(layers, params)):
         arr[i].kind, arr[i].k, arr[i].kx = KIND[L["kind"]], L["k"], L.get("kx", 0)
         arr[i].c_in, arr[i].c_out, arr[i].act = L["c_in"], L["c_out"], ACT[L["act"]]
+        arr[i].s, arr[i].sx = L.get("stride", 0), L.get("stride_x", 0)
         if p is not None:
             w = np.ascontiguousarray(p[0], dtype=np.float64)
             b = np.ascontiguousarray(p[1], dtype=np.float64)

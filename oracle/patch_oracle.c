@@ -14,7 +14,11 @@
  *     input maps with k_y x k_x kernels, plus bias, then the activation; each
  *     map side shrinks by its kernel side minus one;
  *   - max-pooling layer (Section 2.1.2): non-overlapping k_y x k_x maxima;
- *     each map side must be divisible by the pool side and is divided by it;
+ *     each map side must be divisible by the pool side and is divided by it.
+ *     Pools with a stride s other than their size k (a generalisation the
+ *     paper does not treat) take the maxima of the k x k windows at rows
+ *     s*y and columns s_x*x: a side w gives (w - k) / s + 1 and must leave
+ *     no remainder, (w - k) mod s = 0, which for s = k is the rule above;
  *   - fully connected layers (Section 2, "input, convolutional, max-pooling
  *     and fully-connected"): a dot product of the whole flattened map
  *     ([c][y][x] order) with each output neuron's weights, which is the
@@ -36,9 +40,12 @@ typedef struct {
     int kind, k, kx, c_in, c_out, act; /* k: rows of the kernel / pool; kx: columns (0: k) */
     const double *w; /* [c_out][c_in][k][kx] */
     const double *b; /* [c_out] */
+    int s, sx;       /* pools: row and column stride (0: the pool's rows k, columns kx) */
 } olayer;
 
 static int kcols(const olayer *L) { return L->kx ? L->kx : L->k; }
+static int srows(const olayer *L) { return L->s ? L->s : L->k; }
+static int scols(const olayer *L) { return L->sx ? L->sx : kcols(L); }
 
 /* One layer on one patch.  `a` holds c_in maps of h x w as [c][y][x]; the
  * result goes to `o` and its size to *h_out x *w_out.  Returns 0 or -1 on a
@@ -47,15 +54,16 @@ static int run_layer(const olayer *L, const double *a, int h, int w, double *o, 
 {
     const int ky = L->k, kx = kcols(L);
     if (L->kind == O_POOL) {
-        if (ky < 1 || kx < 1 || h % ky != 0 || w % kx != 0) return -1;
-        int ho = h / ky, wo = w / kx;
+        const int sy = srows(L), sx = scols(L);
+        if (ky < 1 || kx < 1 || sy < 1 || sx < 1 || h < ky || w < kx || (h - ky) % sy || (w - kx) % sx) return -1;
+        int ho = (h - ky) / sy + 1, wo = (w - kx) / sx + 1;
         for (int c = 0; c < L->c_in; ++c)
             for (int y = 0; y < ho; ++y)
                 for (int x = 0; x < wo; ++x) {
-                    double m = a[((size_t)c * h + ky * y) * w + kx * x];
+                    double m = a[((size_t)c * h + sy * y) * w + sx * x];
                     for (int i = 0; i < ky; ++i)
                         for (int j = 0; j < kx; ++j) {
-                            double v = a[((size_t)c * h + ky * y + i) * w + kx * x + j];
+                            double v = a[((size_t)c * h + sy * y + i) * w + sx * x + j];
                             if (v > m) m = v;
                         }
                     o[((size_t)c * ho + y) * wo + x] = m;
@@ -114,9 +122,10 @@ int oracle_patch_forward(const olayer *layers, int n_layers, const double *img,
             const int ky = L->k, kx = kcols(L);
             if (ky < 1 || kx < 1) return -1;
             if (L->kind == O_POOL) {
-                if (h % ky || w % kx) return -1;
-                h /= ky;
-                w /= kx;
+                const int sy = srows(L), sx = scols(L);
+                if (sy < 1 || sx < 1 || h < ky || w < kx || (h - ky) % sy || (w - kx) % sx) return -1;
+                h = (h - ky) / sy + 1;
+                w = (w - kx) / sx + 1;
             } else {
                 if (ky > h || kx > w) return -1;
                 h -= ky - 1;

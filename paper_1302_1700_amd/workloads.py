@@ -36,8 +36,16 @@ def conv(k, c_in, c_out, act="tanh", kx=None):
     return _layer("conv", k, c_in, c_out, act, kx)
 
 
-def pool(k, c, kx=None):
-    return _layer("pool", k, c, c, "none", kx)
+def pool(k, c, kx=None, stride=None, stride_x=None):
+    """A k x kx max-pool; stride / stride_x (default: the pool's size, the
+    non-overlapping pools of the paper) give the step between windows."""
+    L = _layer("pool", k, c, c, "none", kx)
+    if stride is not None or stride_x is not None:
+        kx_ = L.get("kx", k)
+        sy = stride if stride is not None else k
+        sx = stride_x if stride_x is not None else (sy if kx_ == k and stride is not None else kx_)
+        L["stride"], L["stride_x"] = sy, sx
+    return L
 
 
 def fc(k, c_in, c_out, act="tanh", kx=None):
@@ -212,6 +220,38 @@ def random_rect_net(rng, max_layers=6, max_c=5):
         ky, kx = L["k"], L.get("kx", L["k"])
         if L["kind"] == "pool":
             h, w = h * ky, w * kx
+        else:
+            h, w = h + ky - 1, w + kx - 1
+    return layers, (h, w), c_in0
+
+
+def random_stride_net(rng, max_layers=6, max_c=5):
+    """A random stack whose pools may overlap (stride below the size) or
+    leave gaps (stride above it), square or rectangular.  Returns (layers,
+    (h0, w0), c_in)."""
+    n_cls = int(rng.integers(2, 4))
+    c = int(rng.integers(1, max_c + 1))
+    c_in0 = c
+    layers = []
+    for _ in range(int(rng.integers(1, max_layers))):
+        if rng.random() < 0.5:
+            ky, kx = int(rng.integers(1, 5)), int(rng.integers(1, 5))
+            sy, sx = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+            layers.append(pool(ky, c, kx=kx, stride=sy, stride_x=sx))
+        else:
+            co = int(rng.integers(1, max_c + 1))
+            layers.append(conv(int(rng.integers(1, 4)), c, co, "tanh" if rng.random() < 0.7 else "none",
+                               kx=int(rng.integers(1, 4))))
+            c = co
+    hidden = int(rng.integers(2, 6))
+    hy, hx = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+    layers.append(fc(hy, c, hidden, "tanh", kx=hx))
+    layers.append(fc(1, hidden, n_cls, "softmax"))
+    h, w = hy, hx
+    for L in reversed(layers[:-2]):
+        ky, kx = L["k"], L.get("kx", L["k"])
+        if L["kind"] == "pool":
+            h, w = (h - 1) * L.get("stride", ky) + ky, (w - 1) * L.get("stride_x", kx) + kx
         else:
             h, w = h + ky - 1, w + kx - 1
     return layers, (h, w), c_in0

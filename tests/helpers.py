@@ -9,13 +9,19 @@ def _k(L):
     return L["k"], L.get("kx", L["k"])
 
 
+def _s(L):
+    """(rows, columns) stride of a pool (its size unless given)."""
+    ky, kx = _k(L)
+    return L.get("stride", ky), L.get("stride_x", kx)
+
+
 def torch_patch_net(layers, params, crop):
     """The net on one patch with torch CPU library routines, float64.
     crop: [h0, w0, C] -> returns [n_out]."""
     x = torch.from_numpy(np.asarray(crop, np.float64)).permute(2, 0, 1)[None]
     for L, p in zip(layers, params):
         if L["kind"] == "pool":
-            x = F.max_pool2d(x, _k(L))
+            x = F.max_pool2d(x, _k(L), stride=_s(L))
         else:
             w = torch.from_numpy(np.asarray(p[0], np.float64))
             b = torch.from_numpy(np.asarray(p[1], np.float64))
@@ -35,7 +41,8 @@ def torch_patch_net(layers, params, crop):
 def dilated_scan(layers, params, image):
     """Whole-map formulation with dilated library convolutions: a conv after
     pools of cumulative stride S is a convolution with dilation S, a k-pool is
-    a stride-1 max-pool with dilation S, and then S grows by k (per axis).
+    a stride-1 max-pool with dilation S, and then S grows by the pool's stride
+    (its size k unless it has another; per axis).
     Output index = patch top-left corner.  [B,H,W,C] -> [B, H-h0+1, W-w0+1, n]."""
     x = torch.from_numpy(np.asarray(image, np.float64)).permute(0, 3, 1, 2)
     Sy = Sx = 1
@@ -43,8 +50,8 @@ def dilated_scan(layers, params, image):
         ky, kx = _k(L)
         if L["kind"] == "pool":
             x = F.max_pool2d(x, (ky, kx), stride=1, dilation=(Sy, Sx))
-            Sy *= ky
-            Sx *= kx
+            Sy *= _s(L)[0]
+            Sx *= _s(L)[1]
         else:
             w = torch.from_numpy(np.asarray(p[0], np.float64))
             b = torch.from_numpy(np.asarray(p[1], np.float64))

@@ -10,6 +10,7 @@ typedef struct {
     int kind, k, kx, c_in, c_out, act;
     const double *w;
     const double *b;
+    int s, sx;
 } olayer;
 
 int oracle_patch_forward(const olayer *layers, int n_layers, const double *img, int B, int H, int W, int C, int h0,
@@ -85,6 +86,19 @@ int main(void)
             re[i].b = fill(re[i].c_out);
         }
     ok = ok && run(re, 5, 2, 19, 23, 2, 7, 11, 1);
+    /* pools with strides: conv 2x2 2->3 tanh, pool 3x2 stride 2x1, pool 2x2 stride 3, fc 1x2 3->2 softmax
+     * (6 x 7) */
+    olayer st[4] = {{0, 2, 2, 2, 3, 1, 0, 0, 0, 0}, {1, 3, 2, 3, 3, 0, 0, 0, 2, 1}, {1, 2, 2, 3, 3, 0, 0, 0, 3, 3},
+                    {2, 1, 2, 3, 2, 2, 0, 0, 0, 0}};
+    for (int i = 0; i < 4; i += 3) {
+        st[i].w = fill((size_t)st[i].c_out * st[i].c_in * st[i].k * st[i].kx);
+        st[i].b = fill(st[i].c_out);
+    }
+    ok = ok && run(st, 4, 2, 17, 15, 2, 6, 7, 1);
+    for (int i = 0; i < 4; i += 3) {
+        free((void *)st[i].w);
+        free((void *)st[i].b);
+    }
     for (int i = 0; i < 6; ++i) {
         free((void *)sq[i].w);
         free((void *)sq[i].b);

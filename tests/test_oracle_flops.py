@@ -5,7 +5,9 @@ that do not come from its own recursion:
 
   - a closed form per axis.  Summed over the fragments, a k-wide layer (a
     convolution, Eqs. 3-4, or a pool, Eqs. 6-7: sum over o < k of
-    div(s - o, k) = s - (k - 1)) removes k - 1 pixels from every fragment,
+    div(s - o, k) = s - (k - 1); for a pool of stride t, sum over o < t of
+    div(s - o - k + t, t) = s - (k - 1) likewise) removes k - 1 pixels from
+    every fragment,
     so the total width after layer l is W - sum_{m <= l} (k_m - 1) * Q_m,
     with Q_m the fragments per axis entering layer m (the size of the map of
     the same layer applied with dilation Q_m, and the final total is the
@@ -43,8 +45,8 @@ def closed_form(layers, B, H, W):
         ky, kx = L["k"], L.get("kx", L["k"])
         Ty -= (ky - 1) * Qy
         Tx -= (kx - 1) * Qx
-        if L["kind"] == "pool":
-            Qy, Qx = Qy * ky, Qx * kx
+        if L["kind"] == "pool":  # its stride, the fragments' step (its size unless given)
+            Qy, Qx = Qy * L.get("stride", ky), Qx * L.get("stride_x", kx)
             res.append(0)
         else:
             res.append(B * Ty * Tx * 2 * L["c_in"] * ky * kx * L["c_out"])
@@ -55,7 +57,7 @@ def _strides(layers):
     Sy = Sx = 1
     for L in layers:
         if L["kind"] == "pool":
-            Sy, Sx = Sy * L["k"], Sx * L.get("kx", L["k"])
+            Sy, Sx = Sy * ix.syx(L)[0], Sx * ix.syx(L)[1]
     return Sy, Sx
 
 
@@ -67,8 +69,10 @@ def _cases():
     for w in wl.WORKLOADS.values():
         out.append((w.layers, w.batch, w.height, w.width))
     rng = np.random.default_rng(9100)
-    for n in range(30):
-        if n % 2:
+    for n in range(45):
+        if n % 3 == 2:
+            layers, (h0, w0), _ = wl.random_stride_net(rng)
+        elif n % 3 == 1:
             layers, (h0, w0), _ = wl.random_rect_net(rng)
         else:
             layers, w0, _ = wl.random_net(rng)

@@ -30,8 +30,12 @@ MUTATIONS = {
                             "L->w[(((size_t)ci * L->c_out + co) * ky + dy) * kx + dx]"),
     "kernel_rows_cols_swapped": ("L->w[(((size_t)co * L->c_in + ci) * ky + dy) * kx + dx]",
                                  "L->w[(((size_t)co * L->c_in + ci) * kx + dx) * ky + dy]"),
-    "pool_rows_cols_swapped": ("double m = a[((size_t)c * h + ky * y) * w + kx * x];",
-                               "double m = a[((size_t)c * h + kx * y) * w + ky * x];"),
+    "pool_rows_cols_swapped": ("double v = a[((size_t)c * h + sy * y + i) * w + sx * x + j];",
+                               "double v = a[((size_t)c * h + sx * y + i) * w + sy * x + j];"),
+    "pool_stride_taken_as_size": ("double v = a[((size_t)c * h + sy * y + i) * w + sx * x + j];",
+                                  "double v = a[((size_t)c * h + ky * y + i) * w + kx * x + j];"),
+    "pool_out_size_as_if_not_overlapping": ("int ho = (h - ky) / sy + 1, wo = (w - kx) / sx + 1;",
+                                            "int ho = h / sy, wo = w / sx;"),
     "activation_on_softmax_layer": ("if (L->act == O_ACT_TANH) s = tanh(s);",
                                     "if (L->act != O_ACT_NONE) s = tanh(s);"),
     "softmax_unnormalised": ("for (int i = 0; i < n; ++i) z[i] /= s;", "for (int i = 0; i < n; ++i) z[i] /= 1.0;"),
@@ -46,6 +50,14 @@ RECT_NET = [{"kind": "conv", "k": 2, "kx": 3, "c_in": 2, "c_out": 3, "act": "tan
             {"kind": "conv", "k": 3, "kx": 2, "c_in": 3, "c_out": 4, "act": "tanh"},
             {"kind": "pool", "k": 1, "kx": 2, "c_in": 4, "c_out": 4, "act": "none"},
             {"kind": "fc", "k": 1, "kx": 1, "c_in": 4, "c_out": 3, "act": "softmax"}]
+
+
+# overlapping (3x2 window, stride 2x1) and gapped (2x2 window, stride 3)
+# pools; window 6 x 7
+STRIDE_NET = [{"kind": "conv", "k": 2, "kx": 2, "c_in": 2, "c_out": 3, "act": "tanh"},
+              {"kind": "pool", "k": 3, "kx": 2, "c_in": 3, "c_out": 3, "act": "none", "stride": 2, "stride_x": 1},
+              {"kind": "pool", "k": 2, "kx": 2, "c_in": 3, "c_out": 3, "act": "none", "stride": 3, "stride_x": 3},
+              {"kind": "fc", "k": 1, "kx": 2, "c_in": 3, "c_out": 2, "act": "softmax"}]
 
 
 def _build_mutant(tmp_path, name):
@@ -101,6 +113,13 @@ def _battery(lib):
         got = oracle.patch_forward(RECT_NET, params, img, (7, 11), lib_path=lib)
         fails.append(np.abs(got[0, 0, 0] - torch_patch_net(RECT_NET, params, img[0, :7, :11])).max() > 1e-12)
         fails.append(np.abs(got - dilated_scan(RECT_NET, params, img)).max() > 1e-12)
+        # pools with a stride other than their size: one window == torch
+        # library net, the whole map == dilated formulation
+        params = wl.make_weights(STRIDE_NET, 6, 0.6)
+        img = wl.make_image(8, 1, 6 + 7, 7 + 5, 2)
+        got = oracle.patch_forward(STRIDE_NET, params, img, (6, 7), lib_path=lib)
+        fails.append(np.abs(got[0, 0, 0] - torch_patch_net(STRIDE_NET, params, img[0, :6, :7])).max() > 1e-12)
+        fails.append(np.abs(got - dilated_scan(STRIDE_NET, params, img)).max() > 1e-12)
         # hand-evaluated ramp (box sums and a max-pool)
         ramp = (10.0 * np.arange(5)[:, None] + np.arange(5)[None, :]).reshape(1, 5, 5, 1)
         lay = [wl.conv(2, 1, 1, "none"), wl.pool(2, 1), wl.fc(1, 1, 1, "none")]
@@ -168,6 +187,27 @@ def test_floor_vs_ceil_extent_fails_coverage():
         if L["kind"] == "pool":
             frags = [(math.ceil((sy - oy) / k), math.ceil((sx - ox) / k))
                      for (sy, sx) in frags for oy in range(k) for ox in range(k)]
+        else:
+            frags = [(sy - (k - 1), sx - (k - 1)) for (sy, sx) in frags]
+    assert sum(a * b for a, b in frags) != n
+
+
+def test_stride_as_size_in_extents_fails_coverage():
+    """Eqs. 6-7 written for non-overlapping pools (div(s - o, k) over k
+    offsets) on a net whose pools overlap or leave gaps breaks the coverage
+    pin; the stride form covers every window once."""
+    layers = [wl.conv(2, 1, 1), wl.pool(3, 1, stride=2), wl.conv(2, 1, 1), wl.pool(2, 1, stride=3),
+              wl.fc(1, 1, 1, "none")]
+    h0 = ix.patch_size(layers)
+    H, W = h0 + 11, h0 + 7
+    n = (H - h0 + 1) * (W - h0 + 1)
+    assert sum(a * b for a, b in ix.fragment_extents(layers, H, W)[-1]) == n
+    frags = [(H, W)]
+    for L in layers:
+        k = L["k"]
+        if L["kind"] == "pool":
+            frags = [(max(sy - oy, 0) // k, max(sx - ox, 0) // k) for (sy, sx) in frags
+                     for oy in range(k) for ox in range(k)]
         else:
             frags = [(sy - (k - 1), sx - (k - 1)) for (sy, sx) in frags]
     assert sum(a * b for a, b in frags) != n

@@ -316,3 +316,86 @@ def test_rect_whole_map_and_frag_cpu(seed):
     got = oracle.frag_cpu.frag_scan(layers, params, img, (h0, w0))
     assert not np.isnan(got).any()
     assert np.abs(got - ref).max() <= 1e-12
+
+
+# ---- Pools whose stride differs from their size (a generalisation: the
+# ---- paper's pools do not overlap, Section 2.1.2) ---------------------------
+
+def test_hand_stride_pools():
+    """Overlapping (3x3, stride 2) and gapped (2x2, stride 3) pools on a
+    ramp: closed forms worked out by hand, for the per-window oracle and the
+    CPU fragment method."""
+    g = _gold("hand_stride_pools.json")
+    img = (10.0 * np.arange(7)[:, None] + np.arange(6)[None, :]).reshape(1, 7, 6, 1)
+    for case in g["cases"]:
+        k, st = case["pool"]["k"], case["pool"]["stride"]
+        layers = [wl.pool(k, 1, stride=st), wl.fc(2, 1, 1, "none")]
+        params = [None, (np.ones((1, 1, 2, 2)), np.zeros(1))]
+        assert ix.patch_size(layers) == 5
+        want = np.array(case["expected"], np.float64)
+        assert np.array_equal(oracle.patch_forward(layers, params, img, 5)[0, :, :, 0], want), case["name"]
+        assert np.array_equal(oracle.frag_cpu.frag_scan(layers, params, img, 5)[0, :, :, 0], want), case["name"]
+
+
+def test_stride_equal_to_size_is_the_paper_pool():
+    """A stride equal to the pool's size changes nothing: the same sizes,
+    fragments and outputs as the plain pool of Section 2.2.2."""
+    plain = wl.WORKLOADS[1].layers
+    strided = [dict(L, stride=L["k"], stride_x=L["k"]) if L["kind"] == "pool" else L for L in plain]
+    params, img = wl.workload_inputs(1, height=30, width=27)
+    assert ix.fragment_extents(plain, 30, 27) == ix.fragment_extents(strided, 30, 27)
+    assert np.array_equal(ix.reassembly_index(plain, 30, 27), ix.reassembly_index(strided, 30, 27))
+    assert np.array_equal(oracle.patch_forward(plain, params, img, 14), oracle.patch_forward(strided, params, img, 14))
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_stride_sizes_counts_and_coverage(seed):
+    """Random stacks with overlapping and gapped pools: the window derived
+    bottom-up reduces to 1 x 1, there are prod(s_y * s_x) final fragments,
+    and every window lands on exactly one position of one final fragment
+    (corner tracking), inside the fragment sizes of the extent recursion."""
+    rng = np.random.default_rng(2500 + seed)
+    layers, (h0, w0), _ = wl.random_stride_net(rng)
+    assert ix.patch_hw(layers) == (h0, w0)
+    assert ix.patch_sizes(layers, h0, 0)[-1] == 1 == ix.patch_sizes(layers, w0, 1)[-1]
+    prod = 1
+    for L in layers:
+        if L["kind"] == "pool":
+            prod *= ix.syx(L)[0] * ix.syx(L)[1]
+    H, W = h0 + int(rng.integers(0, 15)), w0 + int(rng.integers(0, 15))
+    ext = ix.fragment_extents(layers, H, W)
+    assert len(ext[-1]) == prod == ix.n_fragments(layers)
+    idx = ix.reassembly_index(layers, H, W).reshape(-1, 3)
+    keys = set(map(tuple, idx.tolist()))
+    assert len(keys) == idx.shape[0] == (H - h0 + 1) * (W - w0 + 1)
+    assert sum(a * b for a, b in ext[-1]) == len(keys)
+    for f, e in ix.fragment_table(layers, H, W).items():
+        assert e["size"] == ext[-1][f]
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_stride_window_equals_library_net(seed):
+    """One window == torch's max_pool2d with the same stride (library
+    routine) in a torch-CPU net."""
+    rng = np.random.default_rng(2600 + seed)
+    layers, (h0, w0), c0 = wl.random_stride_net(rng)
+    params = wl.make_weights(layers, seed, 0.5)
+    img = wl.make_image(seed, 1, h0, w0, c0)
+    got = oracle.patch_forward(layers, params, img, (h0, w0))[0, 0, 0]
+    assert np.abs(got - torch_patch_net(layers, params, img[0])).max() <= 1e-12
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_stride_whole_map_and_frag_cpu(seed):
+    """Whole map == the dilated library formulation (a pool of stride s
+    multiplies the dilation by s), and the CPU fragment method == the
+    per-window definition, with overlapping and gapped pools."""
+    rng = np.random.default_rng(2700 + seed)
+    layers, (h0, w0), c0 = wl.random_stride_net(rng)
+    params = wl.make_weights(layers, seed, 0.5)
+    img = wl.make_image(seed, 2, h0 + int(rng.integers(0, 9)), w0 + int(rng.integers(0, 9)), c0)
+    ref = oracle.patch_forward(layers, params, img, (h0, w0))
+    assert np.abs(ref - dilated_scan(layers, params, img)).max() <= 1e-12
+    got = oracle.frag_cpu.frag_scan(layers, params, img, (h0, w0))
+    assert not np.isnan(got).any()
+    assert np.abs(got - ref).max() <= 1e-12
