@@ -27,6 +27,14 @@
  *     generalises directly): a layer's k_x gives its columns, the window is
  *     h_0 x w_0, and every rule above holds per axis, rows with h_0 and k,
  *     columns with w_0 and k_x (a k x k_x pool has k * k_x children).
+ *   - Pools whose windows step by s instead of their size k (overlapping for
+ *     s < k, leaving gaps for s > k; not in the paper, whose pools do not
+ *     overlap): the patch-level map side w becomes (w - k) / s + 1 and must
+ *     divide exactly, and every rule above holds with s in place of k where
+ *     it counts children and offsets: s^2 children f * s^2 + o_y * s + o_x,
+ *     o in {0..s-1}^2, each holding div(n - o - k + s, s) pixels per axis of
+ *     a parent of n (the windows starting at o, o + s, ... that end inside
+ *     it).
  *
  * Errors: every call returns an fs_status and never throws or aborts across
  * this boundary; fs_last_error() gives a thread-local message for the last
@@ -84,7 +92,12 @@ typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
  * k_x: the kernel's or pool's columns when they differ from its rows k
  * (Section 2: the square case generalises directly to rectangles, each rule
  * holding per axis); 0 means k_x = k.  An FS_FC layer passing k = 0 passes
- * k_x = 0 too. */
+ * k_x = 0 too.
+ * stride, stride_x (FS_MAXPOOL only): rows / columns between the starts of
+ * neighbouring pooling windows; stride 0 means k (the paper's
+ * non-overlapping pools), stride_x 0 means stride when stride is given, else
+ * k_x.  Convolutions and fully connected layers pass 0 (stride 1; any other
+ * value gives FS_ERR_UNSUPPORTED). */
 typedef struct {
     int32_t kind;
     int32_t k;
@@ -94,6 +107,8 @@ typedef struct {
     const float *weight;
     const float *bias;
     int32_t k_x;
+    int32_t stride;
+    int32_t stride_x;
 } fs_layer;
 
 typedef struct {
@@ -102,13 +117,15 @@ typedef struct {
     int32_t n_classes;    /* c_out of the last layer */
     int32_t n_layers;
     int32_t n_pools;
-    int32_t stride;       /* product of pool sizes: output pixels one final
-                             fragment pixel step covers, per axis (rows) */
+    int32_t stride;       /* product of the pools' strides (their sizes for the
+                             paper's pools): output pixels one final fragment
+                             pixel step covers, per axis (rows) */
     int32_t n_fragments;  /* F_L, the product of the squared pool sizes
-                             (Section 3; rectangular pools: of k * k_x) */
+                             (Section 3; rectangular pools: of k * k_x;
+                             strided pools: of stride * stride_x) */
     int32_t dtype;        /* fs_dtype */
     int32_t patch_x;      /* the window's columns (= patch for square nets) */
-    int32_t stride_x;     /* product of the pools' columns k_x */
+    int32_t stride_x;     /* product of the pools' column strides (k_x) */
 } fs_net_info;
 
 typedef struct {
@@ -146,8 +163,8 @@ typedef struct {
 /* Create a net.  The stack must be: conv / max-pool layers in any order, then
  * one or more fully connected layers (Section 2); channels must chain; every
  * pool must divide the patch-level map it receives (Section 2.1.2:
- * mod(w_{l-1}, k) = 0); the patch-level map after the last layer must be
- * 1 x 1.  `patch` is w_0 (0: derive it from the stack; a rectangular stack,
+ * mod(w_{l-1}, k) = 0; with a stride s, mod(w_{l-1} - k, s) = 0); the
+ * patch-level map after the last layer must be 1 x 1.  `patch` is w_0 (0: derive it from the stack; a rectangular stack,
  * whose window is h_0 x w_0 with h_0 != w_0, must pass 0 and give its fully
  * connected sizes).  A patch that does
  * not agree with the stack gives FS_ERR_SHAPE; more than 16384 channels in a
@@ -293,7 +310,8 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
  * where (h_f, w_f) is the fragment's size after the last layer (Eqs. 3-4 and
  * 6-7, never below 0) and output pixel (Y0 + stride * y, X0 + stride_x * x)
  * holds the fragment's pixel (y, x).  The children of fragment f of a
- * k x k_x pool are f * k * k_x + o_y * k_x + o_x.  Host output; writes at most `capacity`
+ * k x k_x pool are f * k * k_x + o_y * k_x + o_x (of a pool with strides
+ * s x s_x: f * s * s_x + o_y * s_x + o_x).  Host output; writes at most `capacity`
  * int32 and stores the number the full table needs in *n_needed (n_needed
  * may be NULL; h_out may be NULL to query the size). */
 fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_out,

@@ -84,7 +84,8 @@ def frag_scan(layers, params, image, patch):
         for L, p in zip(layers, params):
             if L["kind"] == "pool":
                 ky, kx = L["k"], L.get("kx", L["k"])
-                sy, sx = L.get("stride", ky), L.get("stride_x", kx)
+                sy = L.get("stride", ky)
+                sx = L.get("stride_x", sy if "stride" in L else kx)
                 nxt = []
                 for (by, bx, ty, tx, a) in frags:
                     for (oy, ox), m in _pool_children(a, ky, kx, sy, sx):

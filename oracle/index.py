@@ -50,9 +50,11 @@ def kyx(L):
 
 
 def syx(L):
-    """(rows, columns) stride of a pool (its size unless given)."""
+    """(rows, columns) stride of a pool: its size unless given; a column
+    stride that is not given follows the row stride when that one is."""
     ky, kx = kyx(L)
-    return L.get("stride", ky), L.get("stride_x", kx)
+    sy = L.get("stride", ky)
+    return sy, L.get("stride_x", sy if "stride" in L else kx)
 
 
 def patch_sizes(layers, w0, axis=0):

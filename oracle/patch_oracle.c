@@ -40,12 +40,12 @@ typedef struct {
     int kind, k, kx, c_in, c_out, act; /* k: rows of the kernel / pool; kx: columns (0: k) */
     const double *w; /* [c_out][c_in][k][kx] */
     const double *b; /* [c_out] */
-    int s, sx;       /* pools: row and column stride (0: the pool's rows k, columns kx) */
+    int s, sx;       /* pools: row and column stride (0: the pool's rows k; columns: s if given, else kx) */
 } olayer;
 
 static int kcols(const olayer *L) { return L->kx ? L->kx : L->k; }
 static int srows(const olayer *L) { return L->s ? L->s : L->k; }
-static int scols(const olayer *L) { return L->sx ? L->sx : kcols(L); }
+static int scols(const olayer *L) { return L->sx ? L->sx : (L->s ? L->s : kcols(L)); }
 
 /* One layer on one patch.  `a` holds c_in maps of h x w as [c][y][x]; the
  * result goes to `o` and its size to *h_out x *w_out.  Returns 0 or -1 on a

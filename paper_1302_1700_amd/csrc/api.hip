@@ -86,6 +86,7 @@ uint16_t host_f2bf(float f)
 struct NetLayer {
     int kind, k, cin, cout, act;
     int kx;               // columns of the kernel / pool (k: its rows; Section 2's rectangular case)
+    int sy = 1, sx = 1;   // pools: the step between windows, rows and columns (the paper's: k, kx)
     int h_in, h_out, w_in, w_out;  // patch-level map sizes (Sections 2.1.1, 2.1.2)
     // conv launch parameters fixed at creation
     bool vec = false;     // channel-vector path
@@ -107,8 +108,8 @@ struct fs_net {
     std::vector<NetLayer> L;
     int patch = 0, C = 0, dtype = 0, ncls = 0;  // patch: window rows h_0
     int patch_x = 0;                             // window columns w_0
-    std::vector<int> pool_k, pool_kx;            // pool rows, columns, in layer order
-    int S = 1, Sx = 1, F = 1;                    // products of the pool rows / columns; fragments
+    std::vector<int> pool_k, pool_kx;            // pool strides (the radix of the fragment grid), rows, columns, in layer order
+    int S = 1, Sx = 1, F = 1;                    // products of the pool strides per axis; fragments
     int device = 0;
     bool head_fc = false;     // last layer fused into the head
     size_t head_w_off = 0, head_b_off = 0;
@@ -493,19 +494,21 @@ fs_status plan_conv_tiles(const fs_net *net, const NetLayer &l, const Geo &in, L
     return fail(FS_ERR_UNSUPPORTED, "layer %d: no convolution tile fits in LDS", L.layer);
 }
 
-// Children of a ky x kx pool (Eqs. 5-7, per axis): parent index i and
-// offset o give child i*k + o of size floor((s - o) / k).
-Geo pool_geo(const Geo &g, int ky, int kx)
+// Children of a ky x kx pool with strides sy x sx (Eqs. 5-7, per axis; the
+// paper's pools have s = k): parent index i and offset o < s give child
+// i*s + o, holding the windows o, o + s, ... that end inside the parent:
+// floor((n - o - k + s) / s) of them for a parent of size n, never below 0.
+Geo pool_geo(const Geo &g, int ky, int kx, int sy, int sx)
 {
     Geo o;
-    o.Qy = g.Qy * ky;
-    o.Qx = g.Qx * kx;
+    o.Qy = g.Qy * sy;
+    o.Qx = g.Qx * sx;
     o.ey.assign(o.Qy, 0);
     o.ex.assign(o.Qx, 0);
     for (int i = 0; i < g.Qy; ++i)
-        for (int off = 0; off < ky; ++off) o.ey[i * ky + off] = std::max(g.ey[i] - off, 0) / ky;
+        for (int off = 0; off < sy; ++off) o.ey[i * sy + off] = std::max(g.ey[i] - off - ky + sy, 0) / sy;
     for (int i = 0; i < g.Qx; ++i)
-        for (int off = 0; off < kx; ++off) o.ex[i * kx + off] = std::max(g.ex[i] - off, 0) / kx;
+        for (int off = 0; off < sx; ++off) o.ex[i * sx + off] = std::max(g.ex[i] - off - kx + sx, 0) / sx;
     o.C = g.C;
     o.hmax = *std::max_element(o.ey.begin(), o.ey.end());
     o.wmax = *std::max_element(o.ex.begin(), o.ex.end());
@@ -585,6 +588,7 @@ bool want_pool_fusion(const fs_net *net, int li)
     if (li + 1 >= nl) return false;
     const NetLayer &l = net->L[li], &p = net->L[li + 1];
     if (l.kind == FS_MAXPOOL || p.kind != FS_MAXPOOL || l.nbt != l.nb * l.wn) return false;
+    if (p.sy != p.k || p.sx != p.kx) return false;  // the fused walk samples the filter at steps of k
     if (const char *e = getenv("FRAGSCAN_POOL_FUSE"); e && e[0]) return e[0] == '1';
     const double ov = (p.k == 2 && p.kx == 2) ? 0.35 : 0.5;
     const double ridge = net->dtype == DT_BF16 ? 2516.6e12 / 8e12 : 157.3e12 / 8e12;  // FLOP per byte
@@ -665,9 +669,9 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         Geo o;
         if (l.kind == 1) {  // pool
             const int ky = l.k, kx = l.kx;
-            if (g.Qy * ky > kMaxAxis || g.Qx * kx > kMaxAxis)
+            if (g.Qy * l.sy > kMaxAxis || g.Qx * l.sx > kMaxAxis)
                 return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
-            o = pool_geo(g, ky, kx);
+            o = pool_geo(g, ky, kx, l.sy, l.sx);
             L.type = 1;
             if (g.is_image && view) return fail(FS_ERR_UNSUPPORTED, "a tiled scan needs a convolution first");
             PoolArgs &a = L.pool;
@@ -680,13 +684,15 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             a.C = g.C;
             a.ky = ky;
             a.kx = kx;
-            a.n_children = B * F * ky * kx;
+            a.sy = l.sy;
+            a.sx = l.sx;
+            a.n_children = B * F * l.sy * l.sx;
             fill_axis(a.ext, g);
-            L.gx = (int)std::min<long long>((long long)B * F * ky * kx * a.out_h, kMaxGrid);
-            L.frags = B * F * ky * kx;
+            L.gx = (int)std::min<long long>((long long)B * F * l.sy * l.sx * a.out_h, kMaxGrid);
+            L.frags = B * F * l.sy * l.sx;
             L.out_pixels = (long long)B * true_pixels(o);
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * o.C * es;
-            L.name = pool_kernel_name(net->dtype, g.is_image, ky, kx, g.C);
+            L.name = pool_kernel_name(net->dtype, g.is_image, ky, kx, l.sy, l.sx, g.C);
         } else {  // conv or fc as convolution
             const int ky = l.k, kx = l.kx;
             o.Qy = g.Qy;
@@ -821,7 +827,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 const int kpy = net->L[li + 1].k, kpx = net->L[li + 1].kx;
                 if (g.Qy * kpy > kMaxAxis || g.Qx * kpx > kMaxAxis)
                     return fail(FS_ERR_UNSUPPORTED, "more than %d fragments per axis", kMaxAxis);
-                const Geo o2 = pool_geo(o, kpy, kpx);
+                const Geo o2 = pool_geo(o, kpy, kpx, kpy, kpx);
                 a.pool_ky = kpy;
                 a.pool_kx = kpx;
                 a.pool_oh = std::max(o2.hmax, 1);
@@ -1213,15 +1219,22 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
         if (s.c_in < 1 || s.c_out < 1) return fail(FS_ERR_SHAPE, "layer %d: channel counts must be >= 1", i);
         if (s.c_in > kMaxChannels || s.c_out > kMaxChannels)
             return fail(FS_ERR_UNSUPPORTED, "layer %d: more than %d channels", i, kMaxChannels);
+        if (s.stride < 0 || s.stride_x < 0) return fail(FS_ERR_INVALID_ARG, "layer %d: negative stride", i);
         if (s.kind == FS_MAXPOOL) {
             if (seen_fc) return fail(FS_ERR_SHAPE, "layer %d: pooling after a fully connected layer", i);
             if (s.k < 1 || l.kx < 1) return fail(FS_ERR_SHAPE, "layer %d: pool size must be >= 1", i);
+            // stride 0: the pool's own size (the paper's non-overlapping
+            // pools); stride_x 0: the row stride when one is given
+            l.sy = s.stride ? s.stride : l.k;
+            l.sx = s.stride_x ? s.stride_x : (s.stride ? s.stride : l.kx);
             if (s.c_out != s.c_in) return fail(FS_ERR_SHAPE, "layer %d: a pool keeps the channel count", i);
             if (s.weight || s.bias) return fail(FS_ERR_INVALID_ARG, "layer %d: a pool has no weights", i);
             if (s.act != FS_ACT_NONE) return fail(FS_ERR_UNSUPPORTED, "layer %d: activation on a pool", i);
         } else {
             if (s.kind == FS_CONV && seen_fc)
                 return fail(FS_ERR_SHAPE, "layer %d: convolution after a fully connected layer", i);
+            if (s.stride || s.stride_x)
+                return fail(FS_ERR_UNSUPPORTED, "layer %d: the method's convolutions have stride 1", i);
             if (s.kind == FS_FC) seen_fc = true;
             if (s.k < 0 || (s.k == 0 && s.kind != FS_FC)) return fail(FS_ERR_SHAPE, "layer %d: bad kernel size", i);
             if (s.k_x < 0 || (s.k == 0) != (l.kx == 0))
@@ -1239,8 +1252,8 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
     if (derivable) {
         int h = 1, w = 1;
         for (int i = n_layers - 1; i >= 0; --i) {
-            h = (L[i].kind == FS_MAXPOOL) ? h * L[i].k : h + L[i].k - 1;
-            w = (L[i].kind == FS_MAXPOOL) ? w * L[i].kx : w + L[i].kx - 1;
+            h = (L[i].kind == FS_MAXPOOL) ? (h - 1) * L[i].sy + L[i].k : h + L[i].k - 1;
+            w = (L[i].kind == FS_MAXPOOL) ? (w - 1) * L[i].sx + L[i].kx : w + L[i].kx - 1;
         }
         if (patch == 0) {
             h0 = h;
@@ -1258,11 +1271,13 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
             l.h_in = h;
             l.w_in = w;
             if (l.kind == FS_MAXPOOL) {
-                if (h % l.k || w % l.kx)
-                    return fail(FS_ERR_SHAPE, "layer %d: pool %dx%d does not divide the map %dx%d", i, l.k, l.kx, h,
-                                w);
-                h /= l.k;
-                w /= l.kx;
+                // Section 2.1.2: mod(w, k) = 0; with a stride s, the windows
+                // at 0, s, ... must end at the map's edge: mod(w - k, s) = 0
+                if (h < l.k || w < l.kx || (h - l.k) % l.sy || (w - l.kx) % l.sx)
+                    return fail(FS_ERR_SHAPE, "layer %d: pool %dx%d (stride %dx%d) does not tile the map %dx%d", i,
+                                l.k, l.kx, l.sy, l.sx, h, w);
+                h = (h - l.k) / l.sy + 1;
+                w = (w - l.kx) / l.sx + 1;
             } else {
                 if (l.kind == FS_FC && l.k == 0) {
                     l.k = h;
@@ -1291,11 +1306,11 @@ static fs_status net_create(const fs_layer *layers, int32_t n_layers, int32_t in
     net->ncls = L.back().cout;
     for (auto &l : L)
         if (l.kind == FS_MAXPOOL) {
-            net->pool_k.push_back(l.k);
-            net->pool_kx.push_back(l.kx);
-            net->S *= l.k;
-            net->Sx *= l.kx;
-            net->F *= l.k * l.kx;
+            net->pool_k.push_back(l.sy);
+            net->pool_kx.push_back(l.sx);
+            net->S *= l.sy;
+            net->Sx *= l.sx;
+            net->F *= l.sy * l.sx;
         }
     if (net->S > kMaxAxis || net->Sx > kMaxAxis) {
         delete net;
@@ -1736,9 +1751,8 @@ fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_
 {
     if (!net) return fail(FS_ERR_INVALID_ARG, "net is NULL");
     std::shared_ptr<const Plan> PP;
-    fs_status st = get_plan(net, 1, H, W, PP);
+    fs_status st = get_plan(net, 1, H, W, PP);  // (validates the size)
     if (st != FS_OK) return st;
-    const Plan &P = *PP;
     const int np = (int)net->pool_k.size();
     const size_t rec = 5 + 2 * (size_t)np;
     const size_t need = rec * net->F;
@@ -1750,9 +1764,9 @@ fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_
         if (l.kind == FS_MAXPOOL) {
             std::vector<int> ny, nx;
             for (size_t i = 0; i < ey.size(); ++i)
-                for (int o = 0; o < l.k; ++o) ny.push_back(std::max(ey[i] - o, 0) / l.k);
+                for (int o = 0; o < l.sy; ++o) ny.push_back(std::max(ey[i] - o - l.k + l.sy, 0) / l.sy);
             for (size_t i = 0; i < ex.size(); ++i)
-                for (int o = 0; o < l.kx; ++o) nx.push_back(std::max(ex[i] - o, 0) / l.kx);
+                for (int o = 0; o < l.sx; ++o) nx.push_back(std::max(ex[i] - o - l.kx + l.sx, 0) / l.sx);
             ey.swap(ny);
             ex.swap(nx);
         } else {

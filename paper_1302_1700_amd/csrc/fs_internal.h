@@ -97,12 +97,13 @@ static_assert(sizeof(ConvArgs) <= 4096, "ConvArgs must stay within the kernel-ar
 
 struct PoolArgs {
     const void *in;      // parents  [B*F][in_h][in_w][C]
-    void *out;           // children [B*F*ky*kx][out_h][out_w][C]
+    void *out;           // children [B*F*sy*sx][out_h][out_w][C]
     int F, Qx;           // parents per image; per row of the fragment grid
     int in_h, in_w;
     int out_h, out_w;
     int C, ky, kx;       // pool rows, columns
-    int n_children;      // B * F * ky * kx
+    int sy, sx;          // step between windows, rows and columns (the paper's pools: ky, kx)
+    int n_children;      // B * F * sy * sx
     AxisTable ext;       // true sizes of the parents
 };
 
@@ -157,7 +158,7 @@ std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int taps);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run);
-std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int C);
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
 }  // namespace fs

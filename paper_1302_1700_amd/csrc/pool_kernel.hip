@@ -6,7 +6,11 @@
 //   o_x + k*xbar <= x <= o_x + k*xbar + k - 1 and the same in y       (Eq. 5)
 // and the child's size is div(s - o, k) per axis (Eqs. 6-7), never below 0.
 // A rectangular k_y x k_x pool (Section 2: the square case generalizes
-// directly) has k_y * k_x children and the same rules per axis.
+// directly) has k_y * k_x children and the same rules per axis.  A pool whose
+// windows step by s instead of k (overlapping for s < k, with gaps for s > k;
+// the paper's pools have s = k) has s_y * s_x children, child pixel xbar
+// covering o_x + s*xbar .. o_x + s*xbar + k - 1, and holds
+// div(n - o - k + s, s) pixels of a parent of n.
 //
 // One workgroup writes one row of one child: the row is a contiguous run of
 // w_c * C elements, so stores are fully coalesced; the k parent rows it reads
@@ -40,28 +44,28 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
     using TO = typename std::conditional<BF, uint16_t, float>::type;
     using TI = typename std::conditional<IN_F32, float, TO>::type;
 
-    const int kk = a.ky * a.kx;
-    // blockIdx.x = ((b * F + f) * ky*kx + o) * out_h + ybar, grouped so that
+    const int kk = a.sy * a.sx;
+    // blockIdx.x = ((b * F + f) * sy*sx + o) * out_h + ybar, grouped so that
     // the children of a parent row band are neighbours:
     const int ybar = blockIdx.x % a.out_h;
     const int rest = blockIdx.x / a.out_h;
     const int o = rest % kk;
     const int p = rest / kk;            // parent batch index b * F + fy * Qx + fx
-    const int oy = o / a.kx, ox = o - (o / a.kx) * a.kx;
+    const int oy = o / a.sx, ox = o - (o / a.sx) * a.sx;
     const int b = p / a.F;
     const int rem = p - b * a.F;
     const int fy = rem / a.Qx, fx = rem - (rem / a.Qx) * a.Qx;
     const int hp = a.ext.y[fy], wp = a.ext.x[fx];
-    const int hc = hp >= oy ? (hp - oy) / a.ky : 0;
-    const int wc = wp >= ox ? (wp - ox) / a.kx : 0;
+    const int hc = hp - oy - a.ky >= 0 ? (hp - oy - a.ky) / a.sy + 1 : 0;
+    const int wc = wp - ox - a.kx >= 0 ? (wp - ox - a.kx) / a.sx + 1 : 0;
     if (ybar >= hc || wc <= 0) return;
 
-    // child batch index in the (fy * ky + oy, fx * kx + ox) grid (Qx * kx per row)
-    const int Qc = a.Qx * a.kx;
-    const size_t child = (size_t)b * a.F * kk + (size_t)(fy * a.ky + oy) * Qc + (fx * a.kx + ox);
+    // child batch index in the (fy * sy + oy, fx * sx + ox) grid (Qx * sx per row)
+    const int Qc = a.Qx * a.sx;
+    const size_t child = (size_t)b * a.F * kk + (size_t)(fy * a.sy + oy) * Qc + (fx * a.sx + ox);
 
     const TI *src = reinterpret_cast<const TI *>(a.in) +
-                    ((size_t)p * a.in_h + (oy + a.ky * ybar)) * a.in_w * a.C;
+                    ((size_t)p * a.in_h + (oy + a.sy * ybar)) * a.in_w * a.C;
     TO *dst = reinterpret_cast<TO *>(a.out) + (child * a.out_h + ybar) * a.out_w * a.C;
     const size_t prow = (size_t)a.in_w * a.C;
 
@@ -70,7 +74,7 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
     for (int idx = threadIdx.x; idx < total; idx += 256) {
         const int xbar = idx / nv;
         const int cv = idx - xbar * nv;
-        const size_t base = (size_t)(ox + a.kx * xbar) * a.C + cv * V;
+        const size_t base = (size_t)(ox + a.sx * xbar) * a.C + cv * V;
         float m[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) m[e] = -INFINITY;
@@ -231,7 +235,7 @@ hipError_t go_rows(const PoolArgs &a, hipStream_t s)
 template <bool BF, bool IN_F32, int V>
 hipError_t go_k(const PoolArgs &a, int grid, hipStream_t s)
 {
-    if (a.ky == a.kx) {
+    if (a.ky == a.kx && a.sy == a.ky && a.sx == a.kx) {  // the paper's pools: stride = size
         if (a.ky == 2) return go_rows<2, BF, IN_F32, V>(a, s);
         if (a.ky == 3) return go_rows<3, BF, IN_F32, V>(a, s);
         if (a.ky == 4) return go_rows<4, BF, IN_F32, V>(a, s);
@@ -250,14 +254,14 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
     return (a.C % 8 == 0) ? go_k<true, false, 8>(a, grid, s) : go_k<true, false, 1>(a, grid, s);
 }
 
-std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int C)
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C)
 {
     // the instance launch_pool picks, as the profiler names it
     const bool bf = dtype == DT_BF16, bin = bf && in_f32;
     const int v = !bf ? (C % 4 == 0 ? 4 : 1) : (in_f32 ? 1 : (C % 8 == 0 ? 8 : 1));
     const char *t = bf ? "true" : "false", *ti = bin ? "true" : "false";
     char buf[64];
-    if (ky == kx && ky >= 2 && ky <= 4)
+    if (ky == kx && sy == ky && sx == kx && ky >= 2 && ky <= 4)
         snprintf(buf, sizeof buf, "pool_frag_rows<%d, %s, %s, %d>", ky, t, ti, v);
     else
         snprintf(buf, sizeof buf, "pool_frag<%s, %s, %d>", t, ti, v);

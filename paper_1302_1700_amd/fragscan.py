@@ -30,7 +30,8 @@ class FsError(RuntimeError):
 class fs_layer(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("k", ctypes.c_int32), ("c_in", ctypes.c_int32),
                 ("c_out", ctypes.c_int32), ("act", ctypes.c_int32),
-                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("k_x", ctypes.c_int32)]
+                ("weight", ctypes.c_void_p), ("bias", ctypes.c_void_p), ("k_x", ctypes.c_int32),
+                ("stride", ctypes.c_int32), ("stride_x", ctypes.c_int32)]
 
 
 class fs_net_info(ctypes.Structure):
@@ -149,8 +150,8 @@ class Net:
     """A net loaded into the library.
 
     layers : list of layer dicts (kind, k, c_in, c_out, act; optional kx, the
-             kernel's / pool's columns when they differ from its rows k),
-             see workloads.py
+             kernel's / pool's columns when they differ from its rows k;
+             pools: optional stride, stride_x), see workloads.py
     params : per layer (weight OIHW float32, bias float32) or None for pools
     in_channels, patch (0 = derive), dtype "f32" | "bf16".
     Created on the current HIP device; plan_only=True makes a host-only handle
@@ -165,6 +166,8 @@ class Net:
             arr[i].kind = KIND[L["kind"]]
             arr[i].k = int(L["k"])
             arr[i].k_x = int(L.get("kx") or 0)
+            arr[i].stride = int(L.get("stride") or 0)
+            arr[i].stride_x = int(L.get("stride_x") or 0)
             arr[i].c_in = int(L["c_in"])
             arr[i].c_out = int(L["c_out"])
             arr[i].act = ACT[L["act"]]

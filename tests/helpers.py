@@ -12,7 +12,8 @@ def _k(L):
 def _s(L):
     """(rows, columns) stride of a pool (its size unless given)."""
     ky, kx = _k(L)
-    return L.get("stride", ky), L.get("stride_x", kx)
+    sy = L.get("stride", ky)
+    return sy, L.get("stride_x", sy if "stride" in L else kx)
 
 
 def torch_patch_net(layers, params, crop):

@@ -47,7 +47,7 @@ def _check_tables(layers, H, W, c0=1):
     Sy = Sx = 1
     for L in layers:
         if L["kind"] == "pool":
-            Sy, Sx = Sy * ix.kyx(L)[0], Sx * ix.kyx(L)[1]
+            Sy, Sx = Sy * ix.syx(L)[0], Sx * ix.syx(L)[1]
     assert (net.info["stride"], net.info["stride_x"]) == (Sy, Sx)
     assert net.info["n_fragments"] == ix.n_fragments(layers)
     # reassembly index, every output pixel
@@ -576,3 +576,55 @@ def test_plan_cache(monkeypatch):
         t.join()
     assert not errors, errors[:3]
     net.close()
+
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_tables_random_stride_nets(seed):
+    """Pools whose stride differs from their size (overlapping or gapped):
+    the library's sizes, fragment table and reassembly index agree with the
+    oracle's corner tracking bit for bit."""
+    rng = np.random.default_rng(4800 + seed)
+    layers, (h0, w0), c0 = wl.random_stride_net(rng)
+    H = h0 + int(rng.integers(0, 25))
+    W = w0 + int(rng.integers(0, 25))
+    _check_tables(layers, H, W, c0)
+
+
+def test_stride_rules():
+    """Strides: a pool with stride 0 is the paper's pool; a column stride of
+    0 follows the row stride; a stride that does not tile the map, a negative
+    stride and a strided convolution are refused."""
+    base = [wl.conv(2, 1, 2), wl.pool(3, 2, stride=2), wl.fc(2, 2, 2, "softmax")]
+    assert ix.patch_size(base) == 6  # fc 2 -> pool (2-1)*2+3 = 5 -> conv 6
+    net = _plan_net(base)
+    assert (net.patch, net.info["stride"], net.info["n_fragments"]) == (6, 2, 4)
+    net.close()
+    only_rows = [dict(L) for L in base]
+    del only_rows[1]["stride_x"]  # stride_x follows stride
+    net = _plan_net(only_rows)
+    assert (net.patch, net.patch_x, net.info["stride_x"]) == (6, 6, 2)
+    net.close()
+    # stride 3 on a 3x3 pool is the plain pool
+    plain = _plan_net([wl.conv(2, 1, 2), wl.pool(3, 2), wl.fc(2, 2, 2, "softmax")])
+    same = _plan_net([wl.conv(2, 1, 2), wl.pool(3, 2, stride=3), wl.fc(2, 2, 2, "softmax")])
+    assert plain.launches(1, 40, 37) == same.launches(1, 40, 37)
+    assert np.array_equal(plain.reassembly_index(40, 37), same.reassembly_index(40, 37))
+    plain.close()
+    same.close()
+    # patch 7: the 6 x 6 map after the conv does not end a stride-2 3x3 window
+    params = wl.make_weights(base, 0, 0.1)
+    assert _status(base, params, patch=7) == fsb.FS_ERR_SHAPE
+    bad = [dict(L) for L in base]
+    bad[1]["stride"] = -1
+    assert _status(bad, params) == fsb.FS_ERR_INVALID_ARG
+    bad = [dict(L) for L in base]
+    bad[0]["stride"] = 2
+    assert _status(bad, params) == fsb.FS_ERR_UNSUPPORTED
+    # a strided pool after a convolution is not fused into it
+    layers = [wl.conv(3, 3, 32), wl.pool(3, 32, stride=2), wl.conv(2, 32, 16), wl.pool(2, 16),
+              wl.fc(2, 16, 8), wl.fc(1, 8, 2, "softmax")]
+    net = _plan_net(layers, c0=3)
+    names = [L["name"] for L in net.launches(1, 120, 111)]
+    net.close()
+    assert not names[0].endswith("+pool") and names[1].startswith("pool_frag<"), names

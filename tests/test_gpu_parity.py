@@ -903,3 +903,95 @@ def test_max_fragments_per_axis(fsb, dt):
     got = _scan(fsb, layers, params, img, 1, dtype=dt)
     ref = oracle.patch_forward(layers, params, img, w0)
     assert np.abs(got - ref).max() <= TOL[dt]
+
+
+# ---- pools whose stride differs from their size (overlapping, gapped) -------
+
+@pytest.mark.parametrize("seed", [9302, 9304, 9310, 9313, 9315, 9318, 9321, 9326])
+def test_stride_random_nets(fsb, seed):
+    """Random stacks whose pools overlap (stride below the size) or leave
+    gaps (stride above it), square and rectangular: the full map against
+    the CPU fragment method and sampled windows against the per-window
+    oracle; odd seeds in bf16."""
+    rng = np.random.default_rng(seed)
+    layers, (h0, w0), c0 = wl.random_stride_net(rng)
+    dt = "bf16" if seed % 2 else "f32"
+    B = 1 + seed % 2
+    H, W = h0 + int(rng.integers(0, 40)), w0 + int(rng.integers(0, 40))
+    params = wl.make_weights(layers, seed + 100, 0.4)
+    img = wl.make_image(seed + 200, B, H, W, c0)
+    print("stride net", seed, [(L["kind"], ix.kyx(L), ix.syx(L) if L["kind"] == "pool" else None)
+                               for L in layers], (B, H, W), dt, flush=True)
+    got = _scan(fsb, layers, params, img, c0, 0, dt)
+    ref = oracle.frag_cpu.frag_scan(layers, params, img, (h0, w0))
+    assert got.shape == ref.shape
+    assert np.abs(got - ref).max() <= TOL[dt]
+    pts = _sample_patches(layers, B, H, W, 24, seed)
+    ref_p = oracle.patch_forward(layers, params, img, (h0, w0), pts)
+    assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref_p).max() <= TOL[dt]
+
+
+def _stride_mfma_net():
+    """Matrix-core channel counts with an overlapping 3 x 3 pool of stride 2
+    and a gapped 2 x 2 pool of stride 3; window 15 x 15, 36 final
+    fragments."""
+    layers = [wl.conv(3, 3, 32), wl.pool(3, 32, stride=2), wl.conv(2, 32, 48), wl.pool(2, 48, stride=3),
+              wl.fc(2, 48, 24), wl.fc(1, 24, 3, "softmax")]
+    assert ix.patch_hw(layers) == (15, 15) and ix.n_fragments(layers) == 36
+    return layers
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_stride_mfma_net(fsb, dt):
+    """Vector-path layers around strided pools (not fused into the
+    convolutions), the head fused into the last layer, two images; the full
+    map against the CPU fragment method, and the tiled scan bit for bit."""
+    layers = _stride_mfma_net()
+    params = wl.make_weights(layers, 81, 0.15)
+    img = wl.make_image(82, 2, 15 + 93, 15 + 118, 3)
+    got = _scan(fsb, layers, params, img, 3, 0, dt)
+    ref = oracle.frag_cpu.frag_scan(layers, params, img, 15)
+    assert np.abs(got - ref).max() <= TOL[dt]
+    net = fsb.Net(layers, params, 3, 0, dt)
+    x = torch.from_numpy(img).cuda()
+    out = torch.full((2, 94, 119, 3), float("nan"), device="cuda")
+    net.scan_tiled(x, (37, 50), out=out)
+    torch.cuda.synchronize()
+    net.close()
+    assert np.array_equal(out.cpu().numpy().astype(np.float64), got)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stride_reassembly_bit_exact(fsb, dtype):
+    """Position-encoding probe with overlapping and gapped pools: one-tap
+    convolutions and an image growing along y and x make every output an
+    exact copy of one image pixel (the last of each pooling window), in both
+    precisions."""
+    c = 3
+    layers, params = [], []
+    for kind, k, st in [("conv", 2, None), ("pool", 3, 2), ("conv", 2, None), ("pool", 2, 3), ("pool", 2, 1)]:
+        if kind == "pool":
+            layers.append(wl.pool(k, c, stride=st))
+            params.append(None)
+        else:
+            layers.append(wl.conv(k, c, c, "none"))
+            wt = np.zeros((c, c, k, k), np.float32)
+            for i in range(c):
+                wt[i, i, k - 1, 0] = 1.0
+            params.append((wt, np.zeros(c, np.float32)))
+    layers.append(wl.fc(2, c, c, "none"))
+    wt = np.zeros((c, c, 2, 2), np.float32)
+    for i in range(c):
+        wt[i, i, 0, 1] = 1.0
+    params.append((wt, np.zeros(c, np.float32)))
+    h0, w0 = ix.patch_hw(layers)
+    B, H, W = 2, h0 + 77, w0 + 64
+    yy, xx = np.meshgrid(np.arange(H), np.arange(W), indexing="ij")
+    img = np.zeros((B, H, W, c), np.float32)
+    for b in range(B):
+        img[b, :, :, 0] = yy % 128 + 64 * b
+        img[b, :, :, 1] = xx % 128
+        img[b, :, :, 2] = (yy // 128) * 16 + xx // 128 + 128 * b
+    got = _scan(fsb, layers, params, img, c, dtype=dtype)
+    ref = oracle.patch_forward(layers, params, img, (h0, w0))
+    assert np.array_equal(got, ref)
