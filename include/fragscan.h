@@ -154,7 +154,7 @@ typedef struct {
     double bytes;         /* minimum bytes (see fs_plan_info) */
     int32_t grid;         /* workgroups launched */
     int32_t block;        /* threads per workgroup */
-    char name[64];
+    char name[96];
     int32_t lds_bytes;    /* dynamic LDS per workgroup */
     int32_t per_cu;       /* workgroups resident per CU (registers and LDS;
                              0 when unknown, e.g. plan-only nets) */

@@ -687,12 +687,23 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             a.sy = l.sy;
             a.sx = l.sx;
             a.n_children = B * F * l.sy * l.sx;
+            // Row-band kernel: 8 filter rows per thread, or 4 where that
+            // still leaves at least 32 workgroups per CU (more threads in
+            // flight: N4's pools on 8 x 1024^2 images 2-5% faster; on one
+            // 512^2 image, 2-5% slower).  FRAGSCAN_POOL_ROWS=4/8 forces it.
+            {
+                const int vpp = (net->dtype == DT_F32 && g.C % 4 == 0) ? g.C / 4
+                                : (net->dtype == DT_BF16 && !g.is_image && g.C % 8 == 0) ? g.C / 8 : g.C;
+                const long long wg8 = (long long)B * F * ((g.hmax + 7) / 8) * (((long long)g.wmax * vpp + 255) / 256);
+                a.rows = wg8 >= 32LL * (net->ncu > 0 ? net->ncu : 256) ? 4 : 8;
+                if (const char *e = getenv("FRAGSCAN_POOL_ROWS")) a.rows = atoi(e) == 4 ? 4 : 8;
+            }
             fill_axis(a.ext, g);
             L.gx = (int)std::min<long long>((long long)B * F * l.sy * l.sx * a.out_h, kMaxGrid);
             L.frags = B * F * l.sy * l.sx;
             L.out_pixels = (long long)B * true_pixels(o);
             L.bytes = (double)B * in_pix * g.C * (g.is_image ? 4 : es) + (double)L.out_pixels * o.C * es;
-            L.name = pool_kernel_name(net->dtype, g.is_image, ky, kx, l.sy, l.sx, g.C);
+            L.name = pool_kernel_name(net->dtype, g.is_image, ky, kx, l.sy, l.sx, g.C, a.rows);
         } else {  // conv or fc as convolution
             const int ky = l.k, kx = l.kx;
             o.Qy = g.Qy;
@@ -972,7 +983,8 @@ std::string planner_env()
 {
     static const char *const vars[] = {"FRAGSCAN_TILE", "FRAGSCAN_DIRECT", "FRAGSCAN_POOL_FUSE",
                                        "FRAGSCAN_NO_FUSED_HEAD", "FRAGSCAN_RUN", "FRAGSCAN_ROWTILES",
-                                       "FRAGSCAN_STORE", "FRAGSCAN_LDS_PAD", "FRAGSCAN_WIDE"};
+                                       "FRAGSCAN_STORE", "FRAGSCAN_LDS_PAD", "FRAGSCAN_WIDE",
+                                       "FRAGSCAN_POOL_ROWS"};
     std::string sig;
     for (const char *v : vars) {
         const char *e = getenv(v);

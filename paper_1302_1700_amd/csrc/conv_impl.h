@@ -47,6 +47,7 @@
 #include "fs_internal.h"
 
 #include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 namespace fs {
@@ -1143,11 +1144,20 @@ hipError_t launch_one(const ConvArgs &a, int gx, int gy, hipStream_t s)
 {
     auto kern = conv_frag_mfma<MB, NB, WN, WK, BF, IN_F32, VEC, RUN>;
     if (a.lds_bytes > 65536) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, a.lds_bytes);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();  // do not leave it to be reported by a later launch
-            return e;
+        // the instance may take up to a whole CU's LDS: set once per device
+        // (a runtime call per launch cost tens of microseconds of host time)
+        static std::atomic<uint64_t> done{0};
+        int dev = 0;
+        (void)hipGetDevice(&dev);
+        const uint64_t bit = 1ull << (dev & 63);
+        if (!(done.load(std::memory_order_acquire) & bit)) {
+            hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kMaxLdsBytes);
+            if (e != hipSuccess) {
+                (void)hipGetLastError();  // do not leave it to be reported by a later launch
+                return e;
+            }
+            done.fetch_or(bit, std::memory_order_acq_rel);
         }
     }
     hipLaunchKernelGGL(kern, dim3(gx, gy), dim3(256), a.lds_bytes, s, a);

@@ -104,6 +104,7 @@ struct PoolArgs {
     int C, ky, kx;       // pool rows, columns
     int sy, sx;          // step between windows, rows and columns (the paper's pools: ky, kx)
     int n_children;      // B * F * sy * sx
+    int rows;            // row-band kernel: filter rows per thread (4 or 8)
     AxisTable ext;       // true sizes of the parents
 };
 
@@ -158,7 +159,7 @@ std::string conv_direct_kernel_name(int dtype, bool in_f32, int cin, int taps);
 
 // Kernel names as the profiler reports them (for measurement reports).
 std::string conv_kernel_name(int dtype, bool in_f32, int mb, int nb, int wn, int wk, bool vec, bool run);
-std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C);
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C, int rows);
 const char *head_kernel_name(int dtype, bool in_f32, bool has_fc);
 
 }  // namespace fs

@@ -21,7 +21,9 @@
 // stored back unchanged.
 #include "fs_internal.h"
 
+#include <algorithm>
 #include <cstdio>
+#include <cstdlib>
 #include <type_traits>
 
 namespace fs {
@@ -127,8 +129,8 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
 // So a parent element is fetched from memory once (its k horizontal
 // neighbours share it through the cache) and every child row is written with
 // contiguous stores; the k^2 siblings no longer re-read the parent.
-template <int K, bool BF, bool IN_F32, int V>
-__global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nbands, int nchunks)
+template <int K, int RB, bool BF, bool IN_F32, int V>
+__global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int nbands, int nchunks)
 {
     using TO = typename std::conditional<BF, uint16_t, float>::type;
     using TI = typename std::conditional<IN_F32, float, TO>::type;
@@ -144,8 +146,8 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
     const int nv = a.C / V;
     const int pi = chunk * 256 + threadIdx.x;
     const int x = pi / nv, cv = pi - (pi / nv) * nv;
-    const int y0 = band * rb;
-    const int yend = min(y0 + rb, hp - K + 1);  // M rows [y0, yend)
+    const int y0 = band * RB;
+    const int yend = min(y0 + RB, hp - K + 1);  // M rows [y0, yend)
     if (x > wp - K || y0 >= yend) return;
 
     const TI *src = reinterpret_cast<const TI *>(a.in) + (size_t)p * a.in_h * a.in_w * a.C + (size_t)x * a.C + cv * V;
@@ -154,49 +156,60 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
     const size_t cbase = (size_t)b * a.F * K * K;
     TO *out = reinterpret_cast<TO *>(a.out);
 
-    auto hmax = [&](int row, float (&h)[V]) {
-        const TI *r = src + (size_t)row * prow;
+    // The RB + K - 1 parent rows this thread reads, every load issued before
+    // any maximum is taken (rows past the band's last are clamped to the
+    // fragment's last row: in bounds, and unused), so a thread has all its
+    // loads in flight at once.
+    u4 raw[RB + K - 1][K];
+    float sc[RB + K - 1][K];
 #pragma unroll
-        for (int e = 0; e < V; ++e) h[e] = -INFINITY;
+    for (int r = 0; r < RB + K - 1; ++r) {
+        const TI *row = src + (size_t)min(y0 + r, hp - 1) * prow;
 #pragma unroll
         for (int j = 0; j < K; ++j) {
-            const TI *s = r + (size_t)j * a.C;
             if constexpr (V == 1) {
-                float v;
-                if constexpr (!BF || IN_F32) v = s[0]; else v = bf2f(s[0]);
-                h[0] = fmaxf(h[0], v);
+                if constexpr (!BF || IN_F32)
+                    sc[r][j] = row[(size_t)j * a.C];
+                else
+                    sc[r][j] = bf2f(row[(size_t)j * a.C]);
             } else {
-                u4 raw = *reinterpret_cast<const u4 *>(s);
-                if constexpr (BF) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        h[2 * e] = fmaxf(h[2 * e], bf2f((uint16_t)(raw[e] & 0xffffu)));
-                        h[2 * e + 1] = fmaxf(h[2 * e + 1], bf2f((uint16_t)(raw[e] >> 16)));
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) h[e] = fmaxf(h[e], __uint_as_float(raw[e]));
-                }
+                raw[r][j] = *reinterpret_cast<const u4 *>(row + (size_t)j * a.C);
             }
         }
-    };
-    float win[K][V];  // horizontal maxima of the last K parent rows (ring by shifting)
+    }
+    // horizontal maxima of each row, then the K-row maxima
+    float h[RB + K - 1][V];
 #pragma unroll
-    for (int i = 0; i < K - 1; ++i) hmax(y0 + i, win[i + 1]);
+    for (int r = 0; r < RB + K - 1; ++r) {
+#pragma unroll
+        for (int e = 0; e < V; ++e) h[r][e] = -INFINITY;
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+            if constexpr (V == 1) {
+                h[r][0] = fmaxf(h[r][0], sc[r][j]);
+            } else if constexpr (BF) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    h[r][2 * e] = fmaxf(h[r][2 * e], bf2f((uint16_t)(raw[r][j][e] & 0xffffu)));
+                    h[r][2 * e + 1] = fmaxf(h[r][2 * e + 1], bf2f((uint16_t)(raw[r][j][e] >> 16)));
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) h[r][e] = fmaxf(h[r][e], __uint_as_float(raw[r][j][e]));
+            }
+        }
+    }
     const int ox = x % K, xbar = x / K;
-#pragma unroll 8
-    for (int y = y0; y < yend; ++y) {
 #pragma unroll
-        for (int i = 0; i < K - 1; ++i)
-#pragma unroll
-            for (int e = 0; e < V; ++e) win[i][e] = win[i + 1][e];
-        hmax(y + K - 1, win[K - 1]);
+    for (int i = 0; i < RB; ++i) {
+        const int y = y0 + i;
+        if (y >= yend) break;
         float m[V];
 #pragma unroll
         for (int e = 0; e < V; ++e) {
-            m[e] = win[0][e];
+            m[e] = h[i][e];
 #pragma unroll
-            for (int i = 1; i < K; ++i) m[e] = fmaxf(m[e], win[i][e]);
+            for (int t = 1; t < K; ++t) m[e] = fmaxf(m[e], h[i + t][e]);
         }
         const int oy = y % K, ybar = y / K;
         const size_t child = cbase + (size_t)(fy * K + oy) * Qc + (fx * K + ox);
@@ -218,18 +231,25 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int rb, int nb
     }
 }
 
-template <int K, bool BF, bool IN_F32, int V>
-hipError_t go_rows(const PoolArgs &a, hipStream_t s)
+template <int K, int RB, bool BF, bool IN_F32, int V>
+hipError_t go_rows_rb(const PoolArgs &a, hipStream_t s)
 {
     const int nv = a.C / V;
-    const int rb = 8;
-    const int nbands = (a.in_h + rb - 1) / rb;
+    const int nbands = (a.in_h + RB - 1) / RB;
     const int nchunks = (a.in_w * nv + 255) / 256;
     const long long grid = (long long)a.n_children / (K * K) * nbands * nchunks;
     if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((pool_frag_rows<K, BF, IN_F32, V>), dim3((unsigned)grid), dim3(256), 0, s, a, rb, nbands,
+    hipLaunchKernelGGL((pool_frag_rows<K, RB, BF, IN_F32, V>), dim3((unsigned)grid), dim3(256), 0, s, a, nbands,
                        nchunks);
     return hipGetLastError();
+}
+
+// Filter rows per thread: the planner's choice (PoolArgs::rows).
+template <int K, bool BF, bool IN_F32, int V>
+hipError_t go_rows(const PoolArgs &a, hipStream_t s)
+{
+    if (a.rows == 4) return go_rows_rb<K, 4, BF, IN_F32, V>(a, s);
+    return go_rows_rb<K, 8, BF, IN_F32, V>(a, s);
 }
 
 template <bool BF, bool IN_F32, int V>
@@ -254,7 +274,7 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
     return (a.C % 8 == 0) ? go_k<true, false, 8>(a, grid, s) : go_k<true, false, 1>(a, grid, s);
 }
 
-std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C)
+std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int sx, int C, int rows)
 {
     // the instance launch_pool picks, as the profiler names it
     const bool bf = dtype == DT_BF16, bin = bf && in_f32;
@@ -262,7 +282,7 @@ std::string pool_kernel_name(int dtype, bool in_f32, int ky, int kx, int sy, int
     const char *t = bf ? "true" : "false", *ti = bin ? "true" : "false";
     char buf[64];
     if (ky == kx && sy == ky && sx == kx && ky >= 2 && ky <= 4)
-        snprintf(buf, sizeof buf, "pool_frag_rows<%d, %s, %s, %d>", ky, t, ti, v);
+        snprintf(buf, sizeof buf, "pool_frag_rows<%d, %d, %s, %s, %d>", ky, rows == 4 ? 4 : 8, t, ti, v);
     else
         snprintf(buf, sizeof buf, "pool_frag<%s, %s, %d>", t, ti, v);
     return buf;

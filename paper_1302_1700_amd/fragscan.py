@@ -50,7 +50,7 @@ class fs_launch_info(ctypes.Structure):
     _fields_ = [("layer", ctypes.c_int32), ("n_layers", ctypes.c_int32), ("kind", ctypes.c_int32),
                 ("fragments", ctypes.c_int32), ("out_pixels", ctypes.c_int64),
                 ("flops", ctypes.c_double), ("bytes", ctypes.c_double),
-                ("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("name", ctypes.c_char * 64),
+                ("grid", ctypes.c_int32), ("block", ctypes.c_int32), ("name", ctypes.c_char * 96),
                 ("lds_bytes", ctypes.c_int32), ("per_cu", ctypes.c_int32)]
 
 

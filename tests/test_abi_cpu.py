@@ -628,3 +628,5 @@ def test_stride_rules():
     names = [L["name"] for L in net.launches(1, 120, 111)]
     net.close()
     assert not names[0].endswith("+pool") and names[1].startswith("pool_frag<"), names
+
+

@@ -995,3 +995,24 @@ def test_stride_reassembly_bit_exact(fsb, dtype):
     got = _scan(fsb, layers, params, img, c, dtype=dtype)
     ref = oracle.patch_forward(layers, params, img, (h0, w0))
     assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("wid", [2, 5])
+def test_pool_rows_per_thread_bit_exact(fsb, monkeypatch, wid):
+    """The row-band pool kernel with 4 or 8 filter rows per thread gives the
+    same values bit for bit (pools not fused, so the separate kernel runs;
+    2 x 2 and 3 x 3 pools, f32 and bf16, two images)."""
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid, batch=2, height=171, width=160)
+    monkeypatch.setenv("FRAGSCAN_POOL_FUSE", "0")
+    outs = {}
+    for rows in ("4", "8"):
+        monkeypatch.setenv("FRAGSCAN_POOL_ROWS", rows)
+        net = fsb.Net(w.layers, params, w.channels, 0, w.dtype)
+        names = [L["name"] for L in net.launches(2, 171, 160) if L["kind"] == 1]
+        net.close()
+        assert names and all(n.startswith("pool_frag_rows<") and (", %s," % rows) in n for n in names), names
+        outs[rows] = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    assert np.array_equal(outs["4"], outs["8"])
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    assert np.abs(outs["4"] - ref).max() <= TOL[w.dtype]
