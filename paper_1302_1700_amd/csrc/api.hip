@@ -862,6 +862,10 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 a.Sx = net->Sx;
                 for (int f = 0; f < o.Qy; ++f) a.base_y[f] = (uint16_t)axis_base(net->pool_k, net->S, f);
                 for (int f = 0; f < o.Qx; ++f) a.base_x[f] = (uint16_t)axis_base(net->pool_kx, net->Sx, f);
+                // Fragment tiles in x-sibling order (ConvArgs::xsib):
+                // FRAGSCAN_XSIB=0 keeps fragment order.
+                const char *xs = getenv("FRAGSCAN_XSIB");
+                a.xsib = !a.run && !(xs && xs[0] == '0');
                 L.dst = 2;
                 L.n_layers = 2;
                 const long long npix = (long long)B * P.ny * P.nx;
@@ -984,7 +988,7 @@ std::string planner_env()
     static const char *const vars[] = {"FRAGSCAN_TILE", "FRAGSCAN_DIRECT", "FRAGSCAN_POOL_FUSE",
                                        "FRAGSCAN_NO_FUSED_HEAD", "FRAGSCAN_RUN", "FRAGSCAN_ROWTILES",
                                        "FRAGSCAN_STORE", "FRAGSCAN_LDS_PAD", "FRAGSCAN_WIDE",
-                                       "FRAGSCAN_POOL_ROWS"};
+                                       "FRAGSCAN_POOL_ROWS", "FRAGSCAN_XSIB"};
     std::string sig;
     for (const char *v : vars) {
         const char *e = getenv(v);

@@ -343,6 +343,11 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
     int bid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     const int nunit = RUN ? a.nfrag / a.F : a.nfrag;  // images (run tiles) or fragments
     if (bid >= nunit * a.nbands * a.tiles_per_band) return;
+    int sib = 0;  // xsib: the fragment's column index
+    if (!RUN && a.xsib) {
+        sib = bid % a.Qx;
+        bid /= a.Qx;
+    }
     const int t = bid % a.tiles_per_band;
     bid /= a.tiles_per_band;
     const int band = bid % a.nbands;
@@ -397,10 +402,17 @@ __global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
         hin = a.ext.y[fy];
         win = a.ext.x[fx];
     } else {
-        q = bid / a.nbands;
-        const int rem = q % a.F;
-        fy = rem / a.Qx;
-        fx = rem - (rem / a.Qx) * a.Qx;
+        if (a.xsib) {
+            const int row = bid / a.nbands;  // b * Qy + fy
+            fy = row % a.Qy;
+            fx = sib;
+            q = (row / a.Qy) * a.F + fy * a.Qx + fx;
+        } else {
+            q = bid / a.nbands;
+            const int rem = q % a.F;
+            fy = rem / a.Qx;
+            fx = rem - (rem / a.Qx) * a.Qx;
+        }
         hin = a.ext.y[fy];
         win = a.ext.x[fx];
         const int hout = hin - a.ky + 1, wout = win - a.kx + 1;

@@ -81,6 +81,12 @@ struct ConvArgs {
     // activation, and the reassembly are applied in the epilogue, which then
     // writes the dense output map instead of `out`'s fragment batch.
     int head_ncls, head_act;
+    // xsib = 1 (fused head, fragment tiles): tiles are numbered with the
+    // fragment's column index fx fastest, so the Qx fragments of one row of
+    // the grid, whose outputs interleave in the map's columns (column
+    // base_x[fx] + Sx * x), run the same tile side by side and fill the map's
+    // memory lines together.
+    int xsib;
     const float *head_w;  // [max(head_ncls, kMaxFusedClasses)][nbt * 16], columns in (block, row) order, zero rows past head_ncls
     // bf16 nets whose tile pairs channel blocks: the same weights as the row
     // operand of a 16x16x32 bf16 product, [nbt / 2][64 lanes][8 bf16], lane l

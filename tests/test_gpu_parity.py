@@ -364,6 +364,30 @@ def test_unfused_head_paths(fsb, monkeypatch):
         assert np.abs(got - ref).max() <= TOL[dt], dt
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_head_sibling_order(fsb, monkeypatch, dt):
+    """Fused-head tiles numbered with the fragment column fastest (the x
+    siblings, whose outputs interleave in the map's columns, side by side) or
+    in fragment order: the same map bit for bit, and the oracle's values.
+    The rectangular net (2 x 3 and 3 x 2 pools: 6 x 6 final fragments) on
+    ragged fragments, two images; N4 (16 x 16 final fragments) with the FC
+    tile the planner picks (bf16 N4 runs the separate head kernel)."""
+    cases = [(_rect_mfma_net(), 65, (2, 16 + 97, 25 + 131, 3), (16, 25), 3)]
+    w = wl.WORKLOADS[2]
+    cases.append((w.layers, 67, (1, w.patch + 83, w.patch + 121, 1), w.patch, 1))
+    for layers, seed, shape, patch, c0 in cases:
+        params = wl.make_weights(layers, seed, 0.15)
+        img = wl.make_image(seed + 1, *shape)
+        got = {}
+        for xs in ("1", "0"):
+            monkeypatch.setenv("FRAGSCAN_XSIB", xs)
+            print("head sibling order", dt, shape, xs, flush=True)
+            got[xs] = _scan(fsb, layers, params, img, c0, 0, dt)
+        assert np.array_equal(got["1"], got["0"])
+        ref = oracle.frag_cpu.frag_scan(layers, params, img, patch)
+        assert np.abs(got["1"] - ref).max() <= TOL[dt]
+
+
 @pytest.mark.parametrize("tile", ["2:4,3,1,16,2;4:8,3,1,16,4;6:4,3,1,0,2;8:4,7,2,0,2",
                                   "2:8,3,1,0,4;4:4,3,1,0,2;8:2,13,1,0,2"])
 def test_split_k_tiles(fsb, monkeypatch, tile):
