@@ -324,9 +324,13 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
 }
 
 // RUN: run tiles (ConvArgs::run = 1, no fused pool); the other instances
-// take one band of one fragment per tile sequence.
+// take one band of one fragment per tile sequence.  Float32 tiles of one
+// channel block and up to four pixel blocks (16-channel layers, whose
+// launches wait on memory) are compiled for six workgroups per CU (at most
+// 80 registers: six waves per SIMD instead of five; 4-5% faster on the
+// 2x2 16 -> 16 + pool layers; larger tiles would spill).
 template <int MB, int NB, int WN, int WK, bool BF, bool IN_F32, bool VEC, bool RUN>
-__global__ __launch_bounds__(256) void conv_frag_mfma(ConvArgs a)
+__global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv_frag_mfma(ConvArgs a)
 {
     using TC = typename Elem<BF>::T;                                // LDS / operand element
     using TI = typename std::conditional<IN_F32, float, TC>::type;  // global input element
