@@ -739,6 +739,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
             a.act = (li == nl - 1) ? ACT_NONE : l.act;
             a.ksteps = l.ksteps;
             a.nbt = l.nbt;
+            a.nbu = (l.cout + 15) / 16;
             fill_axis(a.ext, g);
             const bool fused_here = fuse && li == body - 1;
             // Small-K layers with one 16-channel output block reuse each
@@ -866,6 +867,11 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
                 // FRAGSCAN_XSIB=0 keeps fragment order.
                 const char *xs = getenv("FRAGSCAN_XSIB");
                 a.xsib = !a.run && !(xs && xs[0] == '0');
+                // Channel halves swapped in alternate workgroups where the
+                // second half ends in padding (ConvArgs::swapn);
+                // FRAGSCAN_SWAP=0 keeps them in place.
+                const char *sw = getenv("FRAGSCAN_SWAP");
+                a.swapn = a.nbu < a.nbt && !(sw && sw[0] == '0');
                 L.dst = 2;
                 L.n_layers = 2;
                 const long long npix = (long long)B * P.ny * P.nx;
@@ -988,7 +994,8 @@ std::string planner_env()
     static const char *const vars[] = {"FRAGSCAN_TILE", "FRAGSCAN_DIRECT", "FRAGSCAN_POOL_FUSE",
                                        "FRAGSCAN_NO_FUSED_HEAD", "FRAGSCAN_RUN", "FRAGSCAN_ROWTILES",
                                        "FRAGSCAN_STORE", "FRAGSCAN_LDS_PAD", "FRAGSCAN_WIDE",
-                                       "FRAGSCAN_POOL_ROWS", "FRAGSCAN_XSIB"};
+                                       "FRAGSCAN_POOL_ROWS", "FRAGSCAN_XSIB",
+                                       "FRAGSCAN_SWAP"};
     std::string sig;
     for (const char *v : vars) {
         const char *e = getenv(v);

@@ -613,7 +613,16 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
     // addresses) is computed once per wave in scalar registers
     const int lane = threadIdx.x & 63, wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wk = wv / WMN, wmn = wv - (wv / WMN) * WMN;
-    const int wm = wmn / WN, wn = wmn - (wmn / WN) * WN;
+    const int wm = wmn / WN, wn_raw = wmn - (wmn / WN) * WN;
+    // Float32 layers whose two wave columns own unequal work -- the second
+    // half ends in a padding block, whose products it skips (FC1 with the
+    // fused head: 200 outputs in 14 blocks) -- swap the halves between the
+    // columns in every other workgroup of an XCD's run (ConvArgs::swapn), so
+    // the two workgroups sharing a CU tend to load each SIMD with one heavy
+    // and one light wave (N4's FC1 on 8x1024^2 4% faster).  The channel sums
+    // and their order are those of the unswapped tile.
+    const bool swap = !BF && WN == 2 && WK == 1 && a.swapn && ((blockIdx.x / 8) & 1);
+    const int wn = swap ? 1 - wn_raw : wn_raw;
     const int lm = lane & 15, g = lane >> 4;
     const int nb0 = blockIdx.y * (WN * NB) + wn * NB;
 
@@ -667,12 +676,14 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
     const u4 *wp = reinterpret_cast<const u4 *>(a.w) + (size_t)nb0 * 64 + lane;
     const size_t wstep = (size_t)a.nbt * 64;  // u4 per K step
 
-    auto mma = [&](const u4(&av)[MB], const u4(&bv)[NB]) {
+    // nbac: the blocks whose products are taken (the rest are padding)
+    auto mma = [&](const u4(&av)[MB], const u4(&bv)[NB], auto nbac) {
+        constexpr int NBA = decltype(nbac)::value;
         if constexpr (BF) {
 #pragma unroll
             for (int i = 0; i < MB; ++i)
 #pragma unroll
-                for (int j = 0; j < NB; ++j)
+                for (int j = 0; j < NBA; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
                         __builtin_bit_cast(bf8, bv[j]), __builtin_bit_cast(bf8, av[i]), acc[i][j], 0, 0, 0);
         } else {
@@ -681,128 +692,139 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
 #pragma unroll
                 for (int i = 0; i < MB; ++i)
 #pragma unroll
-                    for (int j = 0; j < NB; ++j)
+                    for (int j = 0; j < NBA; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(
                             __uint_as_float(bv[j][e]), __uint_as_float(av[i][e]), acc[i][j], 0, 0, 0);
         }
     };
 
     if constexpr (VEC) {
-        // K step s covers tap (dy, dx) and channels cc*KSTEP ..; the three
-        // indices advance incrementally.  Weights are loaded PD steps ahead
-        // (a ring of PD register buffers, the loop unrolled by PD) and pixels
-        // one step ahead, so the products of a step never wait on the loads
-        // it needs.
-        // (four-deep rings measured slower for bf16: the extra registers
-        // cost a wave per SIMD)
-        constexpr int PD = 2;
-        static_assert(PD % 2 == 0, "the pixel double buffer needs an even unroll");
-        const int ncc = a.cin / KSTEP;
-        const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
-        const int nsteps = s_end - s_begin;
-        // (branch-free: a straight-line loop body lets the compiler wait only
-        // for the operands each product needs)
-        int cc = s_begin % ncc, dx = (s_begin / ncc) % a.kx, dy = (s_begin / ncc) / a.kx;
-        auto advance = [&](int) {
-            ++cc;
-            const int w1 = cc == ncc;
-            cc = w1 ? 0 : cc;
-            dx += w1;
-            const int w2 = dx == a.kx;
-            dx = w2 ? 0 : dx;
-            dy += w2;
-            return (dy * Cc + dx) * CS + cc * KSTEP;
-        };
-        u4 b[PD][NB], av[2][MB];
-        const u4 *wpk = wp + (size_t)s_begin * wstep;
-        const int off0 = (dy * Cc + dx) * CS + cc * KSTEP;
-        const int last = nsteps - 1;
-        // unconditional (clamped) so every path reaches the loop with the same
-        // loads in flight
-#pragma unroll
-        for (int t = 0; t < PD; ++t)
-#pragma unroll
-            for (int j = 0; j < NB; ++j) b[t][j] = wpk[(size_t)min(t, last) * wstep + j * 64];
-#pragma unroll
-        for (int i = 0; i < MB; ++i) av[0][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
-        // The prefetches are issued on every step (past the end they re-read
-        // the last step's weights and the window's first pixel), so every
-        // path through the loop has the same loads in flight and the waits
-        // before the products only cover the operands they use.
-        int off = off0;
-        int s = 0;
-        // Interleaved form (all tiles but the float32 one-block ones): the
-        // step's bookkeeping for later steps -- the tap and channel counters
-        // of step s + t + 2 and the weight pointer of step s + t + PD + 1 --
-        // runs between its products (two scalar instructions after each),
-        // where a lone wave per SIMD would otherwise leave the matrix core
-        // idle; only the loads stay between steps (N4's 48 -> 48 layers and
-        // FC1 2-5% faster, workload 5 2%; the float32 one-block tiles, held to
-        // 80 registers, would spill).
-        constexpr bool IL = BF || NB > 1;
-        int offn = IL ? advance(off) : 0;                       // step 1's offset
-        const u4 *wnx = wpk + (size_t)min(PD, last) * wstep;    // step PD's weights
-        int kw = min(PD, last);                                 // ... their step (clamped)
-        for (; s + PD <= nsteps; s += PD) {
-#pragma unroll
-            for (int t = 0; t < PD; ++t) {
-                // scheduling barriers keep each prefetch ahead of the products
-                // that do not need it (left alone, the compiler sinks the
-                // loads below them to share registers, exposing their latency)
-                if constexpr (IL) {
-                    const int offa = s + t + 1 < nsteps ? offn : off0;
-#pragma unroll
-                    for (int i = 0; i < MB; ++i)
-                        av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
-                    __builtin_amdgcn_sched_barrier(0);
-                    const u4 *wcur = wnx;  // step s + t + PD (clamped to the last)
-                    offn = advance(offn);
-                    const bool more = kw < last;
-                    wnx += more ? wstep : 0;
-                    kw += more;
-                    mma(av[t & 1], b[t]);
-#pragma unroll
-                    for (int k = 0; k < 16; ++k) {
-                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one product
-                        __builtin_amdgcn_sched_group_barrier(0x004, 2, 0);  // two scalar instructions
+        auto kwalk = [&](auto nbac) {
+            // K step s covers tap (dy, dx) and channels cc*KSTEP ..; the three
+            // indices advance incrementally.  Weights are loaded PD steps ahead
+            // (a ring of PD register buffers, the loop unrolled by PD) and pixels
+            // one step ahead, so the products of a step never wait on the loads
+            // it needs.
+            // (four-deep rings measured slower for bf16: the extra registers
+            // cost a wave per SIMD)
+            constexpr int PD = 2;
+            static_assert(PD % 2 == 0, "the pixel double buffer needs an even unroll");
+            const int ncc = a.cin / KSTEP;
+            const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
+            const int nsteps = s_end - s_begin;
+            // (branch-free: a straight-line loop body lets the compiler wait only
+            // for the operands each product needs)
+            int cc = s_begin % ncc, dx = (s_begin / ncc) % a.kx, dy = (s_begin / ncc) / a.kx;
+            auto advance = [&](int) {
+                ++cc;
+                const int w1 = cc == ncc;
+                cc = w1 ? 0 : cc;
+                dx += w1;
+                const int w2 = dx == a.kx;
+                dx = w2 ? 0 : dx;
+                dy += w2;
+                return (dy * Cc + dx) * CS + cc * KSTEP;
+            };
+            u4 b[PD][NB], av[2][MB];
+            const u4 *wpk = wp + (size_t)s_begin * wstep;
+            const int off0 = (dy * Cc + dx) * CS + cc * KSTEP;
+            const int last = nsteps - 1;
+            // unconditional (clamped) so every path reaches the loop with the same
+            // loads in flight
+    #pragma unroll
+            for (int t = 0; t < PD; ++t)
+    #pragma unroll
+                for (int j = 0; j < NB; ++j) b[t][j] = wpk[(size_t)min(t, last) * wstep + j * 64];
+    #pragma unroll
+            for (int i = 0; i < MB; ++i) av[0][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
+            // The prefetches are issued on every step (past the end they re-read
+            // the last step's weights and the window's first pixel), so every
+            // path through the loop has the same loads in flight and the waits
+            // before the products only cover the operands they use.
+            int off = off0;
+            int s = 0;
+            // Interleaved form (all tiles but the float32 one-block ones): the
+            // step's bookkeeping for later steps -- the tap and channel counters
+            // of step s + t + 2 and the weight pointer of step s + t + PD + 1 --
+            // runs between its products (two scalar instructions after each),
+            // where a lone wave per SIMD would otherwise leave the matrix core
+            // idle; only the loads stay between steps (N4's 48 -> 48 layers and
+            // FC1 2-5% faster, workload 5 2%; the float32 one-block tiles, held to
+            // 80 registers, would spill).
+            constexpr bool IL = BF || NB > 1;
+            int offn = IL ? advance(off) : 0;                       // step 1's offset
+            const u4 *wnx = wpk + (size_t)min(PD, last) * wstep;    // step PD's weights
+            int kw = min(PD, last);                                 // ... their step (clamped)
+            for (; s + PD <= nsteps; s += PD) {
+    #pragma unroll
+                for (int t = 0; t < PD; ++t) {
+                    // scheduling barriers keep each prefetch ahead of the products
+                    // that do not need it (left alone, the compiler sinks the
+                    // loads below them to share registers, exposing their latency)
+                    if constexpr (IL) {
+                        const int offa = s + t + 1 < nsteps ? offn : off0;
+    #pragma unroll
+                        for (int i = 0; i < MB; ++i)
+                            av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
+                        __builtin_amdgcn_sched_barrier(0);
+                        const u4 *wcur = wnx;  // step s + t + PD (clamped to the last)
+                        offn = advance(offn);
+                        const bool more = kw < last;
+                        wnx += more ? wstep : 0;
+                        kw += more;
+                        mma(av[t & 1], b[t], nbac);
+    #pragma unroll
+                        for (int k = 0; k < 16; ++k) {
+                            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one product
+                            __builtin_amdgcn_sched_group_barrier(0x004, 2, 0);  // two scalar instructions
+                        }
+                        __builtin_amdgcn_sched_group_barrier(0x008, MB * NB * (BF ? 1 : 4), 0);
+                        __builtin_amdgcn_sched_barrier(0);
+    #pragma unroll
+                        for (int j = 0; j < NB; ++j) b[t][j] = wcur[j * 64];
+                    } else {
+                        off = advance(off);  // step s + t + 1
+                        const int offa = s + t + 1 < nsteps ? off : off0;
+    #pragma unroll
+                        for (int i = 0; i < MB; ++i)
+                            av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
+                        __builtin_amdgcn_sched_barrier(0);
+                        mma(av[t & 1], b[t], nbac);
+                        __builtin_amdgcn_sched_barrier(0);
+                        const size_t wn2 = (size_t)min(s + t + PD, last) * wstep;
+    #pragma unroll
+                        for (int j = 0; j < NB; ++j) b[t][j] = wpk[wn2 + j * 64];
                     }
-                    __builtin_amdgcn_sched_group_barrier(0x008, MB * NB * (BF ? 1 : 4), 0);
-                    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                    for (int j = 0; j < NB; ++j) b[t][j] = wcur[j * 64];
-                } else {
-                    off = advance(off);  // step s + t + 1
-                    const int offa = s + t + 1 < nsteps ? off : off0;
-#pragma unroll
+                }
+            }
+            if constexpr (IL) off = offn;  // the tail advances from the next step's offset
+            // the last nsteps % PD steps (their weights are already loaded)
+    #pragma unroll
+            for (int t = 0; t + 1 < PD; ++t) {
+                if (s + t < nsteps) {
+                    int offa;
+                    if constexpr (IL) {
+                        offa = s + t + 1 < nsteps ? off : off0;
+                        off = advance(off);
+                    } else {
+                        off = advance(off);
+                        offa = s + t + 1 < nsteps ? off : off0;
+                    }
+    #pragma unroll
                     for (int i = 0; i < MB; ++i)
                         av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
-                    __builtin_amdgcn_sched_barrier(0);
-                    mma(av[t & 1], b[t]);
-                    __builtin_amdgcn_sched_barrier(0);
-                    const size_t wn2 = (size_t)min(s + t + PD, last) * wstep;
-#pragma unroll
-                    for (int j = 0; j < NB; ++j) b[t][j] = wpk[wn2 + j * 64];
+                    mma(av[t & 1], b[t], nbac);
                 }
             }
-        }
-        if constexpr (IL) off = offn;  // the tail advances from the next step's offset
-        // the last nsteps % PD steps (their weights are already loaded)
-#pragma unroll
-        for (int t = 0; t + 1 < PD; ++t) {
-            if (s + t < nsteps) {
-                int offa;
-                if constexpr (IL) {
-                    offa = s + t + 1 < nsteps ? off : off0;
-                    off = advance(off);
-                } else {
-                    off = advance(off);
-                    offa = s + t + 1 < nsteps ? off : off0;
-                }
-#pragma unroll
-                for (int i = 0; i < MB; ++i)
-                    av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
-                mma(av[t & 1], b[t]);
-            }
+        };
+        // a wave whose last block is padding (ConvArgs::nbu) skips its products
+        if constexpr (!BF && WN == 2 && WK == 1 && NB >= 2) {
+            if (nb0 + NB - 1 >= a.nbu)
+                kwalk(std::integral_constant<int, NB - 1>());
+            else
+                kwalk(std::integral_constant<int, NB>());
+        } else {
+            kwalk(std::integral_constant<int, NB>());
         }
     } else {
         const int s_begin = (a.ksteps * wk) / WK, s_end = (a.ksteps * (wk + 1)) / WK;
@@ -827,7 +849,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                 for (int e = 0; e < LPE; ++e) v[e] = offs[e] >= 0 ? win_lds[base + offs[e]] : TC(0);
                 __builtin_memcpy(&av[i], v, 16);
             }
-            mma(av, bcur);
+            mma(av, bcur, std::integral_constant<int, NB>());
             if (more) {
 #pragma unroll
                 for (int j = 0; j < NB; ++j) bcur[j] = bnxt[j];

@@ -51,6 +51,8 @@ struct ConvArgs {
     int ky, kx, cin, cout, act;  // kernel rows, columns
     int ksteps;           // K steps of the matrix-core loop
     int nbt;              // total 16-wide output-channel blocks
+    int nbu;              // blocks holding output channels (ceil(cout / 16)); past them the register tile pads
+    int swapn;            // 1: channel halves swapped between the two wave columns in alternate workgroups
     int band_w;           // output columns per band
     int nbands;           // bands per fragment
     int tiles_per_band;   // tiles per band (enough for the tallest fragment)

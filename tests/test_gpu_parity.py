@@ -388,6 +388,33 @@ def test_head_sibling_order(fsb, monkeypatch, dt):
         assert np.abs(got["1"] - ref).max() <= TOL[dt]
 
 
+def test_padding_block_and_half_swap(fsb, monkeypatch):
+    """N4's FC1 (200 outputs in 14 channel blocks) on the 7 x 2 register tile:
+    the wave whose half ends in the padding block skips that block's
+    products, and (head fused) alternate workgroups swap the halves between
+    the two wave columns.  With the swap and without it the map is the same
+    bit for bit, fused head or not, and the oracle's."""
+    w = wl.WORKLOADS[2]
+    H, W = w.patch + 83, w.patch + 121
+    params, img = wl.workload_inputs(2, batch=2, height=H, width=W)
+    ref = oracle.frag_cpu.frag_scan(w.layers, params, img, w.patch)
+    monkeypatch.setenv("FRAGSCAN_WIDE", "0")
+    for fused in ("1", "0"):
+        if fused == "0":
+            monkeypatch.setenv("FRAGSCAN_NO_FUSED_HEAD", "1")
+        got = {}
+        for sw in ("1", "0"):
+            monkeypatch.setenv("FRAGSCAN_SWAP", sw)
+            net = fsb.Net(w.layers, params, 1, 0, "f32")
+            names = [L["name"] for L in net.launches(2, H, W)]
+            net.close()
+            print("padding skip / half swap", fused, sw, names, flush=True)
+            assert any(n.startswith("conv_frag_mfma<4, 7, 2, 1,") for n in names), names
+            got[sw] = _scan(fsb, w.layers, params, img, 1)
+        assert np.array_equal(got["1"], got["0"]), fused
+        assert np.abs(got["1"] - ref).max() <= TOL["f32"], fused
+
+
 @pytest.mark.parametrize("tile", ["2:4,3,1,16,2;4:8,3,1,16,4;6:4,3,1,0,2;8:4,7,2,0,2",
                                   "2:8,3,1,0,4;4:4,3,1,0,2;8:2,13,1,0,2"])
 def test_split_k_tiles(fsb, monkeypatch, tile):
