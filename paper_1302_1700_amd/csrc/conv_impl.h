@@ -731,11 +731,11 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
             const int last = nsteps - 1;
             // unconditional (clamped) so every path reaches the loop with the same
             // loads in flight
-    #pragma unroll
+#pragma unroll
             for (int t = 0; t < PD; ++t)
-    #pragma unroll
+#pragma unroll
                 for (int j = 0; j < NB; ++j) b[t][j] = wpk[(size_t)min(t, last) * wstep + j * 64];
-    #pragma unroll
+#pragma unroll
             for (int i = 0; i < MB; ++i) av[0][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + off0);
             // The prefetches are issued on every step (past the end they re-read
             // the last step's weights and the window's first pixel), so every
@@ -756,14 +756,14 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
             const u4 *wnx = wpk + (size_t)min(PD, last) * wstep;    // step PD's weights
             int kw = min(PD, last);                                 // ... their step (clamped)
             for (; s + PD <= nsteps; s += PD) {
-    #pragma unroll
+#pragma unroll
                 for (int t = 0; t < PD; ++t) {
                     // scheduling barriers keep each prefetch ahead of the products
                     // that do not need it (left alone, the compiler sinks the
                     // loads below them to share registers, exposing their latency)
                     if constexpr (IL) {
                         const int offa = s + t + 1 < nsteps ? offn : off0;
-    #pragma unroll
+#pragma unroll
                         for (int i = 0; i < MB; ++i)
                             av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
                         __builtin_amdgcn_sched_barrier(0);
@@ -773,33 +773,33 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                         wnx += more ? wstep : 0;
                         kw += more;
                         mma(av[t & 1], b[t], nbac);
-    #pragma unroll
+#pragma unroll
                         for (int k = 0; k < 16; ++k) {
                             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one product
                             __builtin_amdgcn_sched_group_barrier(0x004, 2, 0);  // two scalar instructions
                         }
                         __builtin_amdgcn_sched_group_barrier(0x008, MB * NB * (BF ? 1 : 4), 0);
                         __builtin_amdgcn_sched_barrier(0);
-    #pragma unroll
+#pragma unroll
                         for (int j = 0; j < NB; ++j) b[t][j] = wcur[j * 64];
                     } else {
                         off = advance(off);  // step s + t + 1
                         const int offa = s + t + 1 < nsteps ? off : off0;
-    #pragma unroll
+#pragma unroll
                         for (int i = 0; i < MB; ++i)
                             av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
                         __builtin_amdgcn_sched_barrier(0);
                         mma(av[t & 1], b[t], nbac);
                         __builtin_amdgcn_sched_barrier(0);
                         const size_t wn2 = (size_t)min(s + t + PD, last) * wstep;
-    #pragma unroll
+#pragma unroll
                         for (int j = 0; j < NB; ++j) b[t][j] = wpk[wn2 + j * 64];
                     }
                 }
             }
             if constexpr (IL) off = offn;  // the tail advances from the next step's offset
             // the last nsteps % PD steps (their weights are already loaded)
-    #pragma unroll
+#pragma unroll
             for (int t = 0; t + 1 < PD; ++t) {
                 if (s + t < nsteps) {
                     int offa;
@@ -810,7 +810,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                         off = advance(off);
                         offa = s + t + 1 < nsteps ? off : off0;
                     }
-    #pragma unroll
+#pragma unroll
                     for (int i = 0; i < MB; ++i)
                         av[(t + 1) & 1][i] = *reinterpret_cast<const u4 *>(win_lds + abase[i] + offa);
                     mma(av[t & 1], b[t], nbac);
