@@ -130,11 +130,16 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
 // neighbours share it through the cache) and every child row is written with
 // contiguous stores; the k^2 siblings no longer re-read the parent.
 template <int K, int RB, bool BF, bool IN_F32, int V>
-__global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int nbands, int nchunks)
+__global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int nbands, int nchunks, int nblocks)
 {
     using TO = typename std::conditional<BF, uint16_t, float>::type;
     using TI = typename std::conditional<IN_F32, float, TO>::type;
-    int bid = blockIdx.x;
+    // Workgroups are dealt to the 8 XCDs round-robin; renumber them so each
+    // XCD takes a contiguous run of bands, and the K - 1 parent rows that
+    // neighbouring bands share are read from that XCD's L2 rather than twice
+    // from HBM (the grid is padded to a multiple of 8; the padding exits).
+    int bid = (blockIdx.x % 8) * (gridDim.x / 8) + blockIdx.x / 8;
+    if (bid >= nblocks) return;
     const int chunk = bid % nchunks;
     bid /= nchunks;
     const int band = bid % nbands;
@@ -238,9 +243,10 @@ hipError_t go_rows_rb(const PoolArgs &a, hipStream_t s)
     const int nbands = (a.in_h + RB - 1) / RB;
     const int nchunks = (a.in_w * nv + 255) / 256;
     const long long grid = (long long)a.n_children / (K * K) * nbands * nchunks;
-    if (grid <= 0 || grid > 0x7fffffffLL) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((pool_frag_rows<K, RB, BF, IN_F32, V>), dim3((unsigned)grid), dim3(256), 0, s, a, nbands,
-                       nchunks);
+    const long long grid8 = (grid + 7) / 8 * 8;
+    if (grid <= 0 || grid8 > 0x7fffffffLL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((pool_frag_rows<K, RB, BF, IN_F32, V>), dim3((unsigned)grid8), dim3(256), 0, s, a, nbands,
+                       nchunks, (int)grid);
     return hipGetLastError();
 }
 
