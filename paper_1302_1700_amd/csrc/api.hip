@@ -944,10 +944,11 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         digits(net->pool_kx, net->Sx, a.digit_x);
         const long long npix = (long long)B * P.ny * P.nx;
         // the head numbers a window within its image with 32-bit integers
-        if ((long long)P.ny * P.nx >= (1LL << 31) || (npix + 15) / 16 >= kMaxGrid)
+        const long long per_wg = 256LL / kHeadLanesPerPixel * kHeadPixelsPerGroup;
+        if ((long long)P.ny * P.nx >= (1LL << 31) || (npix + per_wg - 1) / per_wg >= kMaxGrid)
             return fail(FS_ERR_UNSUPPORTED, "%d x %d windows per image (batch %d): scan the image in tiles", P.ny,
                         P.nx, B);
-        L.gx = (int)((npix + 15) / 16);
+        L.gx = (int)((npix + per_wg - 1) / per_wg);
         L.frags = B * a.F;
         L.out_pixels = npix;
         L.flops = net->head_fc ? (double)npix * 2.0 * net->head_cin * net->ncls : 0.0;

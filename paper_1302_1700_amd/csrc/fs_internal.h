@@ -23,6 +23,12 @@ namespace fs {
 constexpr int kMaxAxis = 256;   // per-axis fragment count limit (product of pool sizes)
 constexpr int kMaxSide = 65535; // image rows / columns of one scan (fragment sizes are 16-bit)
 constexpr int kMaxHeadClasses = 16;
+// Head kernel: kHeadLanesPerPixel lanes share one output pixel's channel
+// vector, and each group of them takes kHeadPixelsPerGroup pixels in turn, so
+// a workgroup's weight staging serves 256 / kHeadLanesPerPixel *
+// kHeadPixelsPerGroup pixels.
+constexpr int kHeadLanesPerPixel = 4;
+constexpr int kHeadPixelsPerGroup = 4;
 constexpr int kMaxHeadWeights = 8192;  // n_classes * c_in of a fused last layer
 constexpr size_t kMaxLdsBytes = 160 * 1024;  // LDS of one CDNA4 compute unit
 constexpr int kMaxChannels = 16384;           // per layer (kernels divide by channel counts below 2^16)

@@ -14,10 +14,18 @@
 // pools' column sizes.  The host turns "Y mod S_y -> row index of the
 // fragment grid" (and the same for X) into small tables.
 //
-// Mapping: 16 lanes per output pixel, consecutive groups take consecutive
-// output pixels, so the dense output is written contiguously while each group
-// reads its fragment pixel's channel vector contiguously (16-byte loads); the
-// dot products over the channels are finished with cross-lane xor shuffles.
+// Mapping: LPP = kHeadLanesPerPixel lanes per output pixel, consecutive groups
+// take consecutive output pixels, so the dense output is written contiguously
+// while each group reads its fragment pixel's channel vector contiguously
+// (16-byte loads); the dot products over the channels are finished with
+// cross-lane xor shuffles.  A workgroup's 256 / LPP groups take
+// kHeadPixelsPerGroup runs of 256 / LPP consecutive pixels, one run after the
+// other, so the weights it stages in LDS serve that many more pixels.  The
+// per-pixel work every lane of a group repeats (coordinates, softmax) is why
+// the groups are narrow: with 16 lanes per pixel, one run per workgroup and
+// the coordinates divided out per pixel the kernel moved 2.0 TB/s on N4
+// 8 x 1024^2; with 4 lanes, 4 runs and incremental coordinates 3.9 TB/s
+// (2, 8 or 1 lanes and 1, 2 or 8 runs measured slower).
 #include "fs_internal.h"
 
 namespace fs {
@@ -39,98 +47,137 @@ __global__ __launch_bounds__(256) void head_softmax_reassemble(HeadArgs a)
     if (threadIdx.x < kMaxHeadClasses) bl[threadIdx.x] = threadIdx.x < ncls ? a.bias[threadIdx.x] : 0.f;
     __syncthreads();
 
-    const int sub = threadIdx.x & 15;
-    const long long gp = (long long)blockIdx.x * 16 + (threadIdx.x >> 4);
+    constexpr int LPP = kHeadLanesPerPixel, GPW = 256 / LPP;  // lanes per pixel, groups per workgroup
+    const int sub = threadIdx.x & (LPP - 1);
     const long long npix = (long long)a.B * a.ny * a.nx;
+    // The group's pixel: image b, window (Y, X) = (yf * Sy + ym, xf * Sx + xm).
+    // Divided out once; each later run moves GPW pixels on, which advances the
+    // coordinates by additions (a column digit wraps, a row ends, an image
+    // ends), since per-pixel integer divisions had dominated the kernel.
+    long long gp = (long long)blockIdx.x * kHeadPixelsPerGroup * GPW + threadIdx.x / LPP;
     if (gp >= npix) return;
-    const int b = (int)(gp / ((long long)a.ny * a.nx));
-    const int r = (int)(gp - (long long)b * a.ny * a.nx);
-    const int Y = r / a.nx, X = r - (r / a.nx) * a.nx;
-    const int fy = a.digit_y[Y % a.Sy], fx = a.digit_x[X % a.Sx];
-    const int yf = Y / a.Sy, xf = X / a.Sx;
-    const size_t q = (size_t)b * a.F + (size_t)fy * a.Qx + fx;
-    const TI *src = reinterpret_cast<const TI *>(a.in) + ((q * a.in_h + yf) * a.in_w + xf) * a.C;
-
-    float z[kMaxHeadClasses];
-#pragma unroll
-    for (int c = 0; c < kMaxHeadClasses; ++c) z[c] = 0.f;
-
-    if constexpr (HAS_FC) {
-        const int nv = a.C / V;
-        for (int cv = sub; cv < nv; cv += 16) {
-            float v[V];
-            if constexpr (V == 1) {
-                if constexpr (BF && !IN_F32) v[0] = __uint_as_float((uint32_t)src[cv] << 16);
-                else v[0] = src[cv];
-            } else {
-                u4 raw = *reinterpret_cast<const u4 *>(src + cv * V);
-                if constexpr (BF && !IN_F32) {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        v[2 * e] = __uint_as_float(raw[e] << 16);
-                        v[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+    const long long plane = (long long)a.ny * a.nx;
+    int b = (int)(gp / plane);
+    const int r0 = (int)(gp - (long long)b * plane);
+    int Y = r0 / a.nx, X = r0 - Y * a.nx;
+    int yf = Y / a.Sy, ym = Y - yf * a.Sy;
+    int xf = X / a.Sx, xm = X - xf * a.Sx;
+    for (int run = 0; run < kHeadPixelsPerGroup; ++run) {
+        if (run > 0) {
+            gp += GPW;
+            if (gp >= npix) return;
+            X += GPW;
+            xm += GPW;
+            while (xm >= a.Sx) {
+                xm -= a.Sx;
+                ++xf;
+            }
+            if (X >= a.nx) {
+                do {  // past the row's end: the next row, or the next image
+                    X -= a.nx;
+                    ++Y;
+                    if (++ym == a.Sy) {
+                        ym = 0;
+                        ++yf;
                     }
-                } else {
+                    if (Y == a.ny) {
+                        Y = 0;
+                        ym = 0;
+                        yf = 0;
+                        ++b;
+                    }
+                } while (X >= a.nx);
+                xf = X / a.Sx;
+                xm = X - xf * a.Sx;
+            }
+        }
+        const int fy = a.digit_y[ym], fx = a.digit_x[xm];
+        const size_t q = (size_t)b * a.F + (size_t)fy * a.Qx + fx;
+        const TI *src = reinterpret_cast<const TI *>(a.in) + ((q * a.in_h + yf) * a.in_w + xf) * a.C;
+
+        float z[kMaxHeadClasses];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]);
+        for (int c = 0; c < kMaxHeadClasses; ++c) z[c] = 0.f;
+
+        if constexpr (HAS_FC) {
+            const int nv = a.C / V;
+            for (int cv = sub; cv < nv; cv += LPP) {
+                float v[V];
+                if constexpr (V == 1) {
+                    if constexpr (BF && !IN_F32) v[0] = __uint_as_float((uint32_t)src[cv] << 16);
+                    else v[0] = src[cv];
+                } else {
+                    u4 raw = *reinterpret_cast<const u4 *>(src + cv * V);
+                    if constexpr (BF && !IN_F32) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            v[2 * e] = __uint_as_float(raw[e] << 16);
+                            v[2 * e + 1] = __uint_as_float(raw[e] & 0xffff0000u);
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) v[e] = __uint_as_float(raw[e]);
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < kMaxHeadClasses; ++c) {
+                    if (c < ncls) {
+                        const float *wr = wl + c * a.C + cv * V;
+#pragma unroll
+                        for (int e = 0; e < V; ++e) z[c] = fmaf(wr[e], v[e], z[c]);
+                    }
                 }
             }
 #pragma unroll
             for (int c = 0; c < kMaxHeadClasses; ++c) {
                 if (c < ncls) {
-                    const float *wr = wl + c * a.C + cv * V;
+                    float t = z[c];
 #pragma unroll
-                    for (int e = 0; e < V; ++e) z[c] = fmaf(wr[e], v[e], z[c]);
+                    for (int d = LPP / 2; d >= 1; d /= 2) t += __shfl_xor(t, d);
+                    z[c] = t + bl[c];
+                }
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < kMaxHeadClasses; ++c) {
+                if (c < ncls) {
+                    if constexpr (BF && !IN_F32) z[c] = __uint_as_float((uint32_t)src[c] << 16);
+                    else z[c] = src[c];
                 }
             }
         }
+
+        if (a.act == ACT_SOFTMAX) {
+            float m = z[0];
 #pragma unroll
-        for (int c = 0; c < kMaxHeadClasses; ++c) {
-            if (c < ncls) {
-                float t = z[c];
-                t += __shfl_xor(t, 8);
-                t += __shfl_xor(t, 4);
-                t += __shfl_xor(t, 2);
-                t += __shfl_xor(t, 1);
-                z[c] = t + bl[c];
+            for (int c = 1; c < kMaxHeadClasses; ++c)
+                if (c < ncls) m = fmaxf(m, z[c]);
+            float s = 0.f;
+#pragma unroll
+            for (int c = 0; c < kMaxHeadClasses; ++c) {
+                if (c < ncls) {
+                    z[c] = __expf(z[c] - m);  // z - m <= 0: the hardware exp2, a few ulp
+                    s += z[c];
+                }
             }
+            const float inv = 1.0f / s;
+#pragma unroll
+            for (int c = 0; c < kMaxHeadClasses; ++c) z[c] *= inv;
+        } else if (a.act == ACT_TANH) {
+#pragma unroll
+            for (int c = 0; c < kMaxHeadClasses; ++c) z[c] = tanhf(z[c]);
         }
-    } else {
+
+        // lane sub writes classes sub, sub + LPP, ...
 #pragma unroll
-        for (int c = 0; c < kMaxHeadClasses; ++c) {
-            if (c < ncls) {
-                if constexpr (BF && !IN_F32) z[c] = __uint_as_float((uint32_t)src[c] << 16);
-                else z[c] = src[c];
-            }
+        for (int c0 = 0; c0 < kMaxHeadClasses; c0 += LPP) {
+            float mine = 0.f;
+#pragma unroll
+            for (int c = c0; c < c0 + LPP && c < kMaxHeadClasses; ++c)
+                if (c - c0 == sub) mine = z[c];
+            if (c0 + sub < ncls) a.out[(((size_t)b * a.out_ny + Y) * a.out_nx + X) * ncls + c0 + sub] = mine;
         }
     }
-
-    if (a.act == ACT_SOFTMAX) {
-        float m = z[0];
-#pragma unroll
-        for (int c = 1; c < kMaxHeadClasses; ++c)
-            if (c < ncls) m = fmaxf(m, z[c]);
-        float s = 0.f;
-#pragma unroll
-        for (int c = 0; c < kMaxHeadClasses; ++c) {
-            if (c < ncls) {
-                z[c] = expf(z[c] - m);
-                s += z[c];
-            }
-        }
-        const float inv = 1.0f / s;
-#pragma unroll
-        for (int c = 0; c < kMaxHeadClasses; ++c) z[c] *= inv;
-    } else if (a.act == ACT_TANH) {
-#pragma unroll
-        for (int c = 0; c < kMaxHeadClasses; ++c) z[c] = tanhf(z[c]);
-    }
-
-    float mine = 0.f;
-#pragma unroll
-    for (int c = 0; c < kMaxHeadClasses; ++c)
-        if (c == sub) mine = z[c];
-    if (sub < ncls) a.out[(((size_t)b * a.out_ny + Y) * a.out_nx + X) * ncls + sub] = mine;
 }
 
 template <bool BF, bool IN_F32, bool HAS_FC, int V>
