@@ -64,7 +64,10 @@ typedef enum {
     FS_ERR_UNSUPPORTED = 3,  /* allowed by the method, not by this library */
     FS_ERR_WORKSPACE = 4,    /* workspace smaller than fs_scan_plan asks for */
     FS_ERR_OOM = 5,          /* device allocation failed (fs_net_create only) */
-    FS_ERR_HIP = 6           /* a HIP runtime call failed */
+    FS_ERR_HIP = 6,          /* a HIP runtime call failed */
+    FS_ERR_BOUNDS = 7        /* debug library only (libfragscan_debug.so): a kernel's
+                              * bounds check failed; fs_last_error names the checks.
+                              * The scan skipped those accesses: its output is not valid */
 } fs_status;
 
 /* Layer kinds (Section 2: input, convolutional, max-pooling and fully

@@ -74,6 +74,91 @@ fs_status scratch_on(int device, void **out)
     return FS_OK;
 }
 
+#ifdef FRAGSCAN_DEBUG
+}  // namespace
+// Debug builds: the status word of the kernels' bounds checks (bit i: check
+// site i failed), one per device like `scratch`, looked up the same way.
+static __device__ __align__(256) unsigned dbg_word[64];
+__global__ void dbg_clear(unsigned *w) { w[0] = 0u; }
+namespace {
+std::mutex g_dbg_mu;
+unsigned *g_dbg_ptr[kMaxDevices];
+
+const char *const kDbgSiteName[DBG_NSITES] = {
+    "convolution input window", "convolution weight blocks", "convolution output",
+    "fused pool child",         "fused head output map",     "pool parent",
+    "pool child",               "head fragment",             "head output map",
+    "mirror pad image"};
+#endif
+
+// The bounds-check status word of this call (debug builds), cleared on
+// stream s before the call's launches; nullptr in release builds.
+fs_status dbg_begin(hipStream_t s, unsigned **word)
+{
+    *word = nullptr;
+#ifdef FRAGSCAN_DEBUG
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(FS_ERR_UNSUPPORTED, "device %d: no status word", dev);
+    {
+        std::lock_guard<std::mutex> lock(g_dbg_mu);
+        if (!g_dbg_ptr[dev]) {
+            void *p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(dbg_word));
+            if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (dbg_word)");
+            g_dbg_ptr[dev] = static_cast<unsigned *>(p);
+        }
+        *word = g_dbg_ptr[dev];
+    }
+    hipLaunchKernelGGL(dbg_clear, dim3(1), dim3(1), 0, s, *word);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "bounds-check status clear");
+#else
+    (void)s;
+#endif
+    return FS_OK;
+}
+
+// After the call's launches (debug builds): wait for them and report the
+// failed checks as FS_ERR_BOUNDS.
+fs_status dbg_end(hipStream_t s, unsigned *word)
+{
+#ifdef FRAGSCAN_DEBUG
+    unsigned h = 0;
+    hipError_t e = hipMemcpyAsync(&h, word, sizeof h, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "bounds-check status read");
+    if (h) {
+        std::string sites;
+        for (int i = 0; i < DBG_NSITES; ++i)
+            if (h & (1u << i)) sites += std::string(sites.empty() ? "" : ", ") + kDbgSiteName[i];
+        return fail(FS_ERR_BOUNDS, "bounds check failed: %s", sites.c_str());
+    }
+#else
+    (void)s;
+    (void)word;
+#endif
+    return FS_OK;
+}
+
+// Debug builds: FRAGSCAN_DEBUG_SHRINK=<i> makes launch i of a scan's plan
+// check against true sizes one smaller than the real ones (=pad: the mirror
+// pad), so that its checks fail on accesses that are in fact in bounds (a
+// test of the failure path that leaves every access inside the buffers);
+// -1 (-2 for the pad) when unset or in release builds.
+int dbg_shrink_at()
+{
+#ifdef FRAGSCAN_DEBUG
+    const char *v = getenv("FRAGSCAN_DEBUG_SHRINK");
+    if (!v || !*v) return -1;
+    if (std::strcmp(v, "pad") == 0) return -2;
+    return atoi(v);
+#else
+    return -1;
+#endif
+}
+
 uint16_t host_f2bf(float f)
 {
     uint32_t u;
@@ -942,6 +1027,7 @@ fs_status make_plan(const fs_net *net, int B, int H, int W, Plan &P, const View 
         };
         digits(net->pool_k, net->S, a.digit_y);
         digits(net->pool_kx, net->Sx, a.digit_x);
+        fill_axis(a.ext, g);
         const long long npix = (long long)B * P.ny * P.nx;
         // the head numbers a window within its image with 32-bit integers
         const long long per_wg = 256LL / kHeadLanesPerPixel * kHeadPixelsPerGroup;
@@ -1144,9 +1230,12 @@ fs_status tiled_plan(const fs_net *net, int B, int H, int W, int th, int tw, Til
 // launch's arguments are copied and given their buffers here.  img_off /
 // out_off (floats) place a tiled scan's region in the image and the map.
 hipError_t enqueue(const fs_net *net, const Plan &P, const float *d_image, float *d_out, void *d_ws,
-                   hipStream_t s, int i, size_t img_off = 0, size_t out_off = 0)
+                   hipStream_t s, int i, unsigned *dbg, int shrink_at, size_t img_off = 0, size_t out_off = 0)
 {
     Launch L = P.launches[i];
+    const int shrink = i == shrink_at ? 1 : 0;
+    L.conv.dbg = L.pool.dbg = L.head.dbg = dbg;
+    L.conv.dbg_shrink = L.pool.dbg_shrink = L.head.dbg_shrink = shrink;
     char *ws = static_cast<char *>(d_ws);
     d_image += img_off;
     d_out += out_off;
@@ -1204,6 +1293,7 @@ const char *fs_status_str(fs_status s)
     case FS_ERR_WORKSPACE: return "workspace too small";
     case FS_ERR_OOM: return "out of device memory";
     case FS_ERR_HIP: return "HIP runtime error";
+    case FS_ERR_BOUNDS: return "bounds check failed (debug library)";
     }
     return "unknown status";
 }
@@ -1564,19 +1654,23 @@ fs_status fs_scan_tiled(const fs_net *net, const float *d_image, int32_t B, int3
     st = check_device(net);
     if (st != FS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned *dbg = nullptr;
+    st = dbg_begin(s, &dbg);
+    if (st != FS_OK) return st;
+    const int shrink_at = dbg_shrink_at();
     for (int r = 0; r < T.rows; ++r)
         for (int c = 0; c < T.cols; ++c) {
             const Plan &P = *T.shape[r == T.rows - 1][c == T.cols - 1];
             const size_t y0 = (size_t)r * T.th, x0 = (size_t)c * T.tw;
             const size_t img_off = (y0 * W + x0) * net->C, out_off = (y0 * T.nx + x0) * net->ncls;
             for (int i = 0; i < (int)P.launches.size(); ++i) {
-                hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i, img_off, out_off);
+                hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i, dbg, shrink_at, img_off, out_off);
                 if (e != hipSuccess)
                     return fail(FS_ERR_HIP, "tile (%d, %d) launch %d (%s): %s", r, c, i, P.launches[i].name.c_str(),
                                 hipGetErrorString(e));
             }
         }
-    return FS_OK;
+    return dbg_end(s, dbg);
 }
 
 fs_status fs_scan_plan(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_plan_info *out)
@@ -1636,20 +1730,25 @@ fs_status fs_scan_border(const fs_net *net, const float *d_image, int32_t B, int
     st = check_device(net);
     if (st != FS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned *dbg = nullptr;
+    st = dbg_begin(s, &dbg);
+    if (st != FS_OK) return st;
+    const int shrink_at = dbg_shrink_at();
     const float *img = d_image;
     if (border != BORDER_VALID) {
         float *pad = reinterpret_cast<float *>(static_cast<char *>(d_workspace) + pad_off);
         const int p0y = (net->patch - 1) / 2, p0x = (net->patch_x - 1) / 2;
-        hipError_t e = launch_mirror_pad(d_image, pad, B, H, W, net->C, p0y, p0x, He, We, border, s);
+        hipError_t e = launch_mirror_pad(d_image, pad, B, H, W, net->C, p0y, p0x, He, We, border, dbg,
+                                         shrink_at == -2 ? 1 : 0, s);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "mirror pad: %s", hipGetErrorString(e));
         img = pad;
     }
     for (int i = 0; i < (int)P.launches.size(); ++i) {
-        hipError_t e = enqueue(net, P, img, d_out, d_workspace, s, i);
+        hipError_t e = enqueue(net, P, img, d_out, d_workspace, s, i, dbg, shrink_at);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
                                          hipGetErrorString(e));
     }
-    return FS_OK;
+    return dbg_end(s, dbg);
 }
 
 fs_status fs_scan_launches(const fs_net *net, int32_t B, int32_t H, int32_t W, fs_launch_info *h_out,
@@ -1693,12 +1792,16 @@ fs_status fs_scan(const fs_net *net, const float *d_image, int32_t B, int32_t H,
     if (st != FS_OK) return st;
     const Plan &P = *PP;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned *dbg = nullptr;
+    st = dbg_begin(s, &dbg);
+    if (st != FS_OK) return st;
+    const int shrink_at = dbg_shrink_at();
     for (int i = 0; i < (int)P.launches.size(); ++i) {
-        hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+        hipError_t e = enqueue(net, P, d_image, d_out, d_workspace, s, i, dbg, shrink_at);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
                                          hipGetErrorString(e));
     }
-    return FS_OK;
+    return dbg_end(s, dbg);
 }
 
 fs_status fs_scan_noalloc(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W, float *d_out,
@@ -1721,12 +1824,16 @@ fs_status fs_scan_noalloc(const fs_net *net, const float *d_image, int32_t B, in
     st = scratch_on(net->device, &ws);
     if (st != FS_OK) return st;
     hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned *dbg = nullptr;
+    st = dbg_begin(s, &dbg);
+    if (st != FS_OK) return st;
+    const int shrink_at = dbg_shrink_at();
     for (int i = 0; i < (int)P.launches.size(); ++i) {
-        hipError_t e = enqueue(net, P, d_image, d_out, ws, s, i);
+        hipError_t e = enqueue(net, P, d_image, d_out, ws, s, i, dbg, shrink_at);
         if (e != hipSuccess) return fail(FS_ERR_HIP, "launch %d (%s): %s", i, P.launches[i].name.c_str(),
                                          hipGetErrorString(e));
     }
-    return FS_OK;
+    return dbg_end(s, dbg);
 }
 
 fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, int32_t H, int32_t W,
@@ -1745,6 +1852,10 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
     // launch reads one buffer and writes another (or the output), so a
     // repetition recomputes the same values and the launches that follow see
     // exactly what a plain scan leaves them.
+    unsigned *dbg = nullptr;
+    st = dbg_begin(s, &dbg);
+    if (st != FS_OK) return st;
+    const int shrink_at = dbg_shrink_at();
     std::vector<hipEvent_t> ev((size_t)n * 2, nullptr);
     hipError_t e = hipSuccess;
     for (auto &x : ev) {
@@ -1753,7 +1864,8 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
     }
     for (int i = 0; i < n && e == hipSuccess; ++i) {
         e = hipEventRecord(ev[2 * i], s);
-        for (int r = 0; r < reps && e == hipSuccess; ++r) e = enqueue(net, P, d_image, d_out, d_workspace, s, i);
+        for (int r = 0; r < reps && e == hipSuccess; ++r)
+            e = enqueue(net, P, d_image, d_out, d_workspace, s, i, dbg, shrink_at);
         if (e == hipSuccess) e = hipEventRecord(ev[2 * i + 1], s);
     }
     if (e == hipSuccess) e = hipStreamSynchronize(s);
@@ -1767,7 +1879,7 @@ fs_status fs_scan_profile(const fs_net *net, const float *d_image, int32_t B, in
         if (x) (void)hipEventDestroy(x);
     if (e != hipSuccess) return hip_fail(e, "profiled scan");
     for (int i = 0; i < std::min(n, (int)capacity); ++i) h_launch_ms[i] = (float)(ms_i[i] / reps);
-    return FS_OK;
+    return dbg_end(s, dbg);
 }
 
 fs_status fs_fragment_table(const fs_net *net, int32_t H, int32_t W, int32_t *h_out, size_t capacity,

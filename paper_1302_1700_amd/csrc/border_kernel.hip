@@ -27,8 +27,9 @@ __device__ __forceinline__ int mirror_index(int i, int n, int mode)
     return i >= n ? p - 1 - i : i;
 }
 
-__global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, float *__restrict__ out, int H, int W,
-                                                  int C, int p0y, int p0x, int He, int We, int mode, long long total)
+__global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, float *__restrict__ out, int B, int H,
+                                                  int W, int C, int p0y, int p0x, int He, int We, int mode,
+                                                  long long total, unsigned *dbg, int dbg_shrink)
 {
     for (long long e = (long long)blockIdx.x * 256 + threadIdx.x; e < total; e += (long long)gridDim.x * 256) {
         const int c = (int)(e % C);
@@ -38,6 +39,8 @@ __global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, 
         const int y = (int)(p % He);
         const long long b = p / He;
         const int sy = mirror_index(y - p0y, H, mode), sx = mirror_index(x - p0x, W, mode);
+        if (!FS_DBG_OK(dbg, b < B && sy >= 0 && sx >= 0 && sy < H - dbg_shrink && sx < W - dbg_shrink, DBG_PAD_READ))
+            continue;
         out[e] = in[((b * H + sy) * W + sx) * C + c];
     }
 }
@@ -45,12 +48,13 @@ __global__ __launch_bounds__(256) void mirror_pad(const float *__restrict__ in, 
 }  // namespace
 
 hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0y, int p0x, int He,
-                             int We, int mode, hipStream_t s)
+                             int We, int mode, unsigned *dbg, int dbg_shrink, hipStream_t s)
 {
     const long long total = (long long)B * He * We * C;
     const long long blocks = (total + 255) / 256;
     const int grid = (int)(blocks < 65536 ? blocks : 65536);
-    hipLaunchKernelGGL(mirror_pad, dim3(grid), dim3(256), 0, s, in, out, H, W, C, p0y, p0x, He, We, mode, total);
+    hipLaunchKernelGGL(mirror_pad, dim3(grid), dim3(256), 0, s, in, out, B, H, W, C, p0y, p0x, He, We, mode, total,
+                       dbg, dbg_shrink);
     return hipGetLastError();
 }
 

@@ -75,10 +75,17 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
 
     const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * a.in_h * a.in_w * a.in_c +
                     (valid ? ((size_t)y * a.in_w + x) * a.in_c : 0);
+    // a valid pixel's window lies inside its fragment's true size; the others
+    // read the window at (0, 0), inside the storage
+    [[maybe_unused]] const int ry = (valid ? y : 0) + a.ky - 1, rx = (valid ? x : 0) + a.kx - 1;
+    const bool rd = FS_DBG_OK(a.dbg,
+                              q < a.nfrag && ry < a.in_h && rx < a.in_w &&
+                                  (!valid || (ry < a.ext.y[fy] - a.dbg_shrink && rx < a.ext.x[fx] - a.dbg_shrink)),
+                              DBG_CONV_READ);
     float xin[KP];
 #pragma unroll
     for (int kk = 0; kk < KP; ++kk) {
-        const TI raw = inp[offs[kk]];
+        const TI raw = rd ? inp[offs[kk]] : TI(0);
         float v;
         if constexpr (BF && !IN_F32) v = __uint_as_float((uint32_t)raw << 16);
         else v = raw;
@@ -117,13 +124,16 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
     __syncthreads();
     TO *out = reinterpret_cast<TO *>(a.out) + ((size_t)q * a.out_h * a.out_w + pix0 + wv * 64) * a.cout;
     const int wpix0 = pix0 + wv * 64;
+    auto write_ok = [&](int py, int px) {
+        return FS_DBG_OK(a.dbg, q < a.nfrag && py < hout - a.dbg_shrink && px < wout - a.dbg_shrink, DBG_CONV_WRITE);
+    };
     if ((a.cout % G) == 0) {
         const int ng = a.cout / G;
         for (int ch = lane; ch < 64 * ng; ch += 64) {
             const int p = ch / ng, grp = ch - (ch / ng) * ng;
             const int pp = wpix0 + p;
             const int py = pp / a.out_w, px = pp - (pp / a.out_w) * a.out_w;
-            if (pp < a.out_h * a.out_w && py < hout && px < wout)
+            if (pp < a.out_h * a.out_w && py < hout && px < wout && write_ok(py, px))
                 *reinterpret_cast<u4 *>(out + (size_t)ch * G) = *reinterpret_cast<const u4 *>(stage + p * rs + grp * G);
         }
     } else {
@@ -131,7 +141,7 @@ __global__ __launch_bounds__(256) void conv_direct(ConvArgs a, const float *__re
             const int p = e / a.cout, c = e - (e / a.cout) * a.cout;
             const int pp = wpix0 + p;
             const int py = pp / a.out_w, px = pp - (pp / a.out_w) * a.out_w;
-            if (pp < a.out_h * a.out_w && py < hout && px < wout) out[e] = stage[p * rs + c];
+            if (pp < a.out_h * a.out_w && py < hout && px < wout && write_ok(py, px)) out[e] = stage[p * rs + c];
         }
     }
 }

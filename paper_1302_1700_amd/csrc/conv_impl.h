@@ -262,6 +262,17 @@ __device__ __forceinline__ void fused_head_partials(const ConvArgs &a, const f4 
     }
 }
 
+// Bounds check of a fused-head write: output (y, x) of final fragment
+// (fy, fx) of image b lies inside the fragment's true size and its window
+// (Y, X) inside the map.
+__device__ __forceinline__ bool head_ok(const ConvArgs &a, int b, int fy, int fx, int y, int x, int Y, int X)
+{
+    return FS_DBG_OK(a.dbg,
+                     b < a.nfrag / a.F && y < a.ext.y[fy] - a.ky + 1 - a.dbg_shrink &&
+                         x < a.ext.x[fx] - a.kx + 1 - a.dbg_shrink && Y < a.ny && X < a.nx,
+                     DBG_FUSED_HEAD);
+}
+
 // locate(m, fy, fx, y, x): fragment (fy, fx) of image b and output (y, x)
 // in it of the tile's pixel m < npix.
 template <int WN, class Locate>
@@ -283,6 +294,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
             int fy, fx, y, x;
             locate(m, fy, fx, y, x);
             const int Y = a.base_y[fy] + a.Sy * y, X = a.base_x[fx] + a.Sx * x;
+            if (!head_ok(a, b, fy, fx, y, x, Y, X)) continue;
             float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * 2;
             *reinterpret_cast<float2 *>(dst) = float2{z[0], z[1]};
             continue;
@@ -316,6 +328,7 @@ __device__ __forceinline__ void fused_head_finish(const ConvArgs &a, int b, int 
         int fy, fx, y, x;
         locate(m, fy, fx, y, x);
         const int Y = a.base_y[fy] + a.Sy * y, X = a.base_x[fx] + a.Sx * x;
+        if (!head_ok(a, b, fy, fx, y, x, Y, X)) continue;
         float *dst = a.head_out + (((size_t)b * a.ny + Y) * a.nx + X) * ncls;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
@@ -347,6 +360,8 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
     int bid = (blockIdx.x % 8) * per_xcd + blockIdx.x / 8;
     const int nunit = RUN ? a.nfrag / a.F : a.nfrag;  // images (run tiles) or fragments
     if (bid >= nunit * a.nbands * a.tiles_per_band) return;
+    // the tile's channel blocks (weights, bias, last-layer weights) lie in the layer's packing
+    if (!FS_DBG_OK(a.dbg, (int)(blockIdx.y + 1) * (WN * NB) <= a.nbt, DBG_CONV_WEIGHT)) return;
     int sib = 0;  // xsib: the fragment's column index
     if (!RUN && a.xsib) {
         sib = bid % a.Qx;
@@ -468,11 +483,15 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
     const size_t fsz = (size_t)a.in_h * a.in_w * a.in_c;
     const TI *inp = reinterpret_cast<const TI *>(a.in) + (size_t)q * fsz;
     const TI *inp1 = reinterpret_cast<const TI *>(a.in) + (size_t)q1 * fsz;
-    // nrows window rows from row row0 on: rows gy0 .. of fragment src, whose
-    // true size is hh x ww (outside it, zeros)
-    auto stage = [&](const TI *src, int gy0, int hh, int ww, int row0, int nrows) {
+    // nrows window rows from row row0 on: rows gy0 .. of fragment src (batch
+    // index fq), whose true size is hh x ww (outside it, zeros)
+    auto stage = [&](const TI *src, int fq, int gy0, int hh, int ww, int row0, int nrows) {
         const int rowp = a.in_w * a.in_c;  // elements per input row (fragments stay below 2^31)
         const int npx = nrows * Cc;        // window pixels to stage
+        auto read_ok = [&](int gy, int gx) {
+            return FS_DBG_OK(a.dbg, fq < a.nfrag && gy < hh - a.dbg_shrink && gx < ww - a.dbg_shrink && gy < a.in_h &&
+                                        gx < a.in_w, DBG_CONV_READ);
+        };
         // Fast form (up to 64 loads per pixel): a thread owns load v of
         // window pixels p, p + P, p + 2P, ... (P = 256 / loads per pixel);
         // the pixel's (row, column) and both addresses advance by constants,
@@ -504,9 +523,9 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                     // stage two fragments with the wider one's columns.
                     if constexpr (RUN) {
                         val[u] = {};
-                        if (in && gy0 + r < hh && c0 + c < ww) val[u] = load(soff);
+                        if (in && gy0 + r < hh && c0 + c < ww && read_ok(gy0 + r, c0 + c)) val[u] = load(soff);
                     } else {
-                        if (in) val[u] = load(soff);
+                        if (in && read_ok(gy0 + r, c0 + c)) val[u] = load(soff);
                     }
                     dsto[u] = in ? doff : -1;
                     p += P;
@@ -546,7 +565,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                     dcc.qr(p, r, c);
                     const int gy = gy0 + r, gx = c0 + c;
                     val[u] = u4{0u, 0u, 0u, 0u};
-                    if (idx < total && gy < hh && gx < ww)
+                    if (idx < total && gy < hh && gx < ww && read_ok(gy, gx))
                         val[u] = *reinterpret_cast<const u4 *>(src + (gy * rowp + __mul24(gx, a.in_c) + v * LPE));
                     dsto[u] = idx < total ? __mul24(__mul24(row0 + r, Cc) + c, CS) + v * LPE : -1;
                 }
@@ -572,7 +591,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                 dcc.qr(p, r, c);
                 const int gy = gy0 + r, gx = c0 + c;
                 TC val = 0;
-                if (gy < hh && gx < ww) {
+                if (gy < hh && gx < ww && read_ok(gy, gx)) {
                     TI x = src[gy * rowp + __mul24(gx, a.in_c) + ci];
                     if constexpr (BF && IN_F32)
                         val = f2bf(x);
@@ -583,9 +602,9 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
             }
         }
     };
-    stage(inp, yfirst, hin, win, 0, R);
+    stage(inp, q, yfirst, hin, win, 0, R);
     if constexpr (RUN)
-        if (R1 > 0) stage(inp1, 0, hin1, win1, R, R1);
+        if (R1 > 0) stage(inp1, q1, 0, hin1, win1, R, R1);
     if constexpr (!VEC) {
         const Div dci(a.cin), dk(a.kx);
         for (int kk = threadIdx.x; kk < kk_total; kk += 256) {
@@ -636,6 +655,13 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
             dtw1.qr(m - n0, y, x);
         else
             dtw.qr(l0 + m, y, x);
+    };
+    // output (y, x) of segment seg's fragment: inside its true size (Eqs. 3-4)
+    auto write_ok = [&](int seg, int y, int x) {
+        [[maybe_unused]] const int hh = (seg ? hin1 : hin) - a.ky + 1 - a.dbg_shrink,
+                                   ww = (seg ? win1 : win) - a.kx + 1 - a.dbg_shrink;
+        return FS_DBG_OK(a.dbg, (seg ? q1 : q) < a.nfrag && y < hh && x < ww && y < a.out_h && x < a.out_w,
+                         DBG_CONV_WRITE);
     };
     int abase[MB];
 #pragma unroll
@@ -990,6 +1016,18 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
             const size_t qc = cbase + (size_t)(fy * kpy + oy) * Qc + (fx * kpx + ox);
             return reinterpret_cast<TC *>(a.out) + (qc * child_px + (size_t)ybar * a.pool_ow + xbar) * a.cout;
         };
+        // filter value (y0 + r, c0 + c) lies inside its child (size (s - o) div k
+        // per axis of a parent of s, Eqs. 6-7) and the child batch
+        auto child_ok = [&](int r, int c) {
+            int ybar, oy, xbar, ox;
+            dky.qr(y0 + r, ybar, oy);
+            dkx.qr(c0 + c, xbar, ox);
+            [[maybe_unused]] const int hc = (hin - a.ky + 1 - oy) / kpy - a.dbg_shrink,
+                                       wc = (win - a.kx + 1 - ox) / kpx - a.dbg_shrink;
+            return FS_DBG_OK(a.dbg,
+                             q < a.nfrag && ybar < hc && xbar < wc && ybar < a.pool_oh && xbar < a.pool_ow,
+                             DBG_FUSED_POOL);
+        };
         if ((a.cout % TPAD) == 0) {
             // A thread owns one 16-byte channel chunk v of one filter column
             // c and walks a run of consecutive filter rows, so its LDS source
@@ -1027,12 +1065,12 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                         }
                         return m;
                     };
-                    auto put = [&](u4 m) {
+                    auto put = [&](u4 m, int r) {
                         if constexpr (BF) {
 #pragma unroll
                             for (int e = 0; e < 4; ++e) m[e] = bf16x2_key(m[e]);
                         }
-                        *reinterpret_cast<u4 *>(dst) = m;
+                        if (child_ok(r, c)) *reinterpret_cast<u4 *>(dst) = m;
                         if (++oy == KY) {
                             oy = 0;
                             dst += d_yb - (KY - 1) * d_oy;
@@ -1064,7 +1102,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                             u4 m = hr[0];
 #pragma unroll
                             for (int i = 1; i < KC; ++i) m = vmax(m, hr[i]);
-                            put(m);
+                            put(m, r);
 #pragma unroll
                             for (int i = 0; i + 1 < KC; ++i) hr[i] = hr[i + 1];
                             src += rstep;
@@ -1075,7 +1113,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                             for (int i = 0; i < KY; ++i)
                                 for (int j = 0; j < KX; ++j)
                                     m = vmax(m, *reinterpret_cast<const u4 *>(src + __mul24(__mul24(i, ew) + j, TS)));
-                            put(m);
+                            put(m, r);
                             src += ew * TS;
                         }
                     }
@@ -1105,7 +1143,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                             m = fmaxf(m, x);
                     }
                 if constexpr (BF) m = (TC)bf16x2_key(m);
-                child_ptr(r, c)[ch] = m;
+                if (child_ok(r, c)) child_ptr(r, c)[ch] = m;
             }
         }
         return;
@@ -1133,6 +1171,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                 dnv.qr(idx, m, v);
                 locate(m, seg, y, x);
                 x += c0;
+                if (!write_ok(seg, y, x)) continue;
                 *reinterpret_cast<u4 *>((seg ? outp1 : outp) + (y * orow + __mul24(x, a.cout) + v * TPAD)) =
                     *reinterpret_cast<const u4 *>(tile + __mul24(m, TS) + v * TPAD);
             }
@@ -1143,6 +1182,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
                 dnc.qr(idx, m, c);
                 locate(m, seg, y, x);
                 x += c0;
+                if (!write_ok(seg, y, x)) continue;
                 (seg ? outp1 : outp)[y * orow + __mul24(x, a.cout) + c] = tile[__mul24(m, TS) + c];
             }
         }
@@ -1163,6 +1203,7 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
         int seg, y, x;
         locate(m, seg, y, x);
         x += c0;
+        if (!write_ok(seg, y, x)) continue;
         TC *px = (seg ? outp1 : outp) + (y * orow + __mul24(x, a.cout));
         if constexpr (PAIRED) {
 #pragma unroll

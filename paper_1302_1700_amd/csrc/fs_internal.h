@@ -34,6 +34,40 @@ constexpr size_t kMaxLdsBytes = 160 * 1024;  // LDS of one CDNA4 compute unit
 constexpr int kMaxChannels = 16384;           // per layer (kernels divide by channel counts below 2^16)
 constexpr int kMaxFusedClasses = 4;   // classes of a last layer fused into a conv epilogue
 
+// Bounds checks (debug builds: compiled with -DFRAGSCAN_DEBUG into
+// libfragscan_debug.so).  Every fragment read and write of the kernels is
+// checked against the true size of its fragment (the per-axis tables, or
+// Eqs. 6-7 for a pool's children) and its buffer's batch and row pitch, every
+// output-map write against the map.  A failed check sets bit `site` of the
+// launch's status word (`dbg`, device memory the host clears before a scan
+// and reads after it) and skips the access, so the kernel still ends
+// normally; the scan then returns FS_ERR_BOUNDS naming the sites.  A launch's
+// `dbg_shrink` (0 unless forced from the host to test that path) is taken
+// off every true size the checks use.  Release builds compile the checks out.
+enum DbgSite {
+    DBG_CONV_READ = 0,     // convolution: input window
+    DBG_CONV_WEIGHT = 1,   // convolution: weight / bias blocks of the tile
+    DBG_CONV_WRITE = 2,    // convolution: output fragment
+    DBG_FUSED_POOL = 3,    // convolution + pool: child fragment
+    DBG_FUSED_HEAD = 4,    // convolution + last layer: output map
+    DBG_POOL_READ = 5,     // pool: parent fragment
+    DBG_POOL_WRITE = 6,    // pool: child fragment
+    DBG_HEAD_READ = 7,     // head: final fragment
+    DBG_HEAD_WRITE = 8,    // head: output map
+    DBG_PAD_READ = 9,      // mirror pad: image
+    DBG_NSITES = 10
+};
+#ifdef FRAGSCAN_DEBUG
+__device__ __forceinline__ bool dbg_check(unsigned *word, bool ok, int site)
+{
+    if (!ok) atomicOr(word, 1u << site);
+    return ok;
+}
+#define FS_DBG_OK(word, cond, site) ::fs::dbg_check((word), (cond), (site))
+#else
+#define FS_DBG_OK(word, cond, site) true
+#endif
+
 enum ActKind { ACT_NONE = 0, ACT_TANH = 1, ACT_SOFTMAX = 2 };
 enum DType { DT_F32 = 0, DT_BF16 = 1 };
 
@@ -105,6 +139,8 @@ struct ConvArgs {
     float *head_out;      // [B][ny][nx][head_ncls] (ny, nx: the output map's rows and row pitch)
     int ny, nx, Sy, Sx;       // Sy, Sx: products of the pools' row / column sizes
     uint16_t base_y[kMaxAxis], base_x[kMaxAxis];  // per-axis fragment index -> its first output coordinate
+    unsigned *dbg;            // debug builds: status word of the bounds checks
+    int dbg_shrink;
 };
 // Passed by value: the launch arguments of one dispatch (4 KiB at most).
 static_assert(sizeof(ConvArgs) <= 4096, "ConvArgs must stay within the kernel-argument limit");
@@ -120,6 +156,8 @@ struct PoolArgs {
     int n_children;      // B * F * sy * sx
     int rows;            // row-band kernel: filter rows per thread (4 or 8)
     AxisTable ext;       // true sizes of the parents
+    unsigned *dbg;       // debug builds: status word of the bounds checks
+    int dbg_shrink;
 };
 
 // Last stage: (optionally) the last 1x1 layer, its activation, and the
@@ -135,6 +173,9 @@ struct HeadArgs {
     int out_ny, out_nx;  // the output map's rows and row pitch (>= ny, nx)
     int Sy, Sx;          // products of the pools' row / column sizes
     uint16_t digit_y[kMaxAxis], digit_x[kMaxAxis];  // output coordinate mod S -> per-axis fragment index
+    AxisTable ext;       // true sizes of the final fragments (for the bounds checks)
+    unsigned *dbg;       // debug builds: status word of the bounds checks
+    int dbg_shrink;
 };
 
 // Launchers (return hipSuccess or the launch error).  `dtype` selects the
@@ -149,7 +190,7 @@ hipError_t launch_pool(const PoolArgs &a, int dtype, bool in_f32, int grid, hipS
 // (y, x) reading image pixel (mirror(y - p0y, H), mirror(x - p0x, W)).
 enum BorderMode { BORDER_VALID = 0, BORDER_REFLECT = 1, BORDER_SYMMETRIC = 2 };
 hipError_t launch_mirror_pad(const float *in, float *out, int B, int H, int W, int C, int p0y, int p0x, int He,
-                             int We, int mode, hipStream_t s);
+                             int We, int mode, unsigned *dbg, int dbg_shrink, hipStream_t s);
 hipError_t launch_head(const HeadArgs &a, int dtype, bool in_f32, bool has_fc, int grid,
                        hipStream_t s);
 // The float32 4 x 13 x 1 x 1 vector-path tile (conv_f32_wide.hip; no run

@@ -93,6 +93,13 @@ __global__ __launch_bounds__(256) void head_softmax_reassemble(HeadArgs a)
         }
         const int fy = a.digit_y[ym], fx = a.digit_x[xm];
         const size_t q = (size_t)b * a.F + (size_t)fy * a.Qx + fx;
+        // the fragment pixel lies inside its final fragment, the window inside the map
+        if (!FS_DBG_OK(a.dbg,
+                       b < a.B && yf < a.ext.y[fy] - a.dbg_shrink && xf < a.ext.x[fx] - a.dbg_shrink && yf < a.in_h &&
+                           xf < a.in_w,
+                       DBG_HEAD_READ))
+            continue;
+        if (!FS_DBG_OK(a.dbg, Y < a.ny && X < a.nx && Y < a.out_ny && X < a.out_nx, DBG_HEAD_WRITE)) continue;
         const TI *src = reinterpret_cast<const TI *>(a.in) + ((q * a.in_h + yf) * a.in_w + xf) * a.C;
 
         float z[kMaxHeadClasses];

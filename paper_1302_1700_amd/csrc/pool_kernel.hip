@@ -73,9 +73,18 @@ __global__ __launch_bounds__(256) void pool_frag(PoolArgs a)
 
     const int nv = a.C / V;
     const int total = wc * nv;
+    [[maybe_unused]] const int nparents = a.n_children / kk;
     for (int idx = threadIdx.x; idx < total; idx += 256) {
         const int xbar = idx / nv;
         const int cv = idx - xbar * nv;
+        // the window's last parent row and column lie inside the parent's
+        // true size; the child pixel inside the child's storage
+        [[maybe_unused]] const int ly = oy + a.sy * ybar + a.ky - 1, lx = ox + a.sx * xbar + a.kx - 1;
+        if (!FS_DBG_OK(a.dbg, p < nparents && ly < hp - a.dbg_shrink && lx < wp - a.dbg_shrink && ly < a.in_h &&
+                                  lx < a.in_w, DBG_POOL_READ))
+            continue;
+        if (!FS_DBG_OK(a.dbg, child < (size_t)a.n_children && ybar < a.out_h && xbar < a.out_w, DBG_POOL_WRITE))
+            continue;
         const size_t base = (size_t)(ox + a.sx * xbar) * a.C + cv * V;
         float m[V];
 #pragma unroll
@@ -154,6 +163,11 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int nbands, in
     const int y0 = band * RB;
     const int yend = min(y0 + RB, hp - K + 1);  // M rows [y0, yend)
     if (x > wp - K || y0 >= yend) return;
+    // the parent rows and columns the thread reads lie inside the parent's true size
+    [[maybe_unused]] const int lastrow = min(y0 + RB + K - 2, hp - 1), lastcol = x + K - 1;
+    if (!FS_DBG_OK(a.dbg, p < a.n_children / (K * K) && lastrow < hp - a.dbg_shrink && lastcol < wp - a.dbg_shrink &&
+                              lastrow < a.in_h && lastcol < a.in_w, DBG_POOL_READ))
+        return;
 
     const TI *src = reinterpret_cast<const TI *>(a.in) + (size_t)p * a.in_h * a.in_w * a.C + (size_t)x * a.C + cv * V;
     const size_t prow = (size_t)a.in_w * a.C;
@@ -218,6 +232,12 @@ __global__ __launch_bounds__(256) void pool_frag_rows(PoolArgs a, int nbands, in
         }
         const int oy = y % K, ybar = y / K;
         const size_t child = cbase + (size_t)(fy * K + oy) * Qc + (fx * K + ox);
+        // inside the child: (s - o) div K pixels per axis of a parent of s (Eqs. 6-7)
+        if (!FS_DBG_OK(a.dbg,
+                       child < (size_t)a.n_children && ybar < (hp - oy) / K - a.dbg_shrink &&
+                           xbar < (wp - ox) / K - a.dbg_shrink && ybar < a.out_h && xbar < a.out_w,
+                       DBG_POOL_WRITE))
+            continue;
         TO *d = out + ((child * a.out_h + ybar) * a.out_w + xbar) * a.C + cv * V;
         if constexpr (V == 1) {
             if constexpr (BF) d[0] = f2bf(m[0]); else d[0] = m[0];

@@ -13,8 +13,11 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libfragscan.so")
+# the same library with the kernels' bounds checks compiled in (FS_ERR_BOUNDS)
+LIB_DEBUG_PATH = os.path.join(_HERE, "libfragscan_debug.so")
 
-FS_OK, FS_ERR_INVALID_ARG, FS_ERR_SHAPE, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE, FS_ERR_OOM, FS_ERR_HIP = range(7)
+(FS_OK, FS_ERR_INVALID_ARG, FS_ERR_SHAPE, FS_ERR_UNSUPPORTED, FS_ERR_WORKSPACE, FS_ERR_OOM, FS_ERR_HIP,
+ FS_ERR_BOUNDS) = range(8)
 KIND = {"conv": 0, "pool": 1, "fc": 2}
 ACT = {"none": 0, "tanh": 1, "softmax": 2}
 DTYPE = {"f32": 0, "bf16": 1}
@@ -59,18 +62,19 @@ EXPORTS = ["fs_net_create", "fs_net_create_plan_only", "fs_net_destroy", "fs_net
            "fs_status_str", "fs_last_error", "fs_scan_plan_border", "fs_scan_border",
            "fs_scan_plan_tiled", "fs_scan_tiled", "fs_scan_noalloc"]
 
-_lib = None
+_libs = {}
 
 
-def load():
-    """Load libfragscan.so; raises if it has not been built (no fallback)."""
-    global _lib
-    if _lib is not None:
-        return _lib
-    if not os.path.exists(LIB_PATH):
-        raise RuntimeError("libfragscan.so is not built (%s); run __graft_entry__.build() or "
-                           "python paper_1302_1700_amd/build.py" % LIB_PATH)
-    lib = ctypes.CDLL(LIB_PATH)
+def load(debug=False):
+    """Load libfragscan.so (debug=True: libfragscan_debug.so); raises if it
+    has not been built (no fallback)."""
+    if debug in _libs:
+        return _libs[debug]
+    path = LIB_DEBUG_PATH if debug else LIB_PATH
+    if not os.path.exists(path):
+        raise RuntimeError("%s is not built; run __graft_entry__.build() or "
+                           "python paper_1302_1700_amd/build.py" % path)
+    lib = ctypes.CDLL(path)
     P, I32, SZ, VP = ctypes.POINTER, ctypes.c_int32, ctypes.c_size_t, ctypes.c_void_p
     sig = {
         "fs_net_create": [P(fs_layer), I32, I32, I32, I32, P(VP)],
@@ -98,13 +102,13 @@ def load():
     lib.fs_net_destroy.restype = None
     lib.fs_status_str.restype = ctypes.c_char_p
     lib.fs_last_error.restype = ctypes.c_char_p
-    _lib = lib
+    _libs[debug] = lib
     return lib
 
 
-def _check(st):
+def _check(st, lib=None):
     if st != FS_OK:
-        lib = load()
+        lib = lib or load()
         raise FsError(st, lib.fs_last_error().decode())
 
 
@@ -155,11 +159,13 @@ class Net:
     params : per layer (weight OIHW float32, bias float32) or None for pools
     in_channels, patch (0 = derive), dtype "f32" | "bf16".
     Created on the current HIP device; plan_only=True makes a host-only handle
-    for planning and index queries (no device needed, cannot scan).
+    for planning and index queries (no device needed, cannot scan); debug=True
+    loads the net into libfragscan_debug.so, whose kernels check every fragment
+    access (a failed check raises FsError with status FS_ERR_BOUNDS).
     """
 
-    def __init__(self, layers, params, in_channels, patch=0, dtype="f32", plan_only=False):
-        lib = load()
+    def __init__(self, layers, params, in_channels, patch=0, dtype="f32", plan_only=False, debug=False):
+        lib = self._lib = load(debug)
         self._keep = []
         arr = (fs_layer * len(layers))()
         for i, (L, p) in enumerate(zip(layers, params)):
@@ -179,12 +185,12 @@ class Net:
                 arr[i].bias = b.ctypes.data if b is not None else None
         h = ctypes.c_void_p()
         create = lib.fs_net_create_plan_only if plan_only else lib.fs_net_create
-        _check(create(arr, len(layers), int(in_channels), int(patch), DTYPE[dtype], ctypes.byref(h)))
+        _check(create(arr, len(layers), int(in_channels), int(patch), DTYPE[dtype], ctypes.byref(h)), self._lib)
         self._h = h
         self._keep = None
         self._ws = {}
         info = fs_net_info()
-        _check(lib.fs_net_query(self._h, ctypes.byref(info)))
+        _check(lib.fs_net_query(self._h, ctypes.byref(info)), self._lib)
         self.info = {n: getattr(info, n) for n, _ in fs_net_info._fields_}
         self.patch = self.info["patch"]      # window rows h_0
         self.patch_x = self.info["patch_x"]  # window columns w_0
@@ -192,7 +198,7 @@ class Net:
 
     def close(self):
         if getattr(self, "_h", None):
-            load().fs_net_destroy(self._h)
+            self._lib.fs_net_destroy(self._h)
             self._h = None
 
     def __del__(self):
@@ -205,15 +211,15 @@ class Net:
     def plan(self, B, H, W, border="valid"):
         p = fs_plan_info()
         if border == "valid":
-            _check(load().fs_scan_plan(self._h, B, H, W, ctypes.byref(p)))
+            _check(self._lib.fs_scan_plan(self._h, B, H, W, ctypes.byref(p)), self._lib)
         else:
-            _check(load().fs_scan_plan_border(self._h, B, H, W, BORDER[border], ctypes.byref(p)))
+            _check(self._lib.fs_scan_plan_border(self._h, B, H, W, BORDER[border], ctypes.byref(p)), self._lib)
         return {n: getattr(p, n) for n, _ in fs_plan_info._fields_}
 
     def launches(self, B, H, W):
         n = self.plan(B, H, W)["n_launches"]
         arr = (fs_launch_info * n)()
-        _check(load().fs_scan_launches(self._h, B, H, W, arr, n))
+        _check(self._lib.fs_scan_launches(self._h, B, H, W, arr, n), self._lib)
         out = []
         for a in arr:
             d = {n_: getattr(a, n_) for n_, _ in fs_launch_info._fields_}
@@ -222,29 +228,30 @@ class Net:
         return out
 
     def fragment_table(self, H, W):
-        lib = load()
+        lib = self._lib
         need = ctypes.c_size_t()
-        _check(lib.fs_fragment_table(self._h, H, W, None, 0, ctypes.byref(need)))
+        _check(lib.fs_fragment_table(self._h, H, W, None, 0, ctypes.byref(need)), self._lib)
         buf = np.zeros(need.value, np.int32)
         _check(lib.fs_fragment_table(self._h, H, W, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                                     need.value, None))
+                                     need.value, None), self._lib)
         rec = 5 + 2 * self.info["n_pools"]
         return buf.reshape(-1, rec)
 
     def reassembly_index(self, H, W):
-        lib = load()
+        lib = self._lib
         need = ctypes.c_size_t()
-        _check(lib.fs_reassembly_index(self._h, H, W, None, 0, ctypes.byref(need)))
+        _check(lib.fs_reassembly_index(self._h, H, W, None, 0, ctypes.byref(need)), self._lib)
         buf = np.zeros(need.value, np.int32)
         _check(lib.fs_reassembly_index(self._h, H, W, buf.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
-                                       need.value, None))
+                                       need.value, None), self._lib)
         return buf.reshape(H - self.patch + 1, W - self.patch_x + 1, 3)
 
     # -- scanning --------------------------------------------------------------
     def plan_tiled(self, B, H, W, tile):
         """Plan of scan_tiled with output tiles of tile = (rows, cols) windows."""
         p = fs_plan_info()
-        _check(load().fs_scan_plan_tiled(self._h, B, H, W, int(tile[0]), int(tile[1]), ctypes.byref(p)))
+        _check(self._lib.fs_scan_plan_tiled(self._h, B, H, W, int(tile[0]), int(tile[1]), ctypes.byref(p)),
+                                            self._lib)
         return {n: getattr(p, n) for n, _ in fs_plan_info._fields_}
 
     def workspace(self, B, H, W, device=None, border="valid", tile=None):
@@ -274,13 +281,13 @@ class Net:
             out = torch.empty((B, oh, ow, self.n_classes), dtype=torch.float32, device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, border)
         if border == "valid":
-            _check(load().fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
-                                  ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                  _nbytes(ws), _stream_handle(stream)))
+            _check(self._lib.fs_scan(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                     ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                     _nbytes(ws), _stream_handle(stream)), self._lib)
         else:
-            _check(load().fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
-                                         ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                         _nbytes(ws), _stream_handle(stream)))
+            _check(self._lib.fs_scan_border(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, BORDER[border],
+                                            ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                            _nbytes(ws), _stream_handle(stream)), self._lib)
         return out
 
     def scan_noalloc(self, image, out, stream=None):
@@ -294,8 +301,8 @@ class Net:
         if out is None:
             raise ValueError("scan_noalloc writes into a given output tensor")
         check_tensors(image, out, None, self.info["in_channels"], shape)
-        _check(load().fs_scan_noalloc(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
-                                      ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)))
+        _check(self._lib.fs_scan_noalloc(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                         ctypes.c_void_p(out.data_ptr()), _stream_handle(stream)), self._lib)
         return out
 
     def scan_tiled(self, image, tile, out=None, workspace=None, stream=None):
@@ -311,9 +318,9 @@ class Net:
         if out is None:
             out = torch.empty(shape, dtype=torch.float32, device=image.device)
         ws = workspace if workspace is not None else self.workspace(B, H, W, image.device, tile=tile)
-        _check(load().fs_scan_tiled(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, int(tile[0]), int(tile[1]),
-                                    ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), _nbytes(ws),
-                                    _stream_handle(stream)))
+        _check(self._lib.fs_scan_tiled(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W, int(tile[0]), int(tile[1]),
+                                       ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()), _nbytes(ws),
+                                       _stream_handle(stream)), self._lib)
         return out
 
     def profile(self, image, reps=10, out=None, stream=None):
@@ -331,7 +338,7 @@ class Net:
         ws = self.workspace(B, H, W, image.device)
         n = self.plan(B, H, W)["n_launches"]
         ms = (ctypes.c_float * n)()
-        _check(load().fs_scan_profile(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
-                                      ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
-                                      _nbytes(ws), _stream_handle(stream), reps, ms, n))
+        _check(self._lib.fs_scan_profile(self._h, ctypes.c_void_p(image.data_ptr()), B, H, W,
+                                         ctypes.c_void_p(out.data_ptr()), ctypes.c_void_p(ws.data_ptr()),
+                                         _nbytes(ws), _stream_handle(stream), reps, ms, n), self._lib)
         return list(ms)

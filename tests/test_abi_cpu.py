@@ -380,9 +380,33 @@ def test_scan_argument_checks_without_device():
 
 
 def test_status_strings():
-    lib = fsb.load()
-    for s in range(7):
-        assert lib.fs_status_str(s)
+    for debug in (False, True):
+        lib = fsb.load(debug)
+        strs = [lib.fs_status_str(s) for s in range(fsb.FS_ERR_BOUNDS + 1)]
+        assert all(strs) and len(set(strs)) == len(strs)
+        assert b"bounds" in strs[fsb.FS_ERR_BOUNDS]
+
+
+def test_debug_library_exports_and_plans():
+    """libfragscan_debug.so (the same sources with the kernels' bounds checks
+    compiled in) exports every declared entry point and plans the workload
+    nets and random nets launch for launch as the release library does."""
+    lib = fsb.load(debug=True)
+    for n in _header_functions():
+        assert hasattr(lib, n), n
+    cases = [(w.layers, w.channels, w.dtype, w.batch, w.height, w.width) for w in wl.WORKLOADS.values()]
+    for seed in range(6):
+        rng = np.random.default_rng(400 + seed)
+        layers, w0, c0 = wl.random_net(rng, max_c=40)
+        cases.append((layers, c0, "bf16" if seed % 2 else "f32", 2, w0 + 37, w0 + 23))
+    for layers, c0, dt, B, H, W in cases:
+        params = wl.make_weights(layers, 0, 0.1)
+        plans = []
+        for debug in (False, True):
+            net = fsb.Net(layers, params, c0, 0, dt, plan_only=True, debug=debug)
+            plans.append((net.plan(B, H, W), net.launches(B, H, W)))
+            net.close()
+        assert plans[0] == plans[1]
 
 
 def test_bench_cpu_fragment_leg():
