@@ -67,7 +67,10 @@ typedef enum {
     FS_ERR_HIP = 6,          /* a HIP runtime call failed */
     FS_ERR_BOUNDS = 7        /* debug library only (libfragscan_debug.so): a kernel's
                               * bounds check failed; fs_last_error names the checks.
-                              * The scan skipped those accesses: its output is not valid */
+                              * The scan skipped those accesses: its output is not valid.
+                              * Its scans synchronise their stream, and scans that overlap
+                              * on one device share one status word (a failure may be
+                              * reported by any of them) */
 } fs_status;
 
 /* Layer kinds (Section 2: input, convolutional, max-pooling and fully
