@@ -498,7 +498,15 @@ __global__ __launch_bounds__(256, (!BF && NB == 1 && MB <= 4) ? 6 : 1) void conv
         // with at most one carry into the next row per step.  UN loads are
         // in flight per thread before their LDS stores.
         auto walk = [&](int nvec, int width, auto load) {
-            constexpr int UN = 8;
+            // Loads in flight per thread before their LDS stores: two for the
+            // float32 tiles of three or more channel blocks whose waves split
+            // the channels or the K steps in two (FC1's 7 x 2 and the split-K
+            // 4 x 3 of 48 -> 48 layers), whose window staging runs beside
+            // the K walk of another resident workgroup and delays its weight
+            // loads less that way (N4 on 8 x 1024^2: FC1 + head 1.4% and the
+            // 48 -> 48 layers up to 0.9% faster than with eight); eight for
+            // the rest, where two measured 3-4% slower.
+            constexpr int UN = (!BF && VEC && NB >= 3 && (WN == 2 || WK == 2)) ? 2 : 8;
             const int P = 256 / nvec;
             int p, v;
             Div(nvec).qr(threadIdx.x, p, v);
