@@ -77,6 +77,16 @@ def test_workload_nets(fsb, wid, B, H, W):
     assert np.abs(got - ref).max() <= TOL[w.dtype]
 
 
+@pytest.mark.parametrize("wid", [2, 3, 4, 5])
+def test_workload_nets_full_size(fsb, wid):
+    """The benchmarked configurations at their full sizes (the grids of many
+    rounds, the batch offsets and the tiles the planner picks only there):
+    every check passes and the map is the release library's bit for bit."""
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid)
+    _same(fsb, w.layers, params, img, w.channels, w.dtype)
+
+
 @pytest.mark.parametrize("seed", range(4))
 def test_random_nets(fsb, seed):
     rng = np.random.default_rng(7000 + seed)
