@@ -215,6 +215,24 @@ def test_workload2_full_map_cpu_fragment(fsb):
     assert np.abs(got - ref).max() <= TOL["f32"]
 
 
+@pytest.mark.parametrize("wid", [3, 4, 5])
+def test_workload_full_map_dilated(fsb, wid):
+    """Full-size benchmarked configurations, every output of the map against
+    the whole-image formulation with dilated library convolutions and
+    max-pools (float64, torch CPU; pinned to the per-patch definition by the
+    oracle tests): workloads 3 and 5 whole, workload 4's first and last image
+    of its batch of eight (~8 s of CPU per 1024^2 image)."""
+    from helpers import dilated_scan
+    w = wl.WORKLOADS[wid]
+    params, img = wl.workload_inputs(wid)
+    got = _scan(fsb, w.layers, params, img, w.channels, 0, w.dtype)
+    for b in sorted({0, w.batch - 1}):
+        print("full map vs dilated formulation", wid, "image", b, flush=True)
+        ref = dilated_scan(w.layers, params, img[b:b + 1])
+        assert got[b:b + 1].shape == ref.shape
+        assert np.abs(got[b:b + 1] - ref).max() <= TOL[w.dtype], b
+
+
 def test_workload3_logits(fsb):
     """Workload 3's probabilities sit within 1e-3 of 1/2, so also compare the
     logits (last layer without softmax) on a relative scale."""
