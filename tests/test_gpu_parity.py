@@ -233,6 +233,32 @@ def test_workload_full_map_dilated(fsb, wid):
         assert np.abs(got[b:b + 1] - ref).max() <= TOL[w.dtype], b
 
 
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+def test_image_side_limit(fsb, dt):
+    """Images whose width or height is 65,535, the largest side a scan takes
+    (fragment sizes travel in 16-bit tables): the tiny workload net (small-K
+    first layer) and a matrix-core net, the whole map against the dilated
+    whole-image formulation and sampled windows against the per-patch
+    oracle."""
+    from helpers import dilated_scan
+    nets = [(wl.WORKLOADS[1].layers, 1),
+            ([wl.conv(2, 3, 32), wl.pool(2, 32), wl.conv(2, 32, 32), wl.pool(2, 32), wl.fc(2, 32, 16),
+              wl.fc(1, 16, 2, "softmax")], 3)]
+    for n, (layers, c0) in enumerate(nets):
+        w0 = ix.patch_size(layers)
+        params = wl.make_weights(layers, 120 + n, 0.3)
+        for H, W in ((w0 + 5, 65535), (65535, w0 + 3)):
+            img = wl.make_image(130 + n, 1, H, W, c0)
+            print("side limit", dt, n, (H, W), flush=True)
+            got = _scan(fsb, layers, params, img, c0, dtype=dt)
+            ref = dilated_scan(layers, params, img)
+            assert got.shape == ref.shape == (1, H - w0 + 1, W - w0 + 1, 2)
+            assert np.abs(got - ref).max() <= TOL[dt], (n, H, W)
+            pts = _sample_patches(layers, 1, H, W, 64, 140 + n)
+            ref_p = oracle.patch_forward(layers, params, img, w0, pts)
+            assert np.abs(got[pts[:, 0], pts[:, 1], pts[:, 2]] - ref_p).max() <= TOL[dt], (n, H, W)
+
+
 def test_workload3_logits(fsb):
     """Workload 3's probabilities sit within 1e-3 of 1/2, so also compare the
     logits (last layer without softmax) on a relative scale."""
