@@ -174,7 +174,12 @@ typedef struct {
  * whose window is h_0 x w_0 with h_0 != w_0, must pass 0 and give its fully
  * connected sizes).  A patch that does
  * not agree with the stack gives FS_ERR_SHAPE; more than 16384 channels in a
- * layer gives FS_ERR_UNSUPPORTED.  Weights are converted (and
+ * layer gives FS_ERR_UNSUPPORTED.  A convolution stages its input window with
+ * all of its input channels in the 160 KB of LDS, so planning a scan
+ * (fs_scan_plan and the scans) gives FS_ERR_UNSUPPORTED for a layer with more
+ * input channels than a minimal window holds: about 150 (float32, 5 x 5
+ * kernel), 245 (3 x 3), 320 (2 x 2), 440 (1 x 1); bfloat16 265, 450, 610, 860.
+ * Weights are converted (and
  * for FS_BF16 rounded) and uploaded to the current HIP device, which the net
  * is then bound to.  On success *out receives the handle. */
 fs_status fs_net_create(const fs_layer *layers, int32_t n_layers, int32_t in_channels,

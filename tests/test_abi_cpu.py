@@ -473,6 +473,37 @@ def test_image_side_limit():
     net.close()
 
 
+def _wide_layer_net(cin, k):
+    layers = [wl.conv(1, 1, cin, "none"), wl.conv(k, cin, 2), wl.fc(1, 2, 2, "softmax")]
+    params = [(np.zeros((L["c_out"], L["c_in"], L["k"], L["k"]), np.float32), np.zeros(L["c_out"], np.float32))
+              for L in layers]
+    return layers, params
+
+
+@pytest.mark.parametrize("dt,k,cmax", [("f32", 5, 153), ("f32", 3, 245), ("f32", 1, 438),
+                                       ("bf16", 5, 265), ("bf16", 3, 450), ("bf16", 1, 862)])
+def test_input_channel_limit(dt, k, cmax):
+    """A convolution's window holds all its input channels in LDS: the
+    largest input channel count a scan takes is planned, one more is refused
+    with FS_ERR_UNSUPPORTED (not scanned wrongly), and more than 16384
+    channels are refused when the net is created."""
+    for cin, fits in ((cmax, True), (cmax + 1, False)):
+        layers, params = _wide_layer_net(cin, k)
+        w0 = ix.patch_size(layers)
+        net = fsb.Net(layers, params, 1, 0, dt, plan_only=True)
+        if fits:
+            assert net.plan(1, w0 + 40, w0 + 40)["n_launches"] >= 2
+        else:
+            with pytest.raises(fsb.FsError) as e:
+                net.plan(1, w0 + 40, w0 + 40)
+            assert e.value.status == fsb.FS_ERR_UNSUPPORTED and "LDS" in str(e.value)
+        net.close()
+    layers, params = _wide_layer_net(16385, 1)
+    with pytest.raises(fsb.FsError) as e:
+        fsb.Net(layers, params, 1, 0, dt, plan_only=True)
+    assert e.value.status == fsb.FS_ERR_UNSUPPORTED
+
+
 def test_batch_and_grid_limits():
     """Batch times fragments stays below 2^24 (fragment indices), and a head
     with too many windows is refused instead of overflowing."""
