@@ -5,6 +5,8 @@ Tolerances (max abs on the outputs): float32 1e-4, bf16 (fp32 accumulate)
 Index work (which window lands where) is checked bit-exactly with
 position-encoding nets whose arithmetic is exact in both precisions.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -20,11 +22,27 @@ TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 @pytest.fixture(scope="module")
 def fsb():
+    """The binding; with FRAGSCAN_TEST_DEBUG=1 every net of these tests is
+    loaded into the bounds-checked library instead (a failed check then
+    raises FsError, so the whole suite doubles as a memory-safety run)."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_1302_1700_amd import fragscan
     fragscan.load()
-    return fragscan
+    if os.environ.get("FRAGSCAN_TEST_DEBUG") != "1":
+        return fragscan
+    fragscan.load(debug=True)
+
+    class Checked:
+        def __getattr__(self, name):
+            return getattr(fragscan, name)
+
+        @staticmethod
+        def Net(*args, **kw):
+            kw.setdefault("debug", True)
+            return fragscan.Net(*args, **kw)
+
+    return Checked()
 
 
 def _scan(fsb, layers, params, img, c0, patch=0, dtype="f32", poison=False):
